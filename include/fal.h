@@ -1,0 +1,197 @@
+/*
+ * fal.h -- C ABI of libfal.so: one training step (forward + backward) of a
+ * GPT-style Pre-LN decoder stack in three block architectures, on one
+ * MI355X (gfx950):
+ *
+ *   GPT   (Sec. 2, Eq. 1)  X_{i+1} = X_i + MHA_i(LN(X_i))
+ *                                   + MLP_i(LN(X_i + MHA_i(LN(X_i))))
+ *   FAL   (Sec. 4.1, Eq. 2) X_{i+1} = X_i + MHA_i(LN(X_i))
+ *                                   + MLP_i(LN(X_i) + LN(MHA_1(LN(X_1))))
+ *         The first-attention LayerNorm F = LN_F(MHA_1(LN(X_1))) is evaluated
+ *         once, in block 0, and read by every block (Sec. 4.1).
+ *   FAL+  (Sec. 5; Appendix D) block 0 is the GPT block; every later block
+ *         adds its own LayerNorm of the first attention output to the GPT
+ *         MLP input: MLP_i(LN(X_i + A_i) + LN_{F,i}(MHA_1(LN(X_1)))).
+ *
+ * MHA = QKV projection, causal scaled-dot-product attention per head,
+ * concatenation, output projection; MLP = up-projection, GELU (tanh form by
+ * default), down-projection (Sec. 2).  Biases on every linear layer, learned
+ * position embedding, final LayerNorm and an LM head tied to the token
+ * embedding (GPT-2 conventions).
+ *
+ * Conventions shared by every entry point
+ *  - All pointers marked "device" are HIP device pointers allocated by the
+ *    caller; the library never allocates device memory.  The caller owns
+ *    every buffer (parameters, gradients, tokens, outputs, workspace).
+ *  - Tensors are dense, row-major.  Activations are token-major [M, d] with
+ *    M = batch * seq_len (row m = b * seq_len + t).  Linear weights are stored
+ *    [in, out] so a layer computes y = x W + b.
+ *  - Parameters are stored in the config's dtype (fp32, or bf16); the
+ *    residual stream (x_in, x_out, dx_*) and every gradient are fp32.
+ *  - Work is enqueued asynchronously on the main stream given to fal_init.
+ *    With the STREAMS schedule the library forks work onto the aux stream
+ *    and joins back onto the main stream before the call returns.
+ *  - Errors: every call validates its arguments on the host before any
+ *    launch and returns a status; no call aborts.  The message of the last
+ *    failure is available from fal_last_error.  A context is used from one
+ *    host thread at a time.
+ *  - Results are deterministic: the same inputs give bitwise-identical
+ *    outputs run to run, and the SEQ and STREAMS schedules agree bitwise.
+ */
+#ifndef FAL_H
+#define FAL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FAL_OK = 0,
+  FAL_ERR_INVALID_ARG = 1, /* NULL pointer, bad size, bad enum value      */
+  FAL_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim)   */
+  FAL_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than required     */
+  FAL_ERR_HIP = 4,         /* a HIP runtime call or kernel launch failed  */
+  FAL_ERR_STATE = 5        /* call out of order (e.g. bwd before fwd)     */
+} fal_status_t;
+
+typedef enum { FAL_ARCH_GPT = 0, FAL_ARCH_FAL = 1, FAL_ARCH_FALPLUS = 2 } fal_arch_t;
+typedef enum { FAL_F32 = 0, FAL_BF16 = 1 } fal_dtype_t;
+
+/* How the two branches of a FAL block are issued (Sec. 4.2: in FAL a block's
+ * MHA and MLP have no dependency and may run concurrently).
+ *  SEQ     : one stream, branches back to back.
+ *  STREAMS : MHA branch on the main stream, MLP branch on the aux stream,
+ *            joined with HIP events (same kernels as SEQ).
+ *  MERGED  : the independent GEMMs of the two branches are issued as one
+ *            grouped launch, and FAL's output projection and down-projection
+ *            as one GEMM over the concatenated inner dimension.
+ * GPT and FAL+ blocks have no independent branches; the schedule only
+ * affects FAL blocks. */
+typedef enum { FAL_SCHED_SEQ = 0, FAL_SCHED_STREAMS = 1, FAL_SCHED_MERGED = 2 } fal_sched_t;
+
+typedef struct {
+  int32_t n_layer;        /* L >= 1                                           */
+  int32_t d_model;        /* d, multiple of 8                                 */
+  int32_t n_head;         /* heads held on this GPU                           */
+  int32_t head_dim;       /* 16, 32, 64 or 128                                */
+  int32_t d_ff;           /* FFN width f, multiple of 8                       */
+  int32_t vocab;          /* V (ignored when has_embed_head == 0)             */
+  int32_t seq_len;        /* T                                                */
+  int32_t batch;          /* B                                                */
+  int32_t arch;           /* fal_arch_t                                       */
+  int32_t dtype;          /* fal_dtype_t of parameters and saved activations  */
+  int32_t sched;          /* fal_sched_t                                      */
+  float ln_eps;           /* LayerNorm epsilon (GPT-2: 1e-5)                  */
+  int32_t gelu_tanh;      /* 1: tanh-approximate GELU, 0: erf GELU            */
+  int32_t has_embed_head; /* 1: embedding + final LN + tied head + CE loss;
+                             0: block stack only (fal_stack_step)             */
+} fal_config_t;
+
+/* Parameter tensors.  Global tensors (present only when has_embed_head):
+ *   WTE [V, d], WPE [T, d], LNF_G [d], LNF_B [d].
+ * Per-block tensors, identical layout in every block (dA = n_head*head_dim):
+ *   LN1_G [d] LN1_B [d] W_QKV [d, 3dA] B_QKV [3dA] W_O [dA, d] B_O [d]
+ *   LN2_G [d] LN2_B [d] W_FC [d, f] B_FC [f] W_2 [f, d] B_2 [d]
+ *   LNF1_G [d] LNF1_B [d]   first-attention LayerNorm: used by block 0 in FAL
+ *                           (the single LN_F) and by blocks >= 1 in FAL+
+ *                           (LN_{F,i}); unused slots get zero gradients.
+ * W_QKV's columns are [Q | K | V], each head h at columns h*head_dim. */
+enum {
+  FAL_P_WTE = 0, FAL_P_WPE, FAL_P_LNF_G, FAL_P_LNF_B, FAL_P_NGLOBAL
+};
+enum {
+  FAL_B_LN1_G = 0, FAL_B_LN1_B, FAL_B_W_QKV, FAL_B_B_QKV, FAL_B_W_O, FAL_B_B_O,
+  FAL_B_LN2_G, FAL_B_LN2_B, FAL_B_W_FC, FAL_B_B_FC, FAL_B_W_2, FAL_B_B_2,
+  FAL_B_LNF1_G, FAL_B_LNF1_B, FAL_B_NTENSOR
+};
+
+typedef struct fal_ctx fal_ctx_t; /* opaque */
+
+/* Host only; no GPU needed.  FAL_OK if the config is valid and supported. */
+fal_status_t fal_validate_config(const fal_config_t* cfg);
+
+/* Host only.  Element offsets of the parameter tensors inside one flat
+ * parameter buffer (the gradient buffer has the same layout, in fp32).
+ *   global_off[FAL_P_NGLOBAL]  offsets of the global tensors (-1 if absent)
+ *   block_off[FAL_B_NTENSOR]   offsets inside one block, relative to the
+ *                              block's start
+ *   block_base, block_stride   block i starts at block_base + i*block_stride
+ *   total                      number of elements of the whole buffer
+ * Every tensor starts at a multiple of 64 elements.  Any output pointer may
+ * be NULL. */
+fal_status_t fal_param_layout(const fal_config_t* cfg, int64_t* global_off, int64_t* block_off,
+                              int64_t* block_base, int64_t* block_stride, int64_t* total);
+
+/* Host only.  Bytes of device workspace fal_init needs for this config:
+ * saved activations of every block, the residual stream, the LM-head
+ * logits and the backward scratch. */
+fal_status_t fal_workspace_bytes(const fal_config_t* cfg, size_t* bytes);
+
+/* Creates a context bound to the current HIP device.  workspace: device
+ * buffer of at least fal_workspace_bytes bytes, 256-byte aligned, owned by
+ * the caller and kept alive until fal_destroy.  stream_main / stream_aux:
+ * hipStream_t handles (NULL means the default stream; aux may equal main).
+ * *out receives the context. */
+fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
+                      void* stream_main, void* stream_aux, fal_ctx_t** out);
+
+fal_status_t fal_destroy(fal_ctx_t* ctx);
+
+/* Forward of block `layer` (0-based).
+ *   block_params  device, dtype, one block in the FAL_B_* layout
+ *   x_in, x_out   device fp32 [M, d]; x_out = block output (may not alias x_in)
+ *   first_attn    device dtype [M, d].  FAL: block 0 writes F = LN_F(A_1),
+ *                 later blocks read it.  FAL+: block 0 writes the shared
+ *                 normalisation of A_1, later blocks read it.  GPT: ignored
+ *                 (may be NULL).
+ * Saves the activations block `layer`'s backward needs in the workspace. */
+fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
+                           const float* x_in, float* x_out, void* first_attn);
+
+/* Backward of block `layer`; requires fal_block_fwd(layer) of the same step.
+ *   x_in          device fp32 [M, d], the same input given to the forward
+ *   dx_out        device fp32 [M, d], gradient w.r.t. the block output
+ *   dx_in         device fp32 [M, d], receives the gradient w.r.t. x_in
+ *   d_first_attn  device fp32 [M, d] accumulator of the gradient w.r.t. the
+ *                 first-attention tensor (FAL: F; FAL+: the normalisation).
+ *                 Block n_layer-1 overwrites it, blocks below accumulate,
+ *                 block 0 consumes it.  GPT: ignored (may be NULL).
+ *   block_grads   device fp32, one block in the FAL_B_* layout, overwritten */
+fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
+                           const float* x_in, const float* dx_out, float* dx_in,
+                           float* d_first_attn, float* block_grads);
+
+/* One whole training step of the language model (has_embed_head == 1).
+ *   params  device, dtype, full layout of fal_param_layout
+ *   tokens  device int32 [B, T+1]; the model reads [:, :T] and predicts
+ *           [:, 1:]; ids must lie in [0, V) (out-of-range ids are clamped)
+ *   loss    device fp32 scalar: mean next-token cross-entropy over B*T
+ *   logits  device fp32 [B*T, V] or NULL to skip writing them
+ *   grads   device fp32, full layout, overwritten */
+fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* tokens,
+                            float* loss, float* logits, float* grads);
+
+/* One training step of a block stack without embedding or head
+ * (has_embed_head == 0): forward of every block from x_in, surrogate loss
+ * sum(dy * X_L) so the gradient entering the last block is dy, backward.
+ *   x_in   device fp32 [M, d]      dy   device fp32 [M, d]
+ *   loss   device fp32 scalar or NULL
+ *   grads  device fp32, full layout, overwritten
+ *   dx_in  device fp32 [M, d] or NULL: gradient w.r.t. x_in */
+fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_in,
+                            const float* dy, float* loss, float* grads, float* dx_in);
+
+/* Device pointer to the final block output X_L (fp32 [M, d]) held in the
+ * workspace after a step; valid until the next step. */
+fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);
+
+const char* fal_status_string(fal_status_t status);
+const char* fal_last_error(const fal_ctx_t* ctx); /* "" if none; ctx may be NULL */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FAL_H */

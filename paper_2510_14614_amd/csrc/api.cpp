@@ -1,0 +1,831 @@
+// C ABI of libfal.so (declared in include/fal.h): configuration checks,
+// parameter layout, workspace carve-up and the host-side schedule of one
+// training step of a GPT / FAL / FAL+ decoder stack.
+//
+// Block forward (Sec. 2 Eq. 1; Sec. 4.1 Eq. 2; Sec. 5 and Appendix D):
+//   GPT   : H1 = LN1(X); A = MHA(H1); Xm = X + A; H2 = LN2(Xm);
+//           Y = Xm + MLP(H2)
+//   FAL   : block 0: H1 = LN1(X); A_1 = MHA(H1); F = LN_F(A_1);
+//                    H2 = LN2(X) + F; Y = X + A_1 + MLP(H2)
+//           block i>0: one LayerNorm pass gives H1 = LN1(X) and
+//                    H2 = LN2(X) + F; then MHA(H1) and MLP(H2) are
+//                    independent (Sec. 4.2) and are issued concurrently:
+//                    SEQ     back to back on one stream,
+//                    STREAMS MHA on the main stream, MLP on the aux stream,
+//                    MERGED  QKV and FFN-up GEMMs as one grouped launch and
+//                            the output and down projections as one GEMM
+//                            over the concatenated inner dimension [O | G].
+//   FAL+  : block 0 is the GPT block and also saves xhatF = norm(A_1);
+//           block i>0: H2 = LN2(X + A) + gF_i * xhatF + bF_i.
+// The backward mirrors this; FAL's MLP and MHA backward chains are again
+// independent for i > 0 and meet in one LayerNorm backward that handles
+// both LayerNorms of X at once and accumulates dF.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/fal.h"
+#include "kernels.h"
+
+using namespace fal;
+
+namespace {
+
+constexpr int64_t kAlignElems = 64;
+constexpr size_t kAlignBytes = 256;
+
+int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+struct Dims {
+  int L, d, H, hd, dA, f, V, Vp, T, B, M;
+  size_t es;  // bytes per stored element
+};
+
+Dims dims_of(const fal_config_t& c) {
+  Dims D;
+  D.L = c.n_layer; D.d = c.d_model; D.H = c.n_head; D.hd = c.head_dim;
+  D.dA = c.n_head * c.head_dim; D.f = c.d_ff;
+  D.V = c.has_embed_head ? c.vocab : 0;
+  D.Vp = (int)align_up(D.V, 64);
+  D.T = c.seq_len; D.B = c.batch; D.M = c.batch * c.seq_len;
+  D.es = c.dtype == FAL_BF16 ? 2 : 4;
+  return D;
+}
+
+const char* validate(const fal_config_t* c) {
+  if (!c) return "config is NULL";
+  if (c->n_layer < 1) return "n_layer must be >= 1";
+  if (c->d_model < 8 || c->d_model % 8) return "d_model must be a positive multiple of 8";
+  if (c->d_model > 4096) return "d_model above 4096 is not supported";
+  if (c->n_head < 1) return "n_head must be >= 1";
+  if (c->d_ff < 8 || c->d_ff % 8) return "d_ff must be a positive multiple of 8";
+  if (c->seq_len < 1 || c->batch < 1) return "seq_len and batch must be >= 1";
+  if (c->arch < FAL_ARCH_GPT || c->arch > FAL_ARCH_FALPLUS) return "unknown arch";
+  if (c->dtype != FAL_F32 && c->dtype != FAL_BF16) return "unknown dtype";
+  if (c->sched < FAL_SCHED_SEQ || c->sched > FAL_SCHED_MERGED) return "unknown sched";
+  if (!(c->ln_eps > 0.f)) return "ln_eps must be > 0";
+  if (c->gelu_tanh != 0 && c->gelu_tanh != 1) return "gelu_tanh must be 0 or 1";
+  if (c->has_embed_head != 0 && c->has_embed_head != 1) return "has_embed_head must be 0 or 1";
+  if (c->has_embed_head) {
+    if (c->vocab < 1) return "vocab must be >= 1";
+    if (c->vocab > 65535) return "vocab above 65535 is not supported";
+    if ((int64_t)c->batch * c->seq_len > 16384) return "batch*seq_len above 16384 with an embedding is not supported";
+  }
+  if ((int64_t)c->batch * c->seq_len > (1 << 24)) return "batch*seq_len too large";
+  return nullptr;
+}
+
+bool unsupported(const char* why) {
+  return why && (strstr(why, "not supported") != nullptr);
+}
+
+const char* validate_hd(const fal_config_t* c) {
+  const int hd = c->head_dim;
+  if (hd != 16 && hd != 32 && hd != 64 && hd != 128) return "head_dim must be 16, 32, 64 or 128 (not supported otherwise)";
+  if ((c->n_head * hd) % 8) return "n_head*head_dim must be a multiple of 8 (not supported otherwise)";
+  return nullptr;
+}
+
+struct Layout {
+  int64_t goff[FAL_P_NGLOBAL];
+  int64_t boff[FAL_B_NTENSOR];
+  int64_t bsize[FAL_B_NTENSOR];
+  int64_t gsize[FAL_P_NGLOBAL];
+  int64_t block_base, block_stride, total;
+};
+
+Layout layout_of(const fal_config_t& c) {
+  const Dims D = dims_of(c);
+  Layout Lo;
+  int64_t off = 0;
+  const int64_t gs[FAL_P_NGLOBAL] = {(int64_t)D.V * D.d, (int64_t)D.T * D.d, D.d, D.d};
+  for (int i = 0; i < FAL_P_NGLOBAL; ++i) {
+    Lo.gsize[i] = c.has_embed_head ? gs[i] : 0;
+    if (c.has_embed_head) {
+      Lo.goff[i] = off;
+      off += align_up(gs[i], kAlignElems);
+    } else {
+      Lo.goff[i] = -1;
+    }
+  }
+  Lo.block_base = off;
+  const int64_t d = D.d, dA = D.dA, f = D.f;
+  const int64_t bs[FAL_B_NTENSOR] = {d, d, d * 3 * dA, 3 * dA, dA * d, d, d, d, d * f, f, f * d, d, d, d};
+  int64_t b = 0;
+  for (int i = 0; i < FAL_B_NTENSOR; ++i) {
+    Lo.boff[i] = b;
+    Lo.bsize[i] = bs[i];
+    b += align_up(bs[i], kAlignElems);
+  }
+  Lo.block_stride = b;
+  Lo.total = off + b * D.L;
+  return Lo;
+}
+
+// ------------------------------------------------------------ workspace --
+struct Carve {
+  char* base;
+  size_t off = 0;
+  template <typename T> T* take(int64_t n, size_t elem = sizeof(T)) {
+    off = (off + kAlignBytes - 1) / kAlignBytes * kAlignBytes;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += (size_t)n * elem;
+    return p;
+  }
+};
+
+struct LayerSlot {
+  float *mean1, *rstd1, *mean2, *rstd2;
+  void *h1, *h2, *qkv, *og, *pre;
+  float *lse, *xm;
+};
+
+struct Work {
+  LayerSlot* slots = nullptr;  // host array [L]
+  float *a1, *meanF, *rstdF;   // block 0 extras
+  float* resid;                // [L+1][M, d]
+  void* hf;
+  float *meanf, *rstdf;
+  float* logits;               // [M, Vp]
+  void* dlogits;               // [M, Vp]
+  float* row_loss;
+  void* first;                 // dtype [M, d]
+  float* dfirst;               // [M, d]
+  float *dxa, *dxb, *dxm, *da, *dh1, *dh2;
+  void *lp_a, *lp_b, *dxm_lp, *da_lp, *dog, *dqkv;
+  void* first_in;              // first-attention tensor of the current step
+  float* Dvec;
+  float *part_main, *part_aux;
+  int32_t* keys;
+  float* loss_tmp;
+};
+
+void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
+  const Dims D = dims_of(c);
+  Carve cv{base};
+  const int64_t M = D.M, d = D.d, es = (int64_t)D.es;
+  const bool need_xm = c.arch != FAL_ARCH_FAL;
+  for (int i = 0; i < D.L; ++i) {
+    LayerSlot s{};
+    s.mean1 = cv.take<float>(M);
+    s.rstd1 = cv.take<float>(M);
+    s.h1 = cv.take<char>(M * d * es);
+    s.h2 = cv.take<char>(M * d * es);
+    s.qkv = cv.take<char>(M * 3 * D.dA * es);
+    s.og = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
+    s.pre = cv.take<char>(M * D.f * es);
+    s.lse = cv.take<float>((int64_t)D.B * D.H * D.T);
+    if (need_xm || i == 0) {
+      s.xm = cv.take<float>(M * d);
+      s.mean2 = cv.take<float>(M);
+      s.rstd2 = cv.take<float>(M);
+    }
+    if (W.slots) W.slots[i] = s;
+  }
+  W.a1 = cv.take<float>(M * d);
+  W.meanF = cv.take<float>(M);
+  W.rstdF = cv.take<float>(M);
+  W.resid = cv.take<float>((int64_t)(D.L + 1) * M * d);
+  if (c.has_embed_head) {
+    W.hf = cv.take<char>(M * d * es);
+    W.meanf = cv.take<float>(M);
+    W.rstdf = cv.take<float>(M);
+    W.logits = cv.take<float>(M * D.Vp);
+    W.dlogits = cv.take<char>(M * D.Vp * es);
+    W.row_loss = cv.take<float>(M);
+    W.keys = cv.take<int32_t>(embed_bwd_scratch((int)M));
+  } else {
+    W.hf = nullptr; W.meanf = W.rstdf = nullptr; W.logits = nullptr; W.dlogits = nullptr;
+    W.row_loss = nullptr; W.keys = nullptr;
+  }
+  W.first = cv.take<char>(M * d * es);
+  W.dfirst = cv.take<float>(M * d);
+  W.dxa = cv.take<float>(M * d);
+  W.dxb = cv.take<float>(M * d);
+  W.dxm = cv.take<float>(M * d);
+  W.da = cv.take<float>(M * d);
+  W.dh1 = cv.take<float>(M * d);
+  W.dh2 = cv.take<float>(M * d);
+  W.lp_a = cv.take<char>(M * d * es);
+  W.lp_b = cv.take<char>(M * d * es);
+  W.dxm_lp = cv.take<char>(M * d * es);
+  W.da_lp = cv.take<char>(M * d * es);
+  W.dog = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
+  W.dqkv = cv.take<char>(M * 3 * D.dA * es);
+  W.Dvec = cv.take<float>((int64_t)D.B * D.H * D.T);
+  const int64_t wmax = std::max<int64_t>({3 * (int64_t)D.dA, (int64_t)D.f, d, 1});
+  const int64_t part = std::max<int64_t>({ln_bwd_scratch((int)M, (int)d), col_sum_scratch((int)M, (int)wmax),
+                                          dot_scratch(M * d)});
+  W.part_main = cv.take<float>(part);
+  W.part_aux = cv.take<float>(part);
+  W.loss_tmp = cv.take<float>(64);
+  W.first_in = W.first;
+  *total = cv.off + kAlignBytes;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------- context --
+struct fal_ctx {
+  fal_config_t cfg;
+  Dims D;
+  Layout Lo;
+  Work W;
+  char* ws;
+  size_t ws_bytes;
+  hipStream_t sm, sa;
+  hipEvent_t ev_fork, ev_join;
+  int device;
+  std::string err;
+  int fwd_done_mask_ok;
+};
+
+namespace {
+
+struct Fail {};
+
+#define FAL_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t _e = (expr);                                                        \
+    if (_e != hipSuccess) {                                                        \
+      ctx->err = std::string(#expr) + ": " + hipGetErrorString(_e);                \
+      throw Fail{};                                                                \
+    }                                                                              \
+  } while (0)
+
+struct Run {
+  fal_ctx* ctx;
+  DType dt;
+  int tanh;
+  explicit Run(fal_ctx* c) : ctx(c), dt(c->cfg.dtype == FAL_BF16 ? BF16 : F32), tanh(c->cfg.gelu_tanh) {}
+
+  const char* P(const void* base, int k) const {
+    return static_cast<const char*>(base) + ctx->Lo.boff[k] * (int64_t)ctx->D.es;
+  }
+  float* G(float* base, int k) const { return base + ctx->Lo.boff[k]; }
+  char* off(void* p, int64_t elems) const { return static_cast<char*>(p) + elems * (int64_t)ctx->D.es; }
+
+  void gemm_run(int ak, int bk, GemmGroup& g, hipStream_t s) {
+    const char* why = nullptr;
+    hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why);
+    if (e != hipSuccess) {
+      ctx->err = std::string("gemm: ") + (why ? why : hipGetErrorString(e));
+      throw Fail{};
+    }
+  }
+
+  static GemmProblem prob(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int N, int K) {
+    GemmProblem p;
+    memset(&p, 0, sizeof(p));
+    p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.M = M; p.N = N; p.K = K;
+    return p;
+  }
+
+  void gemm1(int ak, int bk, const GemmProblem& p, hipStream_t s) {
+    GemmGroup g;
+    memset(&g, 0, sizeof(g));
+    g.p[0] = p;
+    g.n = 1;
+    gemm_run(ak, bk, g, s);
+  }
+  void gemm2(int ak, int bk, const GemmProblem& p, const GemmProblem& q, hipStream_t s) {
+    GemmGroup g;
+    memset(&g, 0, sizeof(g));
+    g.p[0] = p;
+    g.p[1] = q;
+    g.n = 2;
+    gemm_run(ak, bk, g, s);
+  }
+
+  // ----- forward pieces ----------------------------------------------------
+  GemmProblem qkv_prob(const LayerSlot& S, const void* bp) {
+    const Dims& D = ctx->D;
+    GemmProblem p = prob(S.h1, D.d, P(bp, FAL_B_W_QKV), 3 * D.dA, D.M, 3 * D.dA, D.d);
+    p.epi = EPI_STORE; p.bias = P(bp, FAL_B_B_QKV); p.out = S.qkv; p.ldo = 3 * D.dA;
+    return p;
+  }
+  GemmProblem fc_prob(const LayerSlot& S, const void* bp) {
+    const Dims& D = ctx->D;
+    GemmProblem p = prob(S.h2, D.d, P(bp, FAL_B_W_FC), D.f, D.M, D.f, D.d);
+    p.epi = EPI_GELU; p.bias = P(bp, FAL_B_B_FC);
+    p.out = off(S.og, D.dA); p.ldo = D.dA + D.f;
+    p.out2 = S.pre; p.ldo2 = D.f;
+    return p;
+  }
+  // out-projection: A = O (first dA columns of og)
+  GemmProblem oproj_prob(const LayerSlot& S, const void* bp) {
+    const Dims& D = ctx->D;
+    GemmProblem p = prob(S.og, D.dA + D.f, P(bp, FAL_B_W_O), D.d, D.M, D.d, D.dA);
+    p.bias = P(bp, FAL_B_B_O);
+    return p;
+  }
+  GemmProblem down_prob(const LayerSlot& S, const void* bp) {
+    const Dims& D = ctx->D;
+    GemmProblem p = prob(off(S.og, D.dA), D.dA + D.f, P(bp, FAL_B_W_2), D.d, D.M, D.d, D.f);
+    p.bias = P(bp, FAL_B_B_2);
+    return p;
+  }
+  void attention_fwd(const LayerSlot& S, hipStream_t s) {
+    const Dims& D = ctx->D;
+    FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.hd, S.og, D.dA + D.f, S.lse, s));
+  }
+  void ln(const LnFwdArgs& a, hipStream_t s) { FAL_TRY(ln_fwd(dt, a, s)); }
+  LnFwdArgs lnargs(const float* x, float* mean, float* rstd) {
+    LnFwdArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x; a.M = ctx->D.M; a.d = ctx->D.d; a.eps = ctx->cfg.ln_eps; a.mean = mean; a.rstd = rstd;
+    return a;
+  }
+
+  void fork() {
+    FAL_TRY(hipEventRecord(ctx->ev_fork, ctx->sm));
+    FAL_TRY(hipStreamWaitEvent(ctx->sa, ctx->ev_fork, 0));
+  }
+  void join() {
+    FAL_TRY(hipEventRecord(ctx->ev_join, ctx->sa));
+    FAL_TRY(hipStreamWaitEvent(ctx->sm, ctx->ev_join, 0));
+  }
+  bool streams() const { return ctx->cfg.sched == FAL_SCHED_STREAMS && ctx->sa != ctx->sm; }
+  bool merged() const { return ctx->cfg.sched == FAL_SCHED_MERGED; }
+
+  void block_fwd(int layer, const void* bp, const float* x, float* y, void* first) {
+    const Dims& D = ctx->D;
+    const LayerSlot& S = ctx->W.slots[layer];
+    const int arch = ctx->cfg.arch;
+    hipStream_t sm = ctx->sm;
+    if (arch == FAL_ARCH_FAL && layer > 0) {
+      LnFwdArgs a = lnargs(x, S.mean1, S.rstd1);
+      a.g1 = P(bp, FAL_B_LN1_G); a.b1 = P(bp, FAL_B_LN1_B); a.y1 = S.h1;
+      a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2; a.add2 = first;
+      ln(a, sm);
+      if (merged()) {
+        gemm2(1, 0, qkv_prob(S, bp), fc_prob(S, bp), sm);
+        attention_fwd(S, sm);
+        GemmProblem p = oproj_prob(S, bp);
+        const GemmProblem q = down_prob(S, bp);
+        p.A2 = q.A; p.lda2 = q.lda; p.B2 = q.B; p.ldb2 = q.ldb; p.K2 = q.K; p.bias2 = q.bias;
+        p.epi = EPI_RESID; p.resid = x; p.ldr = D.d; p.out = y; p.ldo = D.d;
+        gemm1(1, 0, p, sm);
+        return;
+      }
+      hipStream_t s2 = sm;
+      if (streams()) { fork(); s2 = ctx->sa; }
+      gemm1(1, 0, fc_prob(S, bp), s2);
+      gemm1(1, 0, qkv_prob(S, bp), sm);
+      attention_fwd(S, sm);
+      GemmProblem po = oproj_prob(S, bp);
+      po.epi = EPI_RESID; po.resid = x; po.ldr = D.d; po.out = y; po.ldo = D.d;
+      gemm1(1, 0, po, sm);
+      if (streams()) join();
+      GemmProblem pd = down_prob(S, bp);
+      pd.epi = EPI_RESID; pd.resid = y; pd.ldr = D.d; pd.out = y; pd.ldo = D.d;
+      gemm1(1, 0, pd, sm);
+      return;
+    }
+    // Sequential blocks: GPT, FAL+, and FAL block 0.
+    {
+      LnFwdArgs a = lnargs(x, S.mean1, S.rstd1);
+      a.g1 = P(bp, FAL_B_LN1_G); a.b1 = P(bp, FAL_B_LN1_B); a.y1 = S.h1;
+      ln(a, sm);
+    }
+    gemm1(1, 0, qkv_prob(S, bp), sm);
+    attention_fwd(S, sm);
+    const bool block0_first = layer == 0 && arch != FAL_ARCH_GPT;
+    GemmProblem po = oproj_prob(S, bp);
+    if (block0_first) {
+      po.epi = EPI_STORE; po.out_f32 = 1; po.out = ctx->W.a1; po.ldo = D.d;
+      gemm1(1, 0, po, sm);
+      FAL_TRY(add_f32(x, ctx->W.a1, S.xm, (int64_t)D.M * D.d, sm));
+      LnFwdArgs a = lnargs(ctx->W.a1, ctx->W.meanF, ctx->W.rstdF);
+      if (arch == FAL_ARCH_FAL) {
+        a.g1 = P(bp, FAL_B_LNF1_G); a.b1 = P(bp, FAL_B_LNF1_B); a.y1 = first;
+      } else {
+        a.xhat_out = first;
+      }
+      ln(a, sm);
+    } else {
+      po.epi = EPI_RESID; po.resid = x; po.ldr = D.d; po.out = S.xm; po.ldo = D.d;
+      gemm1(1, 0, po, sm);
+    }
+    if (arch == FAL_ARCH_FAL) {
+      // block 0 of FAL: H2 = LN2(X_1) + F
+      LnFwdArgs a = lnargs(x, S.mean2, S.rstd2);
+      a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2; a.add2 = first;
+      ln(a, sm);
+    } else {
+      LnFwdArgs a = lnargs(S.xm, S.mean2, S.rstd2);
+      a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2;
+      if (arch == FAL_ARCH_FALPLUS && layer > 0) {
+        a.xhatF = first; a.gF = P(bp, FAL_B_LNF1_G); a.bF = P(bp, FAL_B_LNF1_B);
+      }
+      ln(a, sm);
+    }
+    gemm1(1, 0, fc_prob(S, bp), sm);
+    GemmProblem pd = down_prob(S, bp);
+    pd.epi = EPI_RESID; pd.resid = S.xm; pd.ldr = D.d; pd.out = y; pd.ldo = D.d;
+    gemm1(1, 0, pd, sm);
+  }
+
+  // ----- backward pieces ---------------------------------------------------
+  // dgrad of a linear layer y = x W: dx = dy W^T with W stored [in, out]
+  GemmProblem dgrad(const void* dy, int64_t lddy, const void* W, int in, int out, int M) {
+    return prob(dy, lddy, W, out, M, in, out);
+  }
+  // wgrad: dW[in, out] = x^T dy
+  GemmProblem wgrad(const void* x, int64_t ldx, const void* dy, int64_t lddy, int in, int out, int M,
+                    float* dW) {
+    GemmProblem p = prob(x, ldx, dy, lddy, in, out, M);
+    p.epi = EPI_STORE; p.out_f32 = 1; p.out = dW; p.ldo = out;
+    return p;
+  }
+  void colsum(const void* x, int in_f32, int64_t ld, int N, float* out, float* part, hipStream_t s) {
+    FAL_TRY(col_sum(dt, in_f32, x, ld, ctx->D.M, N, out, part, s));
+  }
+
+  // MLP branch backward: from dM (lp copy, and fp32 for the bias) to dH2
+  // (fp32, in W.dh2).  Writes W_2, B_2, W_FC, B_FC gradients.
+  void mlp_bwd(const LayerSlot& S, const void* bp, const void* dy_lp, const float* dy, float* gb,
+               hipStream_t s, float* part) {
+    const Dims& D = ctx->D;
+    Work& W = ctx->W;
+    void* dP = off(W.dog, D.dA);
+    GemmProblem pg = dgrad(dy_lp, D.d, P(bp, FAL_B_W_2), D.f, D.d, D.M);
+    pg.epi = EPI_GELU_BWD; pg.aux = S.pre; pg.ldaux = D.f; pg.out = dP; pg.ldo = D.dA + D.f;
+    gemm1(1, 1, pg, s);
+    gemm1(0, 0, wgrad(off(S.og, D.dA), D.dA + D.f, dy_lp, D.d, D.f, D.d, D.M, G(gb, FAL_B_W_2)), s);
+    colsum(dy, 1, D.d, D.d, G(gb, FAL_B_B_2), part, s);
+    GemmProblem ph = dgrad(dP, D.dA + D.f, P(bp, FAL_B_W_FC), D.d, D.f, D.M);
+    ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.dh2; ph.ldo = D.d;
+    gemm1(1, 1, ph, s);
+    gemm1(0, 0, wgrad(S.h2, D.d, dP, D.dA + D.f, D.d, D.f, D.M, G(gb, FAL_B_W_FC)), s);
+    colsum(dP, 0, D.dA + D.f, D.f, G(gb, FAL_B_B_FC), part, s);
+  }
+
+  // MHA branch backward: from dA (lp + fp32) to dH1 (fp32, in W.dh1).
+  void mha_bwd(const LayerSlot& S, const void* bp, const void* da_lp, const float* da, float* gb,
+               hipStream_t s, float* part) {
+    const Dims& D = ctx->D;
+    Work& W = ctx->W;
+    GemmProblem po = dgrad(da_lp, D.d, P(bp, FAL_B_W_O), D.dA, D.d, D.M);
+    po.epi = EPI_STORE; po.out = W.dog; po.ldo = D.dA + D.f;
+    gemm1(1, 1, po, s);
+    gemm1(0, 0, wgrad(S.og, D.dA + D.f, da_lp, D.d, D.dA, D.d, D.M, G(gb, FAL_B_W_O)), s);
+    colsum(da, 1, D.d, D.d, G(gb, FAL_B_B_O), part, s);
+    FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, W.dqkv,
+                     W.Dvec, nullptr, s));
+    GemmProblem ph = dgrad(W.dqkv, 3 * D.dA, P(bp, FAL_B_W_QKV), D.d, 3 * D.dA, D.M);
+    ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.dh1; ph.ldo = D.d;
+    gemm1(1, 1, ph, s);
+    gemm1(0, 0, wgrad(S.h1, D.d, W.dqkv, 3 * D.dA, D.d, 3 * D.dA, D.M, G(gb, FAL_B_W_QKV)), s);
+    colsum(W.dqkv, 0, 3 * D.dA, 3 * D.dA, G(gb, FAL_B_B_QKV), part, s);
+  }
+
+  LnBwdArgs lnb(const float* x, const float* mean, const float* rstd) {
+    LnBwdArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x; a.mean = mean; a.rstd = rstd; a.M = ctx->D.M; a.d = ctx->D.d;
+    a.partials = ctx->W.part_main;
+    return a;
+  }
+
+  // dy: fp32 gradient of the block output; dy_lp: its dtype copy.
+  void block_bwd(int layer, const void* bp, const float* x, const float* dy, const void* dy_lp,
+                 float* dx, void* dx_lp, float* dfirst, float* gb) {
+    const Dims& D = ctx->D;
+    Work& W = ctx->W;
+    const LayerSlot& S = W.slots[layer];
+    const int arch = ctx->cfg.arch;
+    hipStream_t sm = ctx->sm;
+    const int64_t Md = (int64_t)D.M * D.d;
+    const bool last = layer == D.L - 1;
+    // first-attention LayerNorm slot: zero unless used by this block
+    const bool uses_lnF = (arch == FAL_ARCH_FAL && layer == 0) || (arch == FAL_ARCH_FALPLUS && layer > 0);
+    if (!uses_lnF) {
+      FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_G), D.d, sm));
+      FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_B), D.d, sm));
+    }
+    if (arch == FAL_ARCH_FAL && layer > 0) {
+      hipStream_t s2 = sm;
+      float* part2 = W.part_main;
+      if (streams()) { fork(); s2 = ctx->sa; part2 = W.part_aux; }
+      mlp_bwd(S, bp, dy_lp, dy, gb, s2, part2);
+      mha_bwd(S, bp, dy_lp, dy, gb, sm, W.part_main);
+      if (streams()) join();
+      LnBwdArgs a = lnb(x, S.mean1, S.rstd1);
+      a.dy1 = W.dh1; a.g1 = P(bp, FAL_B_LN1_G); a.dy2 = W.dh2; a.g2 = P(bp, FAL_B_LN2_G);
+      a.dres = dy; a.dx = dx; a.dx_lp = dx_lp;
+      a.dacc = dfirst; a.dacc_overwrite = last;
+      a.dg1 = G(gb, FAL_B_LN1_G); a.db1 = G(gb, FAL_B_LN1_B);
+      a.dg2 = G(gb, FAL_B_LN2_G); a.db2 = G(gb, FAL_B_LN2_B);
+      FAL_TRY(ln_bwd(dt, a, sm));
+      return;
+    }
+    if (arch == FAL_ARCH_FAL) {  // block 0
+      mlp_bwd(S, bp, dy_lp, dy, gb, sm, W.part_main);
+      if (last) FAL_TRY(hipMemcpyAsync(dfirst, W.dh2, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
+      else FAL_TRY(add_f32(dfirst, W.dh2, dfirst, Md, sm));
+      // dA_1 = dY + LN_F backward of the accumulated dF
+      LnBwdArgs f = lnb(W.a1, W.meanF, W.rstdF);
+      f.dy1 = dfirst; f.g1 = P(bp, FAL_B_LNF1_G); f.dres = dy; f.dx = W.da; f.dx_lp = W.da_lp;
+      f.dg1 = G(gb, FAL_B_LNF1_G); f.db1 = G(gb, FAL_B_LNF1_B);
+      FAL_TRY(ln_bwd(dt, f, sm));
+      mha_bwd(S, bp, W.da_lp, W.da, gb, sm, W.part_main);
+      // LN2 was applied to X_1 with its own statistics (mean2/rstd2 equal
+      // mean1/rstd1 up to rounding; use each LayerNorm's own).
+      LnBwdArgs a2 = lnb(x, S.mean2, S.rstd2);
+      a2.dy2 = W.dh2; a2.g2 = P(bp, FAL_B_LN2_G); a2.dres = dy; a2.dx = dx;
+      a2.dg2 = G(gb, FAL_B_LN2_G); a2.db2 = G(gb, FAL_B_LN2_B);
+      FAL_TRY(ln_bwd(dt, a2, sm));
+      LnBwdArgs a1 = lnb(x, S.mean1, S.rstd1);
+      a1.dy1 = W.dh1; a1.g1 = P(bp, FAL_B_LN1_G); a1.dres = dx; a1.dx = dx; a1.dx_lp = dx_lp;
+      a1.dg1 = G(gb, FAL_B_LN1_G); a1.db1 = G(gb, FAL_B_LN1_B);
+      FAL_TRY(ln_bwd(dt, a1, sm));
+      return;
+    }
+    // GPT and FAL+: MLP backward, LN2 backward (with the FAL+ first-attention
+    // term), MHA backward, LN1 backward.
+    mlp_bwd(S, bp, dy_lp, dy, gb, sm, W.part_main);
+    LnBwdArgs a2 = lnb(S.xm, S.mean2, S.rstd2);
+    a2.dy2 = W.dh2; a2.g2 = P(bp, FAL_B_LN2_G); a2.dres = dy; a2.dx = W.dxm; a2.dx_lp = W.dxm_lp;
+    a2.dg2 = G(gb, FAL_B_LN2_G); a2.db2 = G(gb, FAL_B_LN2_B);
+    if (arch == FAL_ARCH_FALPLUS && layer > 0) {
+      a2.xhatF = ctx->W.first_in; a2.gF = P(bp, FAL_B_LNF1_G);
+      a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
+      a2.dgF = G(gb, FAL_B_LNF1_G); a2.dbF = G(gb, FAL_B_LNF1_B);
+    }
+    FAL_TRY(ln_bwd(dt, a2, sm));
+    const void* da_lp = W.dxm_lp;
+    const float* da = W.dxm;
+    if (arch == FAL_ARCH_FALPLUS && layer == 0 && D.L > 1) {
+      // dA_1 = dXm + backward of norm(A_1) applied to the accumulated dxhatF
+      FAL_TRY(hipMemcpyAsync(W.da, W.dxm, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
+      FAL_TRY(norm_bwd(W.a1, W.meanF, W.rstdF, dfirst, D.M, D.d, W.da, 1, sm));
+      FAL_TRY(cast_from_f32(dt, W.da, W.da_lp, Md, sm));
+      da_lp = W.da_lp;
+      da = W.da;
+    }
+    mha_bwd(S, bp, da_lp, da, gb, sm, W.part_main);
+    LnBwdArgs a1 = lnb(x, S.mean1, S.rstd1);
+    a1.dy1 = W.dh1; a1.g1 = P(bp, FAL_B_LN1_G); a1.dres = W.dxm; a1.dx = dx; a1.dx_lp = dx_lp;
+    a1.dg1 = G(gb, FAL_B_LN1_G); a1.db1 = G(gb, FAL_B_LN1_B);
+    FAL_TRY(ln_bwd(dt, a1, sm));
+  }
+};
+
+}  // namespace
+
+// ================================================================ ABI ====
+extern "C" {
+
+const char* fal_status_string(fal_status_t s) {
+  switch (s) {
+    case FAL_OK: return "ok";
+    case FAL_ERR_INVALID_ARG: return "invalid argument";
+    case FAL_ERR_UNSUPPORTED: return "unsupported";
+    case FAL_ERR_WORKSPACE: return "workspace too small";
+    case FAL_ERR_HIP: return "HIP error";
+    case FAL_ERR_STATE: return "bad call order";
+  }
+  return "unknown status";
+}
+
+const char* fal_last_error(const fal_ctx_t* ctx) { return ctx ? ctx->err.c_str() : ""; }
+
+fal_status_t fal_validate_config(const fal_config_t* cfg) {
+  const char* why = validate(cfg);
+  if (!why) why = validate_hd(cfg);
+  if (!why) return FAL_OK;
+  return unsupported(why) ? FAL_ERR_UNSUPPORTED : FAL_ERR_INVALID_ARG;
+}
+
+fal_status_t fal_param_layout(const fal_config_t* cfg, int64_t* global_off, int64_t* block_off,
+                              int64_t* block_base, int64_t* block_stride, int64_t* total) {
+  fal_status_t st = fal_validate_config(cfg);
+  if (st != FAL_OK) return st;
+  const Layout Lo = layout_of(*cfg);
+  if (global_off) memcpy(global_off, Lo.goff, sizeof(Lo.goff));
+  if (block_off) memcpy(block_off, Lo.boff, sizeof(Lo.boff));
+  if (block_base) *block_base = Lo.block_base;
+  if (block_stride) *block_stride = Lo.block_stride;
+  if (total) *total = Lo.total;
+  return FAL_OK;
+}
+
+fal_status_t fal_workspace_bytes(const fal_config_t* cfg, size_t* bytes) {
+  fal_status_t st = fal_validate_config(cfg);
+  if (st != FAL_OK) return st;
+  if (!bytes) return FAL_ERR_INVALID_ARG;
+  Work W;
+  carve(*cfg, nullptr, W, bytes);
+  return FAL_OK;
+}
+
+fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes, void* stream_main,
+                      void* stream_aux, fal_ctx_t** out) {
+  if (!out) return FAL_ERR_INVALID_ARG;
+  *out = nullptr;
+  fal_status_t st = fal_validate_config(cfg);
+  if (st != FAL_OK) return st;
+  size_t need = 0;
+  {
+    Work W;
+    carve(*cfg, nullptr, W, &need);
+  }
+  if (!workspace || ws_bytes < need) return FAL_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlignBytes) return FAL_ERR_WORKSPACE;
+  fal_ctx* ctx = new (std::nothrow) fal_ctx();
+  if (!ctx) return FAL_ERR_INVALID_ARG;
+  ctx->cfg = *cfg;
+  ctx->D = dims_of(*cfg);
+  ctx->Lo = layout_of(*cfg);
+  ctx->ws = static_cast<char*>(workspace);
+  ctx->ws_bytes = ws_bytes;
+  ctx->sm = static_cast<hipStream_t>(stream_main);
+  ctx->sa = stream_aux ? static_cast<hipStream_t>(stream_aux) : ctx->sm;
+  ctx->W.slots = new (std::nothrow) LayerSlot[cfg->n_layer];
+  if (!ctx->W.slots) { delete ctx; return FAL_ERR_INVALID_ARG; }
+  size_t total = 0;
+  carve(*cfg, ctx->ws, ctx->W, &total);
+  if (hipGetDevice(&ctx->device) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming) != hipSuccess) {
+    delete[] ctx->W.slots;
+    delete ctx;
+    return FAL_ERR_HIP;
+  }
+  *out = ctx;
+  return FAL_OK;
+}
+
+fal_status_t fal_destroy(fal_ctx_t* ctx) {
+  if (!ctx) return FAL_ERR_INVALID_ARG;
+  (void)hipEventDestroy(ctx->ev_fork);
+  (void)hipEventDestroy(ctx->ev_join);
+  delete[] ctx->W.slots;
+  delete ctx;
+  return FAL_OK;
+}
+
+static fal_status_t check_ctx(fal_ctx_t* ctx) {
+  if (!ctx) return FAL_ERR_INVALID_ARG;
+  ctx->err.clear();
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != ctx->device) {
+    ctx->err = "context used on a different HIP device than the one it was created on";
+    return FAL_ERR_STATE;
+  }
+  return FAL_OK;
+}
+
+static fal_status_t bad(fal_ctx_t* ctx, const char* why) {
+  ctx->err = why;
+  return FAL_ERR_INVALID_ARG;
+}
+
+fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_params, const float* x_in,
+                           float* x_out, void* first_attn) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (layer < 0 || layer >= ctx->D.L) return bad(ctx, "layer out of range");
+  if (!block_params || !x_in || !x_out) return bad(ctx, "NULL block_params, x_in or x_out");
+  if (x_in == x_out) return bad(ctx, "x_out may not alias x_in");
+  if (ctx->cfg.arch != FAL_ARCH_GPT && !first_attn) return bad(ctx, "first_attn is required for FAL and FAL+");
+  ctx->W.first_in = first_attn;
+  try {
+    Run r(ctx);
+    r.block_fwd(layer, block_params, x_in, x_out, first_attn);
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_params, const float* x_in,
+                           const float* dx_out, float* dx_in, float* d_first_attn, float* block_grads) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (layer < 0 || layer >= ctx->D.L) return bad(ctx, "layer out of range");
+  if (!block_params || !x_in || !dx_out || !dx_in || !block_grads)
+    return bad(ctx, "NULL block_params, x_in, dx_out, dx_in or block_grads");
+  if (dx_in == dx_out) return bad(ctx, "dx_in may not alias dx_out");
+  if (ctx->cfg.arch != FAL_ARCH_GPT && !d_first_attn) return bad(ctx, "d_first_attn is required for FAL and FAL+");
+  try {
+    Run r(ctx);
+    const int64_t Md = (int64_t)ctx->D.M * ctx->D.d;
+    FAL_TRY(cast_from_f32(r.dt, dx_out, ctx->W.lp_a, Md, ctx->sm));
+    r.block_bwd(layer, block_params, x_in, dx_out, ctx->W.lp_a, dx_in, ctx->W.lp_b, d_first_attn,
+                block_grads);
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* tokens, float* loss,
+                            float* logits, float* grads) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (!ctx->cfg.has_embed_head) return bad(ctx, "fal_model_step needs has_embed_head = 1 (use fal_stack_step)");
+  if (!params || !tokens || !loss || !grads) return bad(ctx, "NULL params, tokens, loss or grads");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  Work& W = ctx->W;
+  hipStream_t sm = ctx->sm;
+  const int64_t Md = (int64_t)D.M * D.d;
+  const char* pb = static_cast<const char*>(params);
+  auto gparam = [&](int k) { return pb + Lo.goff[k] * (int64_t)D.es; };
+  auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
+  auto bgrad = [&](int i) { return grads + Lo.block_base + (int64_t)i * Lo.block_stride; };
+  W.first_in = W.first;
+  try {
+    Run r(ctx);
+    FAL_TRY(embed_fwd(r.dt, tokens, D.B, D.T, D.V, D.d, gparam(FAL_P_WTE), gparam(FAL_P_WPE), W.resid, sm));
+    for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), W.resid + i * Md, W.resid + (i + 1) * Md, W.first);
+    const float* xl = W.resid + (int64_t)D.L * Md;
+    {
+      LnFwdArgs a = r.lnargs(xl, W.meanf, W.rstdf);
+      a.g1 = gparam(FAL_P_LNF_G); a.b1 = gparam(FAL_P_LNF_B); a.y1 = W.hf;
+      r.ln(a, sm);
+    }
+    GemmProblem ph = Run::prob(W.hf, D.d, gparam(FAL_P_WTE), D.d, D.M, D.V, D.d);
+    ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.logits; ph.ldo = D.Vp;
+    r.gemm1(1, 1, ph, sm);
+    FAL_TRY(cross_entropy(r.dt, W.logits, D.Vp, tokens, D.B, D.T, D.V, W.dlogits, D.Vp, W.row_loss, loss, sm));
+    if (logits)
+      FAL_TRY(hipMemcpy2DAsync(logits, (size_t)D.V * 4, W.logits, (size_t)D.Vp * 4, (size_t)D.V * 4, D.M,
+                               hipMemcpyDeviceToDevice, sm));
+    // head backward: dHf = dlogits wte ; dwte = dlogits^T Hf
+    GemmProblem pd = Run::prob(W.dlogits, D.Vp, gparam(FAL_P_WTE), D.d, D.M, D.d, D.V);
+    pd.epi = EPI_STORE; pd.out_f32 = 1; pd.out = W.dh1; pd.ldo = D.d;
+    r.gemm1(1, 0, pd, sm);
+    r.gemm1(0, 0, r.wgrad(W.dlogits, D.Vp, W.hf, D.d, D.V, D.d, D.M, grads + Lo.goff[FAL_P_WTE]), sm);
+    {
+      LnBwdArgs a = r.lnb(xl, W.meanf, W.rstdf);
+      a.dy1 = W.dh1; a.g1 = gparam(FAL_P_LNF_G); a.dx = W.dxa; a.dx_lp = W.lp_a;
+      a.dg1 = grads + Lo.goff[FAL_P_LNF_G]; a.db1 = grads + Lo.goff[FAL_P_LNF_B];
+      FAL_TRY(ln_bwd(r.dt, a, sm));
+    }
+    float *cur = W.dxa, *nxt = W.dxb;
+    void *cur_lp = W.lp_a, *nxt_lp = W.lp_b;
+    for (int i = D.L - 1; i >= 0; --i) {
+      r.block_bwd(i, bparam(i), W.resid + i * Md, cur, cur_lp, nxt, nxt_lp, W.dfirst, bgrad(i));
+      std::swap(cur, nxt);
+      std::swap(cur_lp, nxt_lp);
+    }
+    FAL_TRY(embed_bwd(tokens, D.B, D.T, D.V, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE],
+                      W.keys, W.dh1, sm));
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_in, const float* dy,
+                            float* loss, float* grads, float* dx_in) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (ctx->cfg.has_embed_head) return bad(ctx, "fal_stack_step needs has_embed_head = 0");
+  if (!params || !x_in || !dy || !grads) return bad(ctx, "NULL params, x_in, dy or grads");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  Work& W = ctx->W;
+  hipStream_t sm = ctx->sm;
+  const int64_t Md = (int64_t)D.M * D.d;
+  const char* pb = static_cast<const char*>(params);
+  auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
+  auto bgrad = [&](int i) { return grads + Lo.block_base + (int64_t)i * Lo.block_stride; };
+  auto xin = [&](int i) { return i == 0 ? x_in : W.resid + i * Md; };
+  W.first_in = W.first;
+  try {
+    Run r(ctx);
+    for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), xin(i), W.resid + (i + 1) * Md, W.first);
+    const float* xl = W.resid + (int64_t)D.L * Md;
+    if (loss) FAL_TRY(dot(dy, xl, Md, loss, W.part_main, sm));
+    FAL_TRY(cast_from_f32(r.dt, dy, W.lp_a, Md, sm));
+    const float* cur = dy;
+    float* bufs[2] = {W.dxa, W.dxb};
+    void* lps[2] = {W.lp_a, W.lp_b};
+    int k = 0;
+    for (int i = D.L - 1; i >= 0; --i) {
+      float* out = (i == 0 && dx_in) ? dx_in : bufs[k];
+      r.block_bwd(i, bparam(i), xin(i), cur, lps[k], out, lps[k ^ 1], W.dfirst, bgrad(i));
+      cur = out;
+      k ^= 1;
+    }
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last) {
+  if (!ctx || !x_last) return FAL_ERR_INVALID_ARG;
+  *x_last = ctx->W.resid + (int64_t)ctx->D.L * ctx->D.M * ctx->D.d;
+  return FAL_OK;
+}
+
+}  // extern "C"

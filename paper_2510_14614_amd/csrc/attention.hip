@@ -1,0 +1,298 @@
+// Causal scaled-dot-product attention per head (the MHA of Sec. 2), in the
+// blockwise form with an online softmax so that the T x T score matrix is
+// never stored (FlashAttention, which the paper uses on its GPUs).
+//
+// This file holds the SIMT kernels: fp32 arithmetic on fp32 or bf16
+// storage, any head_dim in {16, 32, 64, 128}.  A workgroup holds 64 query
+// (or key) rows with 4 lanes per row, each lane owning head_dim/4 of the
+// row; K/V (or Q/dO) tiles of 64 rows are staged in LDS.
+//
+// Backward is deterministic without atomics: one kernel accumulates dK, dV
+// per key block over the query blocks at or after it; a second kernel
+// accumulates dQ per query block over the key blocks at or before it.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace fal {
+
+constexpr int ABR = 64;  // rows per tile
+
+template <typename S, int HD>
+__global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H, S* O, int64_t ldo,
+                                                     float* lse) {
+  constexpr int P = HD / 4;
+  __shared__ float Ks[ABR][HD + 1];
+  __shared__ float Vs[ABR][HD + 1];
+  const int qb = gridDim.x - 1 - blockIdx.x;  // long (late) query blocks first
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
+  const int t = qb * ABR + r;
+  const bool valid = t < T;
+  const float scale = 1.f / sqrtf((float)HD);
+  const S* base = qkv + (int64_t)b * T * ld;
+  float q[P], o[P];
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    q[c] = valid ? to_f(base[(int64_t)t * ld + h * HD + part * P + c]) * scale : 0.f;
+    o[c] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  const int kend = min(T, qb * ABR + ABR);
+  for (int k0 = 0; k0 < kend; k0 += ABR) {
+    for (int e = tid; e < ABR * HD; e += 256) {
+      const int kr = e / HD, c = e % HD, key = k0 + kr;
+      const bool ok = key < T;
+      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + dA + h * HD + c]) : 0.f;
+      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + c]) : 0.f;
+    }
+    __syncthreads();
+    float sc[ABR];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < ABR; ++j) {
+      float p = 0.f;
+#pragma unroll
+      for (int c = 0; c < P; ++c) p = fmaf(q[c], Ks[j][part * P + c], p);
+      p += __shfl_xor(p, 1, FAL_WAVE);
+      p += __shfl_xor(p, 2, FAL_WAVE);
+      const int key = k0 + j;
+      sc[j] = (key <= t && key < T) ? p : -INFINITY;
+      mt = fmaxf(mt, sc[j]);
+    }
+    if (mt > -INFINITY) {
+      const float mn = fmaxf(m, mt);
+      const float corr = expf(m - mn);
+      l *= corr;
+#pragma unroll
+      for (int c = 0; c < P; ++c) o[c] *= corr;
+#pragma unroll
+      for (int j = 0; j < ABR; ++j) {
+        const float p = expf(sc[j] - mn);
+        l += p;
+#pragma unroll
+        for (int c = 0; c < P; ++c) o[c] = fmaf(p, Vs[j][part * P + c], o[c]);
+      }
+      m = mn;
+    }
+    __syncthreads();
+  }
+  if (valid) {
+    const float inv = 1.f / l;
+    S* orow = O + ((int64_t)b * T + t) * ldo + h * HD + part * P;
+#pragma unroll
+    for (int c = 0; c < P; ++c) orow[c] = from_f<S>(o[c] * inv);
+    if (part == 0) lse[((int64_t)b * H + h) * T + t] = m + logf(l);
+  }
+}
+
+// D[b, h, t] = sum_c dO[t, h*HD + c] * O[t, h*HD + c]
+template <typename S>
+__global__ __launch_bounds__(256) void attn_bwd_dot(const S* O, int64_t ldo, const S* dO, int64_t lddo,
+                                                    int B, int T, int H, int HD, float* Dvec) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)B * H * T) return;
+  const int t = i % T;
+  const int h = (i / T) % H;
+  const int b = i / ((int64_t)T * H);
+  const int64_t row = (int64_t)b * T + t;
+  float s = 0.f;
+  for (int c = 0; c < HD; ++c) s += to_f(O[row * ldo + h * HD + c]) * to_f(dO[row * lddo + h * HD + c]);
+  Dvec[i] = s;
+}
+
+template <typename S, int HD>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S* dO, int64_t lddo,
+                                                          const float* lse, const float* Dvec, int T,
+                                                          int H, S* dqkv) {
+  constexpr int P = HD / 4;
+  __shared__ float Qs[ABR][HD + 1];
+  __shared__ float dOs[ABR][HD + 1];
+  __shared__ float Ls[ABR], Ds[ABR];
+  const int kb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
+  const int key = kb * ABR + r;
+  const bool valid = key < T;
+  const float scale = 1.f / sqrtf((float)HD);
+  const S* base = qkv + (int64_t)b * T * ld;
+  const S* dObase = dO + (int64_t)b * T * lddo;
+  const float* lrow = lse + ((int64_t)b * H + h) * T;
+  const float* drow = Dvec + ((int64_t)b * H + h) * T;
+  float k[P], v[P], dk[P], dv[P];
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    k[c] = valid ? to_f(base[(int64_t)key * ld + dA + h * HD + part * P + c]) : 0.f;
+    v[c] = valid ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + part * P + c]) : 0.f;
+    dk[c] = 0.f;
+    dv[c] = 0.f;
+  }
+  for (int q0 = kb * ABR; q0 < T; q0 += ABR) {
+    for (int e = tid; e < ABR * HD; e += 256) {
+      const int qr = e / HD, c = e % HD, tq = q0 + qr;
+      const bool ok = tq < T;
+      Qs[qr][c] = ok ? to_f(base[(int64_t)tq * ld + h * HD + c]) : 0.f;
+      dOs[qr][c] = ok ? to_f(dObase[(int64_t)tq * lddo + h * HD + c]) : 0.f;
+    }
+    if (tid < ABR) {
+      const int tq = q0 + tid;
+      Ls[tid] = tq < T ? lrow[tq] : 0.f;
+      Ds[tid] = tq < T ? drow[tq] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int j = 0; j < ABR; ++j) {
+      const int tq = q0 + j;
+      float s = 0.f, dp = 0.f;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        s = fmaf(Qs[j][part * P + c], k[c], s);
+        dp = fmaf(dOs[j][part * P + c], v[c], dp);
+      }
+      s += __shfl_xor(s, 1, FAL_WAVE);
+      s += __shfl_xor(s, 2, FAL_WAVE);
+      dp += __shfl_xor(dp, 1, FAL_WAVE);
+      dp += __shfl_xor(dp, 2, FAL_WAVE);
+      const float p = (valid && tq < T && tq >= key) ? expf(s * scale - Ls[j]) : 0.f;
+      const float ds = p * (dp - Ds[j]) * scale;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        dv[c] = fmaf(p, dOs[j][part * P + c], dv[c]);
+        dk[c] = fmaf(ds, Qs[j][part * P + c], dk[c]);
+      }
+    }
+    __syncthreads();
+  }
+  if (valid) {
+    S* row = dqkv + ((int64_t)b * T + key) * ld + h * HD + part * P;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      row[dA + c] = from_f<S>(dk[c]);
+      row[2 * dA + c] = from_f<S>(dv[c]);
+    }
+  }
+}
+
+template <typename S, int HD>
+__global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* dO, int64_t lddo,
+                                                        const float* lse, const float* Dvec, int T,
+                                                        int H, S* dqkv) {
+  constexpr int P = HD / 4;
+  __shared__ float Ks[ABR][HD + 1];
+  __shared__ float Vs[ABR][HD + 1];
+  const int qb = gridDim.x - 1 - blockIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
+  const int t = qb * ABR + r;
+  const bool valid = t < T;
+  const float scale = 1.f / sqrtf((float)HD);
+  const S* base = qkv + (int64_t)b * T * ld;
+  float q[P], g[P], dq[P];
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    q[c] = valid ? to_f(base[(int64_t)t * ld + h * HD + part * P + c]) : 0.f;
+    g[c] = valid ? to_f(dO[((int64_t)b * T + t) * lddo + h * HD + part * P + c]) : 0.f;
+    dq[c] = 0.f;
+  }
+  const float L = valid ? lse[((int64_t)b * H + h) * T + t] : 0.f;
+  const float Dt = valid ? Dvec[((int64_t)b * H + h) * T + t] : 0.f;
+  const int kend = min(T, qb * ABR + ABR);
+  for (int k0 = 0; k0 < kend; k0 += ABR) {
+    for (int e = tid; e < ABR * HD; e += 256) {
+      const int kr = e / HD, c = e % HD, key = k0 + kr;
+      const bool ok = key < T;
+      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + dA + h * HD + c]) : 0.f;
+      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + c]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int j = 0; j < ABR; ++j) {
+      const int key = k0 + j;
+      float s = 0.f, dp = 0.f;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        s = fmaf(q[c], Ks[j][part * P + c], s);
+        dp = fmaf(g[c], Vs[j][part * P + c], dp);
+      }
+      s += __shfl_xor(s, 1, FAL_WAVE);
+      s += __shfl_xor(s, 2, FAL_WAVE);
+      dp += __shfl_xor(dp, 1, FAL_WAVE);
+      dp += __shfl_xor(dp, 2, FAL_WAVE);
+      const float p = (valid && key <= t && key < T) ? expf(s * scale - L) : 0.f;
+      const float ds = p * (dp - Dt) * scale;
+#pragma unroll
+      for (int c = 0; c < P; ++c) dq[c] = fmaf(ds, Ks[j][part * P + c], dq[c]);
+    }
+    __syncthreads();
+  }
+  if (valid) {
+    S* row = dqkv + ((int64_t)b * T + t) * ld + h * HD + part * P;
+#pragma unroll
+    for (int c = 0; c < P; ++c) row[c] = from_f<S>(dq[c]);
+  }
+}
+
+template <typename F>
+static hipError_t dispatch_hd(int hd, F&& f) {
+  switch (hd) {
+    case 16: return f(std::integral_constant<int, 16>{});
+    case 32: return f(std::integral_constant<int, 32>{});
+    case 64: return f(std::integral_constant<int, 64>{});
+    case 128: return f(std::integral_constant<int, 128>{});
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
+                    float* lse, hipStream_t s) {
+  const dim3 grid(cdiv(T, ABR), H, B), block(256);
+  return dispatch_hd(hd, [&](auto c) {
+    constexpr int HD = decltype(c)::value;
+    if (dt == BF16)
+      hipLaunchKernelGGL((attn_fwd_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv), T, H,
+                         static_cast<bf16*>(O), ldo, lse);
+    else
+      hipLaunchKernelGGL((attn_fwd_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv), T,
+                         H, static_cast<float*>(O), ldo, lse);
+    return hipGetLastError();
+  });
+}
+
+hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const void* dO,
+                    int64_t lddo, const float* lse, int B, int T, int H, int hd, void* dqkv,
+                    float* Dvec, float* dq_acc, hipStream_t s) {
+  (void)dq_acc;
+  const int64_t nrows = (int64_t)B * H * T;
+  if (dt == BF16)
+    hipLaunchKernelGGL((attn_bwd_dot<bf16>), dim3(cdiv(nrows, 256)), dim3(256), 0, s,
+                       static_cast<const bf16*>(O), ldo, static_cast<const bf16*>(dO), lddo, B, T, H, hd, Dvec);
+  else
+    hipLaunchKernelGGL((attn_bwd_dot<float>), dim3(cdiv(nrows, 256)), dim3(256), 0, s,
+                       static_cast<const float*>(O), ldo, static_cast<const float*>(dO), lddo, B, T, H, hd, Dvec);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid(cdiv(T, ABR), H, B), block(256);
+  return dispatch_hd(hd, [&](auto c) {
+    constexpr int HD = decltype(c)::value;
+    if (dt == BF16) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, static_cast<bf16*>(dqkv));
+      hipLaunchKernelGGL((attn_bwd_dq_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, static_cast<bf16*>(dqkv));
+    } else {
+      hipLaunchKernelGGL((attn_bwd_dkdv_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, static_cast<float*>(dqkv));
+      hipLaunchKernelGGL((attn_bwd_dq_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, static_cast<float*>(dqkv));
+    }
+    return hipGetLastError();
+  });
+}
+
+}  // namespace fal

@@ -1,0 +1,189 @@
+// Internal launch interface between the host scheduler (api.cpp) and the
+// HIP kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fal {
+
+enum DType : int { F32 = 0, BF16 = 1 };
+
+// ---------------------------------------------------------------- GEMM ----
+// C[m, n] = sum_k A(m, k) B(k, n) over one or two K segments, followed by an
+// epilogue.  Operand orientation:
+//   a_kmaj = 1: A(m, k) = A[m * lda + k]   (k contiguous)
+//   a_kmaj = 0: A(m, k) = A[k * lda + m]   (m contiguous)
+//   b_kmaj = 1: B(k, n) = B[n * ldb + k]   (k contiguous)
+//   b_kmaj = 0: B(k, n) = B[k * ldb + n]   (n contiguous)
+// A and B hold the storage dtype of the launch; accumulation is fp32.
+enum Epi : int {
+  EPI_STORE = 0,     // out = acc + bias (+ bias2)          (out: f32 or dtype)
+  EPI_GELU = 1,      // out2 = acc + bias (pre-activation), out = GELU(out2)  (dtype)
+  EPI_RESID = 2,     // out(f32) = resid(f32) + acc + bias   (resid may equal out)
+  EPI_GELU_BWD = 3,  // out = acc * GELU'(aux)                (aux, out: dtype)
+};
+
+struct GemmProblem {
+  const void* A;
+  const void* B;
+  const void* A2;  // second K segment (K-concatenation); NULL if K2 == 0
+  const void* B2;
+  int64_t lda, ldb, lda2, ldb2;
+  int M, N, K, K2;
+  int epi;
+  int out_f32;        // EPI_STORE: 1 -> out is fp32, 0 -> out is dtype
+  const void* bias;   // dtype [N] or NULL
+  const void* bias2;  // dtype [N] or NULL, added as well (K-concatenated layers)
+  const float* resid; // EPI_RESID
+  int64_t ldr;
+  void* out;
+  int64_t ldo;
+  void* out2;         // EPI_GELU pre-activation output
+  int64_t ldo2;
+  const void* aux;    // EPI_GELU_BWD pre-activation input
+  int64_t ldaux;
+  // filled in by the launcher
+  int tiles_m, tiles_n, tile_start;
+};
+
+constexpr int kMaxGroup = 4;
+struct GemmGroup {
+  GemmProblem p[kMaxGroup];
+  int n;
+  int total_tiles;
+};
+
+// Launches every problem of `g` (same dtype and operand orientation) as one
+// grouped kernel.  Returns hipSuccess or the launch error; `why` receives a
+// static message for argument errors.
+hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
+                const char** why);
+
+// ----------------------------------------------------------- LayerNorm ----
+// Row LayerNorm over d of fp32 rows x.  Writes
+//   y1 = LN(x; g1, b1)                               (dtype)  if y1
+//   y2 = LN(x; g2, b2) + add2                        (dtype)  if y2 and add2
+//   y2 = LN(x; g2, b2) + gF * xhatF + bF             (dtype)  if y2 and xhatF
+//   y2 = LN(x; g2, b2)                               (dtype)  if y2 only
+//   xhat_out = (x - mean) * rstd                     (dtype)  if xhat_out
+// and saves mean, rstd (fp32 [M]) if non-NULL.  add2, xhatF, gF, bF: dtype.
+struct LnFwdArgs {
+  const float* x;
+  int M, d;
+  float eps;
+  const void *g1, *b1;
+  void* y1;
+  const void *g2, *b2;
+  void* y2;
+  const void* add2;
+  const void *xhatF, *gF, *bF;
+  void* xhat_out;
+  float* mean;
+  float* rstd;
+};
+hipError_t ln_fwd(DType dt, const LnFwdArgs& a, hipStream_t s);
+
+// LayerNorm backward over rows, with up to two LayerNorms of the same input
+// x (fp32; shared mean/rstd):
+//   dxhat = dy1 * g1 + dy2 * g2                                  (dy*: fp32)
+//   dx = dres + rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat * xhat))
+// with xhat = (x - mean) * rstd recomputed.  Optionally
+//   dacc (+)= dy2                       FAL: first-attention accumulator
+//   dxhatF_acc (+)= gF * dy2            FAL+: accumulator of the shared
+//                                       first-attention normalisation
+// ("=" when the matching *_overwrite flag is set).  dx (fp32) may alias
+// dres; dres may be NULL (treated as 0).  dx_lp (dtype copy of dx) is
+// written if non-NULL.  Parameter gradients (fp32 [d], each optional):
+//   dg1 = sum_rows dy1 * xhat, db1 = sum_rows dy1,
+//   dg2 = sum_rows dy2 * xhat, db2 = sum_rows dy2,
+//   dgF = sum_rows dy2 * xhatF, dbF = sum_rows dy2,
+// reduced deterministically through `partials` (ln_bwd_scratch floats).
+struct LnBwdArgs {
+  const float* x;
+  const float* mean;
+  const float* rstd;
+  int M, d;
+  const float* dy1;
+  const void* g1;
+  const float* dy2;
+  const void* g2;
+  const float* dres;
+  float* dx;
+  void* dx_lp;
+  float* dacc;
+  int dacc_overwrite;
+  const void* xhatF;
+  const void* gF;
+  float* dxhatF_acc;
+  int dxhatF_overwrite;
+  float *dg1, *db1, *dg2, *db2, *dgF, *dbF;
+  float* partials;
+};
+hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s);
+int64_t ln_bwd_scratch(int M, int d);
+
+// Backward of the affine-free normalisation xhat = (a - mean) * rstd given
+// dxhat (fp32): da (+)= rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat*xhat))
+// with xhat recomputed from a (fp32).  accumulate=0 overwrites da.
+hipError_t norm_bwd(const float* a, const float* mean, const float* rstd, const float* dxhat,
+                    int M, int d, float* da, int accumulate, hipStream_t s);
+
+// Sum `nblk` partial rows of width d: out[j] = sum_b part[b * stride + j].
+hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float* out, hipStream_t s);
+
+// Column sums of a [M, N] matrix (dtype or fp32) into fp32 out[N] (bias
+// gradients).  Deterministic two-stage reduction with `scratch` of
+// col_sum_scratch(M, N) floats.
+hipError_t col_sum(DType dt, int in_f32, const void* x, int64_t ld, int M, int N, float* out,
+                   float* scratch, hipStream_t s);
+int64_t col_sum_scratch(int M, int N);
+
+// ------------------------------------------------------------ attention ----
+// Causal multi-head attention on the packed QKV activations [M, 3*dA]
+// (Q | K | V, head h at h*hd), M = B*T.  O: dtype [M, ldo] (head h at
+// column h*hd), LSE: fp32 [B, H, T] (natural log of the softmax denominators
+// including the 1/sqrt(hd) scale).
+hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
+                    float* lse, hipStream_t s);
+// Backward: from dO (dtype [M, ldo]) produce dQKV (dtype [M, 3dA]).
+// Dvec: fp32 [B, H, T] scratch (rowsum(dO * O)); dq_acc: fp32 [M, dA] scratch.
+hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const void* dO,
+                    int64_t lddo, const float* lse, int B, int T, int H, int hd, void* dqkv,
+                    float* Dvec, float* dq_acc, hipStream_t s);
+
+// ------------------------------------------------ embedding / loss / misc ----
+// X[m, :] = wte[tok[b, t]] + wpe[t]  (fp32 out), tokens [B, T+1].
+hipError_t embed_fwd(DType dt, const int32_t* tokens, int B, int T, int V, int d, const void* wte,
+                     const void* wpe, float* X, hipStream_t s);
+// dwte[v] += sum over positions with input id v of dX rows (deterministic:
+// sorted by (id, position)), dwpe[t] = sum_b dX[b, t].  sort_scratch: int32
+// of embed_bwd_scratch(M) elements; partial: fp32 [M, d] scratch.
+// Requires B*T <= 16384.
+hipError_t embed_bwd(const int32_t* tokens, int B, int T, int V, int d, const float* dX,
+                     float* dwte, float* dwpe, int32_t* sort_scratch, float* partial,
+                     hipStream_t s);
+int64_t embed_bwd_scratch(int M);
+
+// Cross-entropy over rows of fp32 logits [M, V] (row stride ldl) with
+// targets tokens[b, t + 1].  Writes dlogits = (softmax - onehot) / M as
+// dtype [M, ldd] (columns V..ldd-1 zeroed) and per-row loss (fp32 [M]);
+// then loss = mean(row_loss) (fp32 scalar, fixed-order reduction).
+hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32_t* tokens, int B,
+                         int T, int V, void* dlogits, int64_t ldd, float* row_loss, float* loss,
+                         hipStream_t s);
+
+// loss = sum(a * b) over n fp32 elements (fixed-order reduction); scratch of
+// dot_scratch(n) floats.
+hipError_t dot(const float* a, const float* b, int64_t n, float* loss, float* scratch,
+               hipStream_t s);
+int64_t dot_scratch(int64_t n);
+
+// y = a + b (fp32, n elements); y may alias a.
+hipError_t add_f32(const float* a, const float* b, float* y, int64_t n, hipStream_t s);
+// Convert fp32 -> dtype.
+hipError_t cast_from_f32(DType dt, const float* x, void* y, int64_t n, hipStream_t s);
+// Fill fp32 with zero (a kernel, so it can live inside captured graphs).
+hipError_t zero_f32(float* y, int64_t n, hipStream_t s);
+
+}  // namespace fal
