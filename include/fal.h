@@ -188,6 +188,24 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
  * workspace after a step; valid until the next step. */
 fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);
 
+/* Kernel timing, for measurement.  While enabled, each launch of the
+ * classes below is bracketed by HIP events recorded on the stream the
+ * kernel runs on; fal_profile_read synchronises the context's streams and
+ * returns, per class since the last enable: the number of launches, the
+ * summed event time in ms, and the summed algorithmic FLOPs and bytes of
+ * those launches (GEMM: 2*M*N*K; attention forward: 2*B*H*hd*T*(T+1), the
+ * causal half of QK^T and PV; attention backward: twice that; norm: bytes
+ * of the rows read and written).  fal_profile_enable(ctx, 0) turns timing
+ * off; either call clears the counters.  Host memory only; no device
+ * allocation. */
+typedef enum {
+  FAL_PROF_GEMM = 0, FAL_PROF_ATTN_FWD = 1, FAL_PROF_ATTN_BWD = 2, FAL_PROF_NORM = 3,
+  FAL_PROF_NCLASS = 4
+} fal_prof_class_t;
+fal_status_t fal_profile_enable(fal_ctx_t* ctx, int32_t enable);
+fal_status_t fal_profile_read(fal_ctx_t* ctx, int32_t cls, int64_t* launches, double* total_ms,
+                              double* flops, double* bytes);
+
 const char* fal_status_string(fal_status_t status);
 const char* fal_last_error(const fal_ctx_t* ctx); /* "" if none; ctx may be NULL */
 

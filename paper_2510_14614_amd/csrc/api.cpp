@@ -27,6 +27,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "../../include/fal.h"
 #include "kernels.h"
@@ -230,6 +231,12 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
 }  // namespace
 
 // ------------------------------------------------------------- context --
+struct ProfSpan {
+  int cls;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
 struct fal_ctx {
   fal_config_t cfg;
   Dims D;
@@ -241,7 +248,13 @@ struct fal_ctx {
   hipEvent_t ev_fork, ev_join;
   int device;
   std::string err;
-  int fwd_done_mask_ok;
+  // kernel timing (fal_profile_enable)
+  bool prof_on = false;
+  std::vector<hipEvent_t> prof_pool;
+  size_t prof_used = 0;
+  std::vector<ProfSpan> prof_spans;
+  int64_t prof_n[FAL_PROF_NCLASS] = {};
+  double prof_ms[FAL_PROF_NCLASS] = {}, prof_flops[FAL_PROF_NCLASS] = {}, prof_bytes[FAL_PROF_NCLASS] = {};
 };
 
 namespace {
@@ -257,6 +270,32 @@ struct Fail {};
     }                                                                              \
   } while (0)
 
+// Brackets one launch with HIP events on the stream it runs on when kernel
+// timing is enabled; a no-op otherwise.
+struct Span {
+  fal_ctx* c;
+  hipStream_t s;
+  int idx = -1;
+  Span(fal_ctx* ctx, int cls, hipStream_t st, double flops, double bytes) : c(ctx), s(st) {
+    if (!c->prof_on) return;
+    if (c->prof_used + 2 > c->prof_pool.size()) {
+      for (int i = 0; i < 256; ++i) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        c->prof_pool.push_back(e);
+      }
+    }
+    ProfSpan sp{cls, c->prof_pool[c->prof_used], c->prof_pool[c->prof_used + 1], flops, bytes};
+    c->prof_used += 2;
+    if (hipEventRecord(sp.a, s) != hipSuccess) return;
+    idx = (int)c->prof_spans.size();
+    c->prof_spans.push_back(sp);
+  }
+  ~Span() {
+    if (idx >= 0) (void)hipEventRecord(c->prof_spans[idx].b, s);
+  }
+};
+
 struct Run {
   fal_ctx* ctx;
   DType dt;
@@ -271,6 +310,14 @@ struct Run {
 
   void gemm_run(int ak, int bk, GemmGroup& g, hipStream_t s) {
     const char* why = nullptr;
+    double flops = 0.0, bytes = 0.0;
+    for (int i = 0; i < g.n; ++i) {
+      const GemmProblem& q = g.p[i];
+      flops += 2.0 * q.M * (double)q.N * (q.K + q.K2);
+      bytes += (double)ctx->D.es * ((double)q.M * (q.K + q.K2) + (double)q.N * (q.K + q.K2)) +
+               (double)q.M * q.N * ((q.out_f32 || q.epi == EPI_RESID) ? 4.0 : (double)ctx->D.es);
+    }
+    Span span(ctx, FAL_PROF_GEMM, s, flops, bytes);
     hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why);
     if (e != hipSuccess) {
       ctx->err = std::string("gemm: ") + (why ? why : hipGetErrorString(e));
@@ -331,9 +378,21 @@ struct Run {
   }
   void attention_fwd(const LayerSlot& S, hipStream_t s) {
     const Dims& D = ctx->D;
+    const double fl = 2.0 * D.B * D.H * (double)D.hd * D.T * (D.T + 1.0);
+    Span span(ctx, FAL_PROF_ATTN_FWD, s, fl, (double)D.es * D.M * 4.0 * D.dA);
     FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.hd, S.og, D.dA + D.f, S.lse, s));
   }
-  void ln(const LnFwdArgs& a, hipStream_t s) { FAL_TRY(ln_fwd(dt, a, s)); }
+  void ln(const LnFwdArgs& a, hipStream_t s) {
+    const double row = 4.0 + (double)ctx->D.es * (!!a.y1 + !!a.y2 + !!a.add2 + !!a.xhatF + !!a.xhat_out);
+    Span span(ctx, FAL_PROF_NORM, s, 0.0, row * a.M * a.d);
+    FAL_TRY(ln_fwd(dt, a, s));
+  }
+  void lnbwd(const LnBwdArgs& a, hipStream_t s) {
+    const double row = 8.0 + 4.0 * (!!a.dy1 + !!a.dy2 + !!a.dres) + 8.0 * (!!a.dacc + !!a.dxhatF_acc) +
+                       (double)ctx->D.es * (!!a.dx_lp + !!a.xhatF);
+    Span span(ctx, FAL_PROF_NORM, s, 0.0, row * a.M * a.d);
+    FAL_TRY(ln_bwd(dt, a, s));
+  }
   LnFwdArgs lnargs(const float* x, float* mean, float* rstd) {
     LnFwdArgs a;
     memset(&a, 0, sizeof(a));
@@ -475,8 +534,12 @@ struct Run {
     gemm1(1, 1, po, s);
     gemm1(0, 0, wgrad(S.og, D.dA + D.f, da_lp, D.d, D.dA, D.d, D.M, G(gb, FAL_B_W_O)), s);
     colsum(da, 1, D.d, D.d, G(gb, FAL_B_B_O), part, s);
-    FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, W.dqkv,
-                     W.Dvec, nullptr, s));
+    {
+      const double fl = 4.0 * D.B * D.H * (double)D.hd * D.T * (D.T + 1.0);
+      Span span(ctx, FAL_PROF_ATTN_BWD, s, fl, (double)D.es * D.M * 8.0 * D.dA);
+      FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, W.dqkv,
+                       W.Dvec, nullptr, s));
+    }
     GemmProblem ph = dgrad(W.dqkv, 3 * D.dA, P(bp, FAL_B_W_QKV), D.d, 3 * D.dA, D.M);
     ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.dh1; ph.ldo = D.d;
     gemm1(1, 1, ph, s);
@@ -521,7 +584,7 @@ struct Run {
       a.dacc = dfirst; a.dacc_overwrite = last;
       a.dg1 = G(gb, FAL_B_LN1_G); a.db1 = G(gb, FAL_B_LN1_B);
       a.dg2 = G(gb, FAL_B_LN2_G); a.db2 = G(gb, FAL_B_LN2_B);
-      FAL_TRY(ln_bwd(dt, a, sm));
+      lnbwd(a, sm);
       return;
     }
     if (arch == FAL_ARCH_FAL) {  // block 0
@@ -532,18 +595,18 @@ struct Run {
       LnBwdArgs f = lnb(W.a1, W.meanF, W.rstdF);
       f.dy1 = dfirst; f.g1 = P(bp, FAL_B_LNF1_G); f.dres = dy; f.dx = W.da; f.dx_lp = W.da_lp;
       f.dg1 = G(gb, FAL_B_LNF1_G); f.db1 = G(gb, FAL_B_LNF1_B);
-      FAL_TRY(ln_bwd(dt, f, sm));
+      lnbwd(f, sm);
       mha_bwd(S, bp, W.da_lp, W.da, gb, sm, W.part_main);
       // LN2 was applied to X_1 with its own statistics (mean2/rstd2 equal
       // mean1/rstd1 up to rounding; use each LayerNorm's own).
       LnBwdArgs a2 = lnb(x, S.mean2, S.rstd2);
       a2.dy2 = W.dh2; a2.g2 = P(bp, FAL_B_LN2_G); a2.dres = dy; a2.dx = dx;
       a2.dg2 = G(gb, FAL_B_LN2_G); a2.db2 = G(gb, FAL_B_LN2_B);
-      FAL_TRY(ln_bwd(dt, a2, sm));
+      lnbwd(a2, sm);
       LnBwdArgs a1 = lnb(x, S.mean1, S.rstd1);
       a1.dy1 = W.dh1; a1.g1 = P(bp, FAL_B_LN1_G); a1.dres = dx; a1.dx = dx; a1.dx_lp = dx_lp;
       a1.dg1 = G(gb, FAL_B_LN1_G); a1.db1 = G(gb, FAL_B_LN1_B);
-      FAL_TRY(ln_bwd(dt, a1, sm));
+      lnbwd(a1, sm);
       return;
     }
     // GPT and FAL+: MLP backward, LN2 backward (with the FAL+ first-attention
@@ -557,7 +620,7 @@ struct Run {
       a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
       a2.dgF = G(gb, FAL_B_LNF1_G); a2.dbF = G(gb, FAL_B_LNF1_B);
     }
-    FAL_TRY(ln_bwd(dt, a2, sm));
+    lnbwd(a2, sm);
     const void* da_lp = W.dxm_lp;
     const float* da = W.dxm;
     if (arch == FAL_ARCH_FALPLUS && layer == 0 && D.L > 1) {
@@ -572,7 +635,7 @@ struct Run {
     LnBwdArgs a1 = lnb(x, S.mean1, S.rstd1);
     a1.dy1 = W.dh1; a1.g1 = P(bp, FAL_B_LN1_G); a1.dres = W.dxm; a1.dx = dx; a1.dx_lp = dx_lp;
     a1.dg1 = G(gb, FAL_B_LN1_G); a1.db1 = G(gb, FAL_B_LN1_B);
-    FAL_TRY(ln_bwd(dt, a1, sm));
+    lnbwd(a1, sm);
   }
 };
 
@@ -663,6 +726,7 @@ fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
 
 fal_status_t fal_destroy(fal_ctx_t* ctx) {
   if (!ctx) return FAL_ERR_INVALID_ARG;
+  for (hipEvent_t e : ctx->prof_pool) (void)hipEventDestroy(e);
   (void)hipEventDestroy(ctx->ev_fork);
   (void)hipEventDestroy(ctx->ev_join);
   delete[] ctx->W.slots;
@@ -767,7 +831,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       LnBwdArgs a = r.lnb(xl, W.meanf, W.rstdf);
       a.dy1 = W.dh1; a.g1 = gparam(FAL_P_LNF_G); a.dx = W.dxa; a.dx_lp = W.lp_a;
       a.dg1 = grads + Lo.goff[FAL_P_LNF_G]; a.db1 = grads + Lo.goff[FAL_P_LNF_B];
-      FAL_TRY(ln_bwd(r.dt, a, sm));
+      r.lnbwd(a, sm);
     }
     float *cur = W.dxa, *nxt = W.dxb;
     void *cur_lp = W.lp_a, *nxt_lp = W.lp_b;
@@ -819,6 +883,55 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }
+  return FAL_OK;
+}
+
+fal_status_t fal_profile_enable(fal_ctx_t* ctx, int32_t enable) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (hipStreamSynchronize(ctx->sm) != hipSuccess || hipStreamSynchronize(ctx->sa) != hipSuccess) {
+    ctx->err = "stream synchronisation failed";
+    return FAL_ERR_HIP;
+  }
+  ctx->prof_on = enable != 0;
+  ctx->prof_spans.clear();
+  ctx->prof_used = 0;
+  for (int k = 0; k < FAL_PROF_NCLASS; ++k) {
+    ctx->prof_n[k] = 0; ctx->prof_ms[k] = ctx->prof_flops[k] = ctx->prof_bytes[k] = 0.0;
+  }
+  while (enable && ctx->prof_pool.size() < 4096) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) { ctx->err = "hipEventCreate failed"; return FAL_ERR_HIP; }
+    ctx->prof_pool.push_back(e);
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_profile_read(fal_ctx_t* ctx, int32_t cls, int64_t* launches, double* total_ms,
+                              double* flops, double* bytes) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (cls < 0 || cls >= FAL_PROF_NCLASS) return bad(ctx, "unknown profile class");
+  if (!ctx->prof_spans.empty()) {
+    if (hipStreamSynchronize(ctx->sm) != hipSuccess || hipStreamSynchronize(ctx->sa) != hipSuccess) {
+      ctx->err = "stream synchronisation failed";
+      return FAL_ERR_HIP;
+    }
+    for (const ProfSpan& sp : ctx->prof_spans) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, sp.a, sp.b) != hipSuccess) { ctx->err = "hipEventElapsedTime failed"; return FAL_ERR_HIP; }
+      ctx->prof_n[sp.cls] += 1;
+      ctx->prof_ms[sp.cls] += ms;
+      ctx->prof_flops[sp.cls] += sp.flops;
+      ctx->prof_bytes[sp.cls] += sp.bytes;
+    }
+    ctx->prof_spans.clear();
+    ctx->prof_used = 0;
+  }
+  if (launches) *launches = ctx->prof_n[cls];
+  if (total_ms) *total_ms = ctx->prof_ms[cls];
+  if (flops) *flops = ctx->prof_flops[cls];
+  if (bytes) *bytes = ctx->prof_bytes[cls];
   return FAL_OK;
 }
 

@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, byref, c_char_p, c_float, c_int32, c_int64, c_size_t, c_void_p
+from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_void_p
 
 import numpy as np
 
@@ -27,8 +27,10 @@ BLOCK_TENSORS = BLOCK_NAMES
 ABI_FUNCTIONS = (
     "fal_validate_config", "fal_param_layout", "fal_workspace_bytes", "fal_init", "fal_destroy",
     "fal_block_fwd", "fal_block_bwd", "fal_model_step", "fal_stack_step", "fal_residual_out",
-    "fal_status_string", "fal_last_error",
+    "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error",
 )
+PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM = range(4)
+PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm"}
 
 
 class fal_config_t(ctypes.Structure):
@@ -68,6 +70,9 @@ def lib():
         L.fal_model_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_stack_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_residual_out.argtypes = [c_void_p, POINTER(c_void_p)]
+        L.fal_profile_enable.argtypes = [c_void_p, c_int32]
+        L.fal_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_int64), POINTER(c_double),
+                                       POINTER(c_double), POINTER(c_double)]
         L.fal_status_string.argtypes = [c_int32]
         L.fal_status_string.restype = c_char_p
         L.fal_last_error.argtypes = [c_void_p]
@@ -238,6 +243,17 @@ class Fal:
                                    c_void_p(dx_in.data_ptr()),
                                    c_void_p(dfirst.data_ptr()) if dfirst is not None else None,
                                    c_void_p(self.block_grad_ptr(layer))), self.ctx)
+
+    def profile_enable(self, on: bool = True):
+        _check(lib().fal_profile_enable(self.ctx, 1 if on else 0), self.ctx)
+
+    def profile_read(self) -> dict:
+        out = {}
+        for cls, name in PROF_NAMES.items():
+            n, ms, fl, by = c_int64(), c_double(), c_double(), c_double()
+            _check(lib().fal_profile_read(self.ctx, cls, byref(n), byref(ms), byref(fl), byref(by)), self.ctx)
+            out[name] = {"launches": n.value, "ms": ms.value, "flops": fl.value, "bytes": by.value}
+        return out
 
     def residual_out(self):
         p = c_void_p()
