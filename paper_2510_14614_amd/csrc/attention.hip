@@ -89,19 +89,31 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
   }
 }
 
-// D[b, h, t] = sum_c dO[t, h*HD + c] * O[t, h*HD + c]
+// D[b, h, t] = sum_c dO[t, h*HD + c] * O[t, h*HD + c]; consecutive threads
+// take consecutive heads of one row, reading 8 elements at a time.
 template <typename S>
 __global__ __launch_bounds__(256) void attn_bwd_dot(const S* O, int64_t ldo, const S* dO, int64_t lddo,
                                                     int B, int T, int H, int HD, float* Dvec) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (int64_t)B * H * T) return;
-  const int t = i % T;
-  const int h = (i / T) % H;
-  const int b = i / ((int64_t)T * H);
-  const int64_t row = (int64_t)b * T + t;
+  const int h = i % H;
+  const int64_t row = i / H;
+  const int t = row % T, b = row / T;
+  const S* o = O + row * ldo + h * HD;
+  const S* g = dO + row * lddo + h * HD;
   float s = 0.f;
-  for (int c = 0; c < HD; ++c) s += to_f(O[row * ldo + h * HD + c]) * to_f(dO[row * lddo + h * HD + c]);
-  Dvec[i] = s;
+  for (int c = 0; c < HD; c += 8) {
+    S a[8], e[8];
+    *reinterpret_cast<uint4*>(a) = *reinterpret_cast<const uint4*>(o + c);
+    *reinterpret_cast<uint4*>(e) = *reinterpret_cast<const uint4*>(g + c);
+    if (sizeof(S) == 4) {
+      *reinterpret_cast<uint4*>(a + 4) = *reinterpret_cast<const uint4*>(o + c + 4);
+      *reinterpret_cast<uint4*>(e + 4) = *reinterpret_cast<const uint4*>(g + c + 4);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += to_f(a[j]) * to_f(e[j]);
+  }
+  Dvec[((int64_t)b * H + h) * T + t] = s;
 }
 
 template <typename S, int HD>
@@ -249,8 +261,15 @@ static hipError_t dispatch_hd(int hd, F&& f) {
   return hipErrorInvalidValue;
 }
 
+bool attn_mfma_supported(int hd);
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
+                                hipStream_t s);
+hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, const float* lse, const float* Dvec,
+                                int B, int T, int H, int hd, void* dqkv, hipStream_t s);
+
 hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
                     float* lse, hipStream_t s) {
+  if (dt == BF16 && attn_mfma_supported(hd)) return attn_fwd_mfma_launch(qkv, B, T, H, hd, O, ldo, lse, s);
   const dim3 grid(cdiv(T, ABR), H, B), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
@@ -277,6 +296,8 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
                        static_cast<const float*>(O), ldo, static_cast<const float*>(dO), lddo, B, T, H, hd, Dvec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (dt == BF16 && attn_mfma_supported(hd))
+    return attn_bwd_mfma_launch(qkv, dO, lddo, lse, Dvec, B, T, H, hd, dqkv, s);
   const dim3 grid(cdiv(T, ABR), H, B), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;

@@ -1,0 +1,428 @@
+// Causal attention on the gfx950 matrix cores (bf16 in, fp32 accumulate),
+// head_dim 64 or 128.  Same mathematics as the SIMT kernels in
+// attention.hip (blockwise, online softmax, deterministic backward), laid
+// out for v_mfma_f32_32x32x16_bf16:
+//
+//  * A wavefront owns 32 rows of the "outer" sequence dimension (queries in
+//    the forward and dQ kernels, keys in the dK/dV kernel); a workgroup of
+//    four wavefronts owns 128.  The other dimension streams through LDS in
+//    tiles of 64 rows.
+//  * Forward computes S^T = K Q^T, so each lane holds 16 scores of one query
+//    and the row max/sum need one cross-lane exchange (lane ^ 32).  The
+//    accumulator registers of S^T are exactly the B operand of O^T = V^T P^T
+//    (the contraction index order of A and B only has to agree), so P never
+//    leaves registers; V is transposed on its way into LDS.
+//  * dK/dV kernel computes S = Q K^T and dP = dO V^T per key block; P^T and
+//    dS^T feed dV += P^T dO and dK += dS^T Q straight from registers, with
+//    dO and Q transposed in LDS.
+//  * dQ kernel computes S^T and dP^T per query block and accumulates
+//    dQ^T += K^T dS^T.
+// Accumulator layout of one 32x32 tile: lane l, register r holds
+// C[8*(r/4) + 4*(l/32) + r%4][l%32].
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace fal {
+
+typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4v __attribute__((ext_vector_type(4)));
+typedef float f32x16v __attribute__((ext_vector_type(16)));
+
+constexpr int AT = 64;        // rows per LDS tile of the streamed dimension
+constexpr int ATP = AT + 8;   // padded row of a transposed tile ([dim][row])
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ f32x16v mfma32(bf16x8v a, bf16x8v b, f32x16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16v zero16() {
+  f32x16v z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// 8 bf16 made of two runs of 4 (each 8 bytes, 8-byte aligned)
+__device__ __forceinline__ bf16x8v ld_2x4(const bf16* p0, const bf16* p1) {
+  const bf16x4v a = *reinterpret_cast<const bf16x4v*>(p0);
+  const bf16x4v b = *reinterpret_cast<const bf16x4v*>(p1);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+__device__ __forceinline__ bf16x8v pack8(const f32x16v& v, int base) {
+  bf16x8v o;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) o[j] = static_cast<bf16>(v[base + j]);
+  return o;
+}
+
+// Row r of the 32x32 accumulator tile held by lane group g.
+__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// Copy AT rows (row0..row0+AT-1, zero past T) of a head slice into LDS,
+// row-major [row][HD + 8].
+template <int HD>
+__device__ __forceinline__ void tile_rows(bf16* s, const bf16* src, int64_t ld, int row0, int T, int tid) {
+  constexpr int CH = HD / 8;
+  for (int i = tid; i < AT * CH; i += 256) {
+    const int r = i / CH, c = (i % CH) * 8, row = row0 + r;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row < T) v = *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c);
+    *reinterpret_cast<uint4*>(s + r * (HD + 8) + c) = v;
+  }
+}
+
+// Same rows, stored transposed: [dim][AT + 8].  Each unit is 4 rows x 8 dims.
+template <int HD>
+__device__ __forceinline__ void tile_rows_t(bf16* s, const bf16* src, int64_t ld, int row0, int T, int tid) {
+  constexpr int CH = HD / 8;
+  for (int i = tid; i < (AT / 4) * CH; i += 256) {
+    const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = row0 + rg + j;
+      v[j] = row < T ? *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c) : make_uint4(0, 0, 0, 0);
+    }
+    const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
+    const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
+    const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
+    const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint2 lo, hi;
+      lo.x = (w0[q] & 0xFFFFu) | (w1[q] << 16);
+      lo.y = (w2[q] & 0xFFFFu) | (w3[q] << 16);
+      hi.x = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
+      hi.y = (w2[q] >> 16) | (w3[q] & 0xFFFF0000u);
+      *reinterpret_cast<uint2*>(s + (c + 2 * q) * ATP + rg) = lo;
+      *reinterpret_cast<uint2*>(s + (c + 2 * q + 1) * ATP + rg) = hi;
+    }
+  }
+}
+
+// A or B operand fragment from a row-major LDS tile: row `row`, dims
+// 16*kk + 8*g .. +7.
+template <int HD>
+__device__ __forceinline__ bf16x8v frag_rows(const bf16* s, int row, int kk, int g) {
+  return *reinterpret_cast<const bf16x8v*>(s + row * (HD + 8) + 16 * kk + 8 * g);
+}
+
+// Operand fragment from a transposed LDS tile for a contraction over the
+// tile's rows: dim `dim`, rows {16*ks + 8*(j/4) + 4*g + j%4}.
+__device__ __forceinline__ bf16x8v frag_cols(const bf16* s, int dim, int rowbase, int ks, int g) {
+  const bf16* p = s + dim * ATP + rowbase + 16 * ks + 4 * g;
+  return ld_2x4(p, p + 8);
+}
+
+// Operand fragment straight from global memory (row of a head slice).
+template <int HD>
+__device__ __forceinline__ bf16x8v frag_global(const bf16* src, int64_t ld, int row, int T, int kk, int g) {
+  if (row >= T) {
+    bf16x8v z;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) z[j] = static_cast<bf16>(0.f);
+    return z;
+  }
+  return *reinterpret_cast<const bf16x8v*>(src + (int64_t)row * ld + 16 * kk + 8 * g);
+}
+
+// ------------------------------------------------------------- forward --
+template <int HD>
+__global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int H, bf16* O, int64_t ldo,
+                                                     float* lse) {
+  constexpr int KK = HD / 16, NT = HD / 32;
+  __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sVt[HD * ATP];
+  const int qb = gridDim.x - 1 - blockIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
+  const bf16* Kg = Qg + dA;
+  const bf16* Vg = Qg + 2 * dA;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
+  const int q0 = qb * 128 + wave * 32;
+  const int tq = q0 + c;
+  const float sl2 = kLog2e / sqrtf((float)HD);
+
+  bf16x8v qf[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) qf[kk] = frag_global<HD>(Qg, ld, tq, T, kk, g);
+  f32x16v acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = zero16();
+  float m = -INFINITY, lsum = 0.f;
+
+  const int kend = min(T, qb * 128 + 128);
+  const int wave_kend = min(T, q0 + 32);
+  for (int k0 = 0; k0 < kend; k0 += AT) {
+    __syncthreads();
+    tile_rows<HD>(sK, Kg, ld, k0, T, tid);
+    tile_rows_t<HD>(sVt, Vg, ld, k0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < AT / 32; ++sub) {
+      const int kb = k0 + 32 * sub;
+      if (kb >= wave_kend) break;
+      f32x16v s = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + acc_row(r, g);
+        const float v = (key <= tq && key < T) ? s[r] * sl2 : -INFINITY;
+        s[r] = v;
+        mx = fmaxf(mx, v);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(m, mx);
+      const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
+      lsum *= alpha;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = (mn == -INFINITY) ? 0.f : exp2f(s[r] - mn);
+        s[r] = p;
+        lsum += p;
+      }
+      m = mn;
+      const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        acc[t] = mfma32(frag_cols(sVt, 32 * t + c, 32 * sub, 0, g), p0, acc[t]);
+        acc[t] = mfma32(frag_cols(sVt, 32 * t + c, 32 * sub, 1, g), p1, acc[t]);
+      }
+    }
+  }
+  const float l = lsum + __shfl_xor(lsum, 32, 64);
+  if (tq < T) {
+    const float inv = 1.f / l;
+    bf16* orow = O + ((int64_t)b * T + tq) * ldo + h * HD;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        bf16x4v o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = static_cast<bf16>(acc[t][4 * r4 + j] * inv);
+        *reinterpret_cast<bf16x4v*>(orow + 32 * t + 8 * r4 + 4 * g) = o;
+      }
+    if (g == 0) lse[((int64_t)b * H + h) * T + tq] = (m + log2f(l)) * 0.6931471805599453f;
+  }
+}
+
+// ------------------------------------------------------- backward: dK dV --
+template <int HD>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
+                                                          const float* lse, const float* Dvec, int T, int H,
+                                                          bf16* dqkv) {
+  constexpr int KK = HD / 16, NT = HD / 32;
+  __shared__ __attribute__((aligned(16))) bf16 sQ[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sdO[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sQt[HD * ATP];
+  __shared__ __attribute__((aligned(16))) bf16 sdOt[HD * ATP];
+  __shared__ float sL[AT], sD[AT];
+  const int kb0 = blockIdx.x * 128;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
+  const bf16* Kg = Qg + dA;
+  const bf16* Vg = Qg + 2 * dA;
+  const bf16* dOg = dO + (int64_t)b * T * lddo + h * HD;
+  const float* Lg = lse + ((int64_t)b * H + h) * T;
+  const float* Dg = Dvec + ((int64_t)b * H + h) * T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
+  const int kw = kb0 + wave * 32;  // this wave's first key
+  const int key = kw + c;          // this lane's key (column of S)
+  const float sl2 = kLog2e / sqrtf((float)HD);
+
+  bf16x8v kf[KK], vf[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    kf[kk] = frag_global<HD>(Kg, ld, key, T, kk, g);
+    vf[kk] = frag_global<HD>(Vg, ld, key, T, kk, g);
+  }
+  f32x16v dk[NT], dv[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) { dk[t] = zero16(); dv[t] = zero16(); }
+
+  for (int q0 = kb0; q0 < T; q0 += AT) {
+    __syncthreads();
+    tile_rows<HD>(sQ, Qg, ld, q0, T, tid);
+    tile_rows<HD>(sdO, dOg, lddo, q0, T, tid);
+    tile_rows_t<HD>(sQt, Qg, ld, q0, T, tid);
+    tile_rows_t<HD>(sdOt, dOg, lddo, q0, T, tid);
+    if (tid < AT) {
+      const int tq = q0 + tid;
+      sL[tid] = tq < T ? Lg[tq] * kLog2e : 0.f;
+      sD[tid] = tq < T ? Dg[tq] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < AT / 32; ++sub) {
+      const int qs = q0 + 32 * sub;
+      if (qs + 31 < kw || qs >= T) continue;  // whole sub-tile before this wave's keys
+      f32x16v s = zero16(), dp = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        s = mfma32(frag_rows<HD>(sQ, 32 * sub + c, kk, g), kf[kk], s);
+        dp = mfma32(frag_rows<HD>(sdO, 32 * sub + c, kk, g), vf[kk], dp);
+      }
+      // s[r] = S[query qs + acc_row(r, g)][key]
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qr = 32 * sub + acc_row(r, g);
+        const int tq = q0 + qr;
+        const float p = (tq < T && key <= tq && key < T) ? exp2f(s[r] * sl2 - sL[qr]) : 0.f;
+        s[r] = p;
+        dp[r] = p * (dp[r] - sD[qr]);
+      }
+      const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
+      const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        dv[t] = mfma32(p0, frag_cols(sdOt, 32 * t + c, 32 * sub, 0, g), dv[t]);
+        dv[t] = mfma32(p1, frag_cols(sdOt, 32 * t + c, 32 * sub, 1, g), dv[t]);
+        dk[t] = mfma32(d0, frag_cols(sQt, 32 * t + c, 32 * sub, 0, g), dk[t]);
+        dk[t] = mfma32(d1, frag_cols(sQt, 32 * t + c, 32 * sub, 1, g), dk[t]);
+      }
+    }
+  }
+  // dk[t][r] = dK[key kw + acc_row(r, g)][dim 32t + c]
+  const float scale = 1.f / sqrtf((float)HD);
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int kr = kw + acc_row(r, g);
+      if (kr < T) {
+        bf16* row = dqkv + ((int64_t)b * T + kr) * ld + h * HD + 32 * t + c;
+        row[dA] = static_cast<bf16>(dk[t][r] * scale);
+        row[2 * dA] = static_cast<bf16>(dv[t][r]);
+      }
+    }
+}
+
+// ----------------------------------------------------------- backward: dQ --
+template <int HD>
+__global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
+                                                        const float* lse, const float* Dvec, int T, int H,
+                                                        bf16* dqkv) {
+  constexpr int KK = HD / 16, NT = HD / 32;
+  __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sKt[HD * ATP];
+  const int qb = gridDim.x - 1 - blockIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int dA = H * HD;
+  const int64_t ld = 3 * (int64_t)dA;
+  const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
+  const bf16* Kg = Qg + dA;
+  const bf16* Vg = Qg + 2 * dA;
+  const bf16* dOg = dO + (int64_t)b * T * lddo + h * HD;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
+  const int q0 = qb * 128 + wave * 32;
+  const int tq = q0 + c;
+  const float sl2 = kLog2e / sqrtf((float)HD);
+
+  bf16x8v qf[KK], of[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    qf[kk] = frag_global<HD>(Qg, ld, tq, T, kk, g);
+    of[kk] = frag_global<HD>(dOg, lddo, tq, T, kk, g);
+  }
+  const float L2 = tq < T ? lse[((int64_t)b * H + h) * T + tq] * kLog2e : 0.f;
+  const float Dq = tq < T ? Dvec[((int64_t)b * H + h) * T + tq] : 0.f;
+  f32x16v dq[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dq[t] = zero16();
+
+  const int kend = min(T, qb * 128 + 128);
+  const int wave_kend = min(T, q0 + 32);
+  for (int k0 = 0; k0 < kend; k0 += AT) {
+    __syncthreads();
+    tile_rows<HD>(sK, Kg, ld, k0, T, tid);
+    tile_rows<HD>(sV, Vg, ld, k0, T, tid);
+    tile_rows_t<HD>(sKt, Kg, ld, k0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < AT / 32; ++sub) {
+      const int kb = k0 + 32 * sub;
+      if (kb >= wave_kend) break;
+      f32x16v s = zero16(), dp = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
+        dp = mfma32(frag_rows<HD>(sV, 32 * sub + c, kk, g), of[kk], dp);
+      }
+      // s[r] = S^T[key kb + acc_row(r, g)][query tq]
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int k = kb + acc_row(r, g);
+        const float p = (tq < T && k <= tq && k < T) ? exp2f(s[r] * sl2 - L2) : 0.f;
+        dp[r] = p * (dp[r] - Dq);
+      }
+      const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        dq[t] = mfma32(frag_cols(sKt, 32 * t + c, 32 * sub, 0, g), d0, dq[t]);
+        dq[t] = mfma32(frag_cols(sKt, 32 * t + c, 32 * sub, 1, g), d1, dq[t]);
+      }
+    }
+  }
+  if (tq < T) {
+    const float scale = 1.f / sqrtf((float)HD);
+    bf16* row = dqkv + ((int64_t)b * T + tq) * ld + h * HD;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        bf16x4v o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = static_cast<bf16>(dq[t][4 * r4 + j] * scale);
+        *reinterpret_cast<bf16x4v*>(row + 32 * t + 8 * r4 + 4 * g) = o;
+      }
+  }
+}
+
+bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
+
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
+                                hipStream_t s) {
+  const dim3 grid(cdiv(T, 128), H, B), block(256);
+  const bf16* q = static_cast<const bf16*>(qkv);
+  bf16* o = static_cast<bf16*>(O);
+  if (hd == 64) hipLaunchKernelGGL((attn_fwd_mfma<64>), grid, block, 0, s, q, T, H, o, ldo, lse);
+  else if (hd == 128) hipLaunchKernelGGL((attn_fwd_mfma<128>), grid, block, 0, s, q, T, H, o, ldo, lse);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, const float* lse, const float* Dvec,
+                                int B, int T, int H, int hd, void* dqkv, hipStream_t s) {
+  const dim3 grid(cdiv(T, 128), H, B), block(256);
+  const bf16* q = static_cast<const bf16*>(qkv);
+  const bf16* d = static_cast<const bf16*>(dO);
+  bf16* o = static_cast<bf16*>(dqkv);
+  if (hd == 64) {
+    hipLaunchKernelGGL((attn_bwd_dkdv_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    hipLaunchKernelGGL((attn_bwd_dq_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+  } else if (hd == 128) {
+    hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    hipLaunchKernelGGL((attn_bwd_dq_mfma<128>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fal

@@ -75,3 +75,17 @@ def test_stack_step_shard_shapes(arch, dtype):
     ref = oracle.stack_step(cfg, blocks, x1, gout)
     ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
     compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"stack a{arch} dt{dtype}")
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL])
+def test_long_sequence_multi_block_attention(arch, hd):
+    # several 128-query blocks with a ragged last block exercise the causal
+    # tiling of the matrix-core attention kernels (forward and backward)
+    cfg = Config(n_layer=2, d_model=2 * hd, n_head=2, head_dim=hd, d_ff=384, vocab=512, seq_len=300,
+                 batch=2, arch=arch, dtype=1)
+    log(f"long sequence arch={arch} hd={hd}")
+    g, blocks = synth.make_params(cfg, seed=8)
+    tok = synth.make_tokens(cfg, seed=9, dist="zipf")
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"long a{arch} hd{hd}")
