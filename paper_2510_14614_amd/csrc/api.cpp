@@ -161,6 +161,8 @@ struct Work {
   void* first_in;              // first-attention tensor of the current step
   float* Dvec;
   float *part_main, *part_aux;
+  float *splitk_main, *splitk_aux;  // split-K partials, one region per stream
+  int64_t splitk_floats;
   int32_t* keys;
   float* loss_tmp;
 };
@@ -223,6 +225,11 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
                                           dot_scratch(M * d)});
   W.part_main = cv.take<float>(part);
   W.part_aux = cv.take<float>(part);
+  // a split is only chosen while fewer than 512 output tiles of 128x128
+  // exist, so (512 + 512) tiles of partials bound every split decision
+  W.splitk_floats = (int64_t)1024 * 128 * 128;
+  W.splitk_main = cv.take<float>(W.splitk_floats);
+  W.splitk_aux = cv.take<float>(W.splitk_floats);
   W.loss_tmp = cv.take<float>(64);
   W.first_in = W.first;
   *total = cv.off + kAlignBytes;
@@ -318,7 +325,9 @@ struct Run {
                (double)q.M * q.N * ((q.out_f32 || q.epi == EPI_RESID) ? 4.0 : (double)ctx->D.es);
     }
     Span span(ctx, FAL_PROF_GEMM, s, flops, bytes);
-    hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why);
+    const bool aux = s == ctx->sa && ctx->sa != ctx->sm;
+    hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why, aux ? ctx->W.splitk_aux : ctx->W.splitk_main,
+                             ctx->W.splitk_floats);
     if (e != hipSuccess) {
       ctx->err = std::string("gemm: ") + (why ? why : hipGetErrorString(e));
       throw Fail{};

@@ -12,6 +12,8 @@
 //  * gemm_simt: fp32 FMA kernel (fp32 parity mode).
 // Both launch every problem of a group in one grid, so the independent
 // GEMMs of FAL's two branches can share a launch.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -115,89 +117,106 @@ __global__ __launch_bounds__(256) void gemm_simt(GemmGroup g, int gelu_tanh) {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int MT = 128, NT = 128, KT = 64, LDK = KT + 8;  // LDS row: 72 bf16 = 144 B
+constexpr int KT = 64, LDK = KT + 8;  // LDS row: 72 bf16 = 144 B (conflict-free 16 B reads)
 
-// Rows r0.. of a k-contiguous operand: 128 rows x 64 k = 1024 16-byte chunks,
-// 4 per thread.  Chunks past K are zero-filled element-wise.
-__device__ __forceinline__ void load_kmaj(uint4 (&r)[4], const bf16* X, int64_t ld, int r0, int R,
-                                          int k0, int K, int tid) {
+// Global -> register staging of one operand tile (R rows of the output
+// dimension x KT of k).  Loads are unconditional (out-of-range chunks read a
+// clamped in-bounds address) so that every load of a tile is in flight at
+// once; the validity of each chunk is applied when the registers are written
+// to LDS, after the MFMA phase has given the loads time to land.
+template <int R, int KMAJ>
+struct Stage {
+  // k-contiguous: R*KT/8 chunks of 8; mn-contiguous: units of 4 k x 8 mn.
+  static constexpr int NC = KMAJ ? R * KT / 8 / 256 : 4 * (R * KT / 32) / 256;
+  uint4 v[NC];
+  int nvalid[NC];  // valid elements of the chunk (k-contiguous) or 0/8
+
+  __device__ __forceinline__ void load(const bf16* X, int64_t ld, int r0, int Rmax, int k0, int K, int tid) {
+    if (KMAJ) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
-    const int gr = r0 + row, gk = k0 + kc;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (gr < R && gk < K) {
-      v = *reinterpret_cast<const uint4*>(X + (int64_t)gr * ld + gk);
-      if (gk + 8 > K) {
-        uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+      for (int i = 0; i < NC; ++i) {
+        const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
+        const int gr = r0 + row, gk = k0 + kc;
+        const bool ok = gr < Rmax && gk < K;
+        nvalid[i] = ok ? min(8, K - gk) : 0;
+        const bf16* p = ok ? X + (int64_t)gr * ld + gk : X;
+        v[i] = *reinterpret_cast<const uint4*>(p);
+      }
+    } else {
+      // unit u: 4 consecutive k rows x 8 consecutive columns
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-          if (gk + q >= K) e[q] = 0;
+      for (int u = 0; u < NC / 4; ++u) {
+        const int id = tid + 256 * u;
+        const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int gk = k0 + kg + j, gr = r0 + mc;
+          const bool ok = gk < K && gr < Rmax;
+          nvalid[4 * u + j] = ok ? 8 : 0;
+          const bf16* p = ok ? X + (int64_t)gk * ld + gr : X;
+          v[4 * u + j] = *reinterpret_cast<const uint4*>(p);
+        }
       }
     }
-    r[i] = v;
   }
-}
 
-__device__ __forceinline__ void store_kmaj(const uint4 (&r)[4], bf16* s, int tid) {
+  __device__ __forceinline__ void store(bf16* s, int tid) const {
+    if (KMAJ) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
-    *reinterpret_cast<uint4*>(s + row * LDK + kc) = r[i];
-  }
-}
-
-// Rows r0.. of an operand whose rows are contiguous along m (or n): 64 k
-// rows x 128 columns.  Thread: 4 consecutive k x 8 consecutive columns.
-__device__ __forceinline__ void load_mnmaj(uint4 (&r)[4], const bf16* X, int64_t ld, int r0, int R,
-                                           int k0, int K, int tid) {
-  const int kg = (tid & 15) * 4, mc = (tid >> 4) * 8;
+      for (int i = 0; i < NC; ++i) {
+        const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
+        uint4 w = v[i];
+        if (nvalid[i] < 8) {
+          uint16_t* e = reinterpret_cast<uint16_t*>(&w);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int gk = k0 + kg + j, gr = r0 + mc;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (gk < K && gr < R) v = *reinterpret_cast<const uint4*>(X + (int64_t)gk * ld + gr);
-    r[j] = v;
-  }
-}
-
-// Transpose the 4 (k) x 8 (column) block in registers and store it as 8
-// k-contiguous LDS rows of 4 elements.
-__device__ __forceinline__ void store_mnmaj(const uint4 (&r)[4], bf16* s, int tid) {
-  const int kg = (tid & 15) * 4, mc = (tid >> 4) * 8;
-  const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&r[0]);
-  const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&r[1]);
-  const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&r[2]);
-  const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&r[3]);
+          for (int q = 0; q < 8; ++q)
+            if (q >= nvalid[i]) e[q] = 0;
+        }
+        *reinterpret_cast<uint4*>(s + row * LDK + kc) = w;
+      }
+    } else {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    // columns 2q (low halves) and 2q+1 (high halves)
-    uint2 lo, hi;
-    lo.x = (w0[q] & 0xFFFFu) | (w1[q] << 16);
-    lo.y = (w2[q] & 0xFFFFu) | (w3[q] << 16);
-    hi.x = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
-    hi.y = (w2[q] >> 16) | (w3[q] & 0xFFFF0000u);
-    *reinterpret_cast<uint2*>(s + (mc + 2 * q) * LDK + kg) = lo;
-    *reinterpret_cast<uint2*>(s + (mc + 2 * q + 1) * LDK + kg) = hi;
+      for (int u = 0; u < NC / 4; ++u) {
+        const int id = tid + 256 * u;
+        const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
+        uint32_t w[4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint4 x = nvalid[4 * u + j] ? v[4 * u + j] : make_uint4(0, 0, 0, 0);
+          w[j][0] = x.x; w[j][1] = x.y; w[j][2] = x.z; w[j][3] = x.w;
+        }
+        // transpose 4 (k) x 8 (mn) into 8 k-contiguous rows of 4
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint2 lo, hi;
+          lo.x = (w[0][q] & 0xFFFFu) | (w[1][q] << 16);
+          lo.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
+          hi.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
+          hi.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
+          *reinterpret_cast<uint2*>(s + (mc + 2 * q) * LDK + kg) = lo;
+          *reinterpret_cast<uint2*>(s + (mc + 2 * q + 1) * LDK + kg) = hi;
+        }
+      }
+    }
   }
-}
+};
 
-// Epilogue of one wavefront's 64x64 accumulator block; one instantiation per
-// epilogue kind keeps every accumulator index a compile-time constant.
-template <int EPI, int F32OUT>
-__device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t (&acc)[4][4], int mb, int nb,
+// Epilogue of one wavefront's (FM*16) x (FN*16) accumulator block; one
+// instantiation per epilogue kind keeps every accumulator index constant.
+template <int EPI, int F32OUT, int FM, int FN>
+__device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], int mb, int nb,
                                             int gelu_tanh) {
   const bf16* bias = static_cast<const bf16*>(P.bias);
   const bf16* bias2 = static_cast<const bf16*>(P.bias2);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < FN; ++j) {
     const int n = nb + j * 16;
     if (n >= P.N) continue;
     float bn = 0.f;
     if (bias) bn += to_f(bias[n]);
     if (bias2) bn += to_f(bias2[n]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb + i * 16 + r;
@@ -220,78 +239,135 @@ __device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t 
   }
 }
 
-template <int AK, int BKM>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh) {
-  __shared__ __attribute__((aligned(16))) bf16 sA[MT * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[NT * LDK];
+// BM x BN output tile per 256-thread workgroup, 2 x 2 wavefronts of
+// (BM/2) x (BN/2), K staged through two LDS buffers 64 at a time.
+template <int AK, int BKM, int BM, int BN>
+__global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh) {
+  constexpr int FM = BM / 32, FN = BN / 32;  // 16x16 fragments per wavefront
+  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * LDK];
   const GemmProblem P = find_problem(g, blockIdx.x);
-  const int local = blockIdx.x - P.tile_start;
-  const int m0 = (local / P.tiles_n) * MT, n0 = (local % P.tiles_n) * NT;
+  const int per_split = P.tiles_m * P.tiles_n;
+  const int local = (blockIdx.x - P.tile_start) % per_split;
+  const int split = (blockIdx.x - P.tile_start) / per_split;
+  const int m0 = (local / P.tiles_n) * BM, n0 = (local % P.tiles_n) * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nt1 = (P.K + KT - 1) / KT;
-  const int nt = nt1 + (P.K2 > 0 ? (P.K2 + KT - 1) / KT : 0);
-  uint4 ra[4], rb[4];
-
-  auto fetch = [&](int t) {
-    const int seg = t >= nt1;
+  int nt = nt1 + (P.K2 > 0 ? (P.K2 + KT - 1) / KT : 0);
+  int tbeg = 0;
+  if (P.splits > 1) {  // single K segment: this slice covers k-tiles [tbeg, tbeg + nt)
+    const int per = (nt1 + P.splits - 1) / P.splits;
+    tbeg = split * per;
+    nt = max(0, min(nt1, tbeg + per) - tbeg);
+  }
+  Stage<BM, AK> sa;
+  Stage<BN, BKM> sb;
+  auto fetch = [&](int tt) {
+    const int t = tt + tbeg;
+    const bool seg = t >= nt1;
     const bf16* A = static_cast<const bf16*>(seg ? P.A2 : P.A);
     const bf16* B = static_cast<const bf16*>(seg ? P.B2 : P.B);
     const int64_t lda = seg ? P.lda2 : P.lda, ldb = seg ? P.ldb2 : P.ldb;
     const int K = seg ? P.K2 : P.K;
     const int k0 = (seg ? t - nt1 : t) * KT;
-    if (AK) load_kmaj(ra, A, lda, m0, P.M, k0, K, tid);
-    else load_mnmaj(ra, A, lda, m0, P.M, k0, K, tid);
-    if (BKM) load_kmaj(rb, B, ldb, n0, P.N, k0, K, tid);
-    else load_mnmaj(rb, B, ldb, n0, P.N, k0, K, tid);
+    sa.load(A, lda, m0, P.M, k0, K, tid);
+    sb.load(B, ldb, n0, P.N, k0, K, tid);
   };
 
-  fetch(0);
+  if (nt > 0) {
+    fetch(0);
+    sa.store(sA[0], tid);
+    sb.store(sB[0], tid);
+  }
+  __syncthreads();
   for (int t = 0; t < nt; ++t) {
-    if (AK) store_kmaj(ra, sA, tid); else store_mnmaj(ra, sA, tid);
-    if (BKM) store_kmaj(rb, sB, tid); else store_mnmaj(rb, sB, tid);
-    __syncthreads();
+    const int cur = t & 1;
     if (t + 1 < nt) fetch(t + 1);
+    const bf16* a_s = sA[cur];
+    const bf16* b_s = sB[cur];
 #pragma unroll
     for (int ks = 0; ks < KT / 32; ++ks) {
-      bf16x8_t a[4], b[4];
+      bf16x8_t a[FM], b[FN];
       const int koff = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf16x8_t*>(sA + (wm * 64 + i * 16 + (lane & 15)) * LDK + koff);
+      for (int i = 0; i < FM; ++i)
+        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + (wm * (BM / 2) + i * 16 + (lane & 15)) * LDK + koff);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const bf16x8_t*>(sB + (wn * 64 + j * 16 + (lane & 15)) * LDK + koff);
+      for (int j = 0; j < FN; ++j)
+        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + (wn * (BN / 2) + j * 16 + (lane & 15)) * LDK + koff);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (t + 1 < nt) {
+      sa.store(sA[cur ^ 1], tid);
+      sb.store(sB[cur ^ 1], tid);
     }
     __syncthreads();
   }
 
   // acc[i][j][r] holds C[row 4*(lane/16) + r][col lane%16] of 16x16 tile (i, j).
-  const int mb = m0 + wm * 64 + (lane >> 4) * 4, nb = n0 + wn * 64 + (lane & 15);
+  const int mb = m0 + wm * (BM / 2) + (lane >> 4) * 4, nb = n0 + wn * (BN / 2) + (lane & 15);
+  if (P.splits > 1) {
+    float* part = P.part + (int64_t)split * P.M * P.N;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = nb + j * 16;
+      if (n >= P.N) continue;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + i * 16 + r;
+          if (m < P.M) part[(int64_t)m * P.N + n] = acc[i][j][r];
+        }
+    }
+    return;
+  }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_tiles<EPI_STORE, 1>(P, acc, mb, nb, gelu_tanh);
-      else store_tiles<EPI_STORE, 0>(P, acc, mb, nb, gelu_tanh);
+      if (P.out_f32) store_tiles<EPI_STORE, 1, FM, FN>(P, acc, mb, nb, gelu_tanh);
+      else store_tiles<EPI_STORE, 0, FM, FN>(P, acc, mb, nb, gelu_tanh);
       break;
-    case EPI_GELU: store_tiles<EPI_GELU, 0>(P, acc, mb, nb, gelu_tanh); break;
-    case EPI_RESID: store_tiles<EPI_RESID, 1>(P, acc, mb, nb, gelu_tanh); break;
-    case EPI_GELU_BWD: store_tiles<EPI_GELU_BWD, 0>(P, acc, mb, nb, gelu_tanh); break;
+    case EPI_GELU: store_tiles<EPI_GELU, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
+    case EPI_RESID: store_tiles<EPI_RESID, 1, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
+    case EPI_GELU_BWD: store_tiles<EPI_GELU_BWD, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
   }
 }
 
+// out[m, n] = sum_s part[s, m, n] (+ bias), s in order.
+__global__ __launch_bounds__(256) void splitk_reduce(const float* part, int splits, int M, int N, const bf16* bias,
+                                                     const bf16* bias2, float* out, int64_t ldo) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)M * N) return;
+  const int m = i / N, n = i % N;
+  const int64_t MN = (int64_t)M * N;
+  float v = 0.f;
+  for (int s = 0; s < splits; ++s) v += part[s * MN + i];
+  if (bias) v += to_f(bias[n]);
+  if (bias2) v += to_f(bias2[n]);
+  out[(int64_t)m * ldo + n] = v;
+}
+
 // ------------------------------------------------------------- launcher --
+#ifndef FAL_GEMM_BM
+#define FAL_GEMM_BM 128
+#endif
+#ifndef FAL_GEMM_BN
+#define FAL_GEMM_BN 128
+#endif
+constexpr int kBM = FAL_GEMM_BM, kBN = FAL_GEMM_BN;
+constexpr int kSplitTarget = 512;  // workgroups to aim for (2 per CU on 256 CUs)
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 static const char* check_vec_operand(const void* X, int64_t ld, int kmaj, int rows, int K) {
@@ -307,10 +383,10 @@ static const char* check_vec_operand(const void* X, int64_t ld, int kmaj, int ro
 }
 
 hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
-                const char** why) {
+                const char** why, float* splitk_scratch, int64_t splitk_floats) {
   *why = nullptr;
   if (g.n < 1 || g.n > kMaxGroup) { *why = "bad GEMM group size"; return hipErrorInvalidValue; }
-  const int tm = dt == BF16 ? MT : ST, tn = dt == BF16 ? NT : ST;
+  const int tm = dt == BF16 ? kBM : ST, tn = dt == BF16 ? kBN : ST;
   int total = 0;
   for (int i = 0; i < g.n; ++i) {
     GemmProblem& P = g.p[i];
@@ -325,24 +401,45 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     P.tiles_m = (P.M + tm - 1) / tm;
     P.tiles_n = (P.N + tn - 1) / tn;
     P.tile_start = total;
+    P.splits = 1;
+    P.part = nullptr;
     total += P.tiles_m * P.tiles_n;
+  }
+  // Split K for launches that would leave compute units idle: aim for two
+  // resident workgroups per CU with at least 512 of K per slice.
+  if (dt == BF16 && splitk_scratch && g.n == 1) {
+    GemmProblem& P = g.p[0];
+    const int tiles = P.tiles_m * P.tiles_n;
+    const int want = (kSplitTarget + tiles - 1) / tiles;
+    int sp = std::min({want, P.K / 512, 8});
+    if (sp > 1 && P.K2 == 0 && P.epi == EPI_STORE && P.out_f32 &&
+        (int64_t)sp * P.M * P.N <= splitk_floats) {
+      P.splits = sp;
+      P.part = splitk_scratch;
+      total = tiles * sp;
+    }
   }
   g.total_tiles = total;
   const dim3 grid(total), block(256);
-#define FAL_GEMM_LAUNCH(KERNEL)                                                              \
-  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((KERNEL<1, 1>), grid, block, 0, s, g, gelu_tanh); \
-  else if (a_kmaj) hipLaunchKernelGGL((KERNEL<1, 0>), grid, block, 0, s, g, gelu_tanh);      \
-  else if (b_kmaj) hipLaunchKernelGGL((KERNEL<0, 1>), grid, block, 0, s, g, gelu_tanh);      \
-  else hipLaunchKernelGGL((KERNEL<0, 0>), grid, block, 0, s, g, gelu_tanh);
   if (dt == BF16) {
-    FAL_GEMM_LAUNCH(gemm_bf16_mfma)
+    if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 1, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
+    else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 0, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
+    else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<0, 1, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
+    else hipLaunchKernelGGL((gemm_bf16_mfma<0, 0, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
+    const GemmProblem& P = g.p[0];
+    if (g.n == 1 && P.splits > 1) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(splitk_reduce, dim3(cdiv((int64_t)P.M * P.N, 256)), dim3(256), 0, s, P.part, P.splits,
+                         P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
+                         static_cast<float*>(P.out), P.ldo);
+    }
   } else {
     if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 1>), grid, block, 0, s, g, gelu_tanh);
     else if (a_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 0>), grid, block, 0, s, g, gelu_tanh);
     else if (b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 0, 1>), grid, block, 0, s, g, gelu_tanh);
     else hipLaunchKernelGGL((gemm_simt<float, 0, 0>), grid, block, 0, s, g, gelu_tanh);
   }
-#undef FAL_GEMM_LAUNCH
   return hipGetLastError();
 }
 

@@ -45,6 +45,8 @@ struct GemmProblem {
   int64_t ldaux;
   // filled in by the launcher
   int tiles_m, tiles_n, tile_start;
+  int splits;        // K split into this many slices (fp32 partials + reduce)
+  float* part;       // [splits][M][N] fp32 partials when splits > 1
 };
 
 constexpr int kMaxGroup = 4;
@@ -55,10 +57,15 @@ struct GemmGroup {
 };
 
 // Launches every problem of `g` (same dtype and operand orientation) as one
-// grouped kernel.  Returns hipSuccess or the launch error; `why` receives a
-// static message for argument errors.
+// grouped kernel.  Problems that would leave most compute units idle (few
+// output tiles, long K, fp32 EPI_STORE output, single K segment) have their
+// K range split across workgroups: each slice writes fp32 partials to
+// `splitk_scratch` and a second kernel sums the slices in a fixed order, so
+// results stay deterministic.  splitk_floats: capacity of the scratch (0
+// disables splitting).  Returns hipSuccess or the launch error; `why`
+// receives a static message for argument errors.
 hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
-                const char** why);
+                const char** why, float* splitk_scratch = nullptr, int64_t splitk_floats = 0);
 
 // ----------------------------------------------------------- LayerNorm ----
 // Row LayerNorm over d of fp32 rows x.  Writes
