@@ -117,7 +117,22 @@ __global__ __launch_bounds__(256) void gemm_simt(GemmGroup g, int gelu_tanh) {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int KT = 64, LDK = KT + 8;  // LDS row: 72 bf16 = 144 B (conflict-free 16 B reads)
+#ifndef FAL_LDS_SWZ
+#define FAL_LDS_SWZ 2
+#endif
+#ifndef FAL_LDS_PAD
+#define FAL_LDS_PAD 8
+#endif
+constexpr int KT = 64;
+// LDS operand tiles are k-contiguous rows of KT elements.  Either padded
+// rows (FAL_LDS_SWZ 0) or unpadded rows whose 16-byte chunks are permuted
+// by an XOR of the row index (FAL_LDS_SWZ 1: row & 7, 2: (row >> 1) & 7).
+constexpr int LDK = FAL_LDS_SWZ ? KT : KT + FAL_LDS_PAD;
+__device__ __forceinline__ int lds_off(int row, int k) {
+  if (FAL_LDS_SWZ == 0) return row * LDK + k;
+  const int f = FAL_LDS_SWZ == 1 ? (row & 7) : ((row >> 1) & 7);
+  return row * LDK + ((((k >> 3) ^ f)) << 3) + (k & 7);
+}
 
 // Global -> register staging of one operand tile (R rows of the output
 // dimension x KT of k).  Loads are unconditional (out-of-range chunks read a
@@ -172,7 +187,7 @@ struct Stage {
           for (int q = 0; q < 8; ++q)
             if (q >= nvalid[i]) e[q] = 0;
         }
-        *reinterpret_cast<uint4*>(s + row * LDK + kc) = w;
+        *reinterpret_cast<uint4*>(s + lds_off(row, kc)) = w;
       }
     } else {
 #pragma unroll
@@ -193,16 +208,15 @@ struct Stage {
           lo.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
           hi.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
           hi.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
-          *reinterpret_cast<uint2*>(s + (mc + 2 * q) * LDK + kg) = lo;
-          *reinterpret_cast<uint2*>(s + (mc + 2 * q + 1) * LDK + kg) = hi;
+          *reinterpret_cast<uint2*>(s + lds_off(mc + 2 * q, kg)) = lo;
+          *reinterpret_cast<uint2*>(s + lds_off(mc + 2 * q + 1, kg)) = hi;
         }
       }
     }
   }
 };
 
-// Epilogue of one wavefront's (FM*16) x (FN*16) accumulator block; one
-// instantiation per epilogue kind keeps every accumulator index constant.
+// Direct epilogue from the accumulator registers (one element per store).
 template <int EPI, int F32OUT, int FM, int FN>
 __device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], int mb, int nb,
                                             int gelu_tanh) {
@@ -239,18 +253,152 @@ __device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t 
   }
 }
 
+// Epilogue of one wavefront's WR x WC block staged in LDS (fp32, columns
+// XOR-permuted in groups of 4 by row to spread banks).  Each lane handles 8
+// consecutive columns of a row: 8 lanes per row, 8 rows per pass.  One
+// instantiation per epilogue kind.
+template <int EPI, int F32OUT, int WR, int WC>
+__device__ __forceinline__ void store_rows(const GemmProblem& P, const float* stage, int rm0, int cn0, int lane,
+                                           int gelu_tanh) {
+  constexpr int LPR = WC / 8;       // lanes per row
+  constexpr int RPP = 64 / LPR;     // rows per pass
+  const bf16* bias = static_cast<const bf16*>(P.bias);
+  const bf16* bias2 = static_cast<const bf16*>(P.bias2);
+  const int c8 = (lane % LPR) * 8;
+  const int n = cn0 + c8;
+  if (n >= P.N) return;
+  const bool full = n + 8 <= P.N;
+  float bn[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    float b = 0.f;
+    if (n + q < P.N) {
+      if (bias) b += to_f(bias[n + q]);
+      if (bias2) b += to_f(bias2[n + q]);
+    }
+    bn[q] = b;
+  }
+#pragma unroll
+  for (int pass = 0; pass < WR / RPP; ++pass) {
+    const int row = pass * RPP + lane / LPR;
+    const int m = rm0 + row;
+    if (m >= P.M) continue;
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = stage[row * WC + ((c8 + q) ^ ((row & 7) << 2))] + bn[q];
+    const int64_t o = (int64_t)m * P.ldo + n;
+    if (EPI == EPI_STORE && F32OUT) {
+      float* dst = static_cast<float*>(P.out) + o;
+      if (full && P.vec_out) {
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        for (int q = 0; q < 8 && n + q < P.N; ++q) dst[q] = v[q];
+      }
+    } else if (EPI == EPI_RESID) {
+      float* dst = static_cast<float*>(P.out) + o;
+      const float* res = P.resid + (int64_t)m * P.ldr + n;
+      if (full && P.vec_out) {
+        const float4 r0 = *reinterpret_cast<const float4*>(res);
+        const float4 r1 = *reinterpret_cast<const float4*>(res + 4);
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0] + r0.x, v[1] + r0.y, v[2] + r0.z, v[3] + r0.w);
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4] + r1.x, v[5] + r1.y, v[6] + r1.z, v[7] + r1.w);
+      } else {
+        for (int q = 0; q < 8 && n + q < P.N; ++q) dst[q] = res[q] + v[q];
+      }
+    } else {
+      bf16 out[8], out2[8];
+      if (EPI == EPI_GELU) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          out2[q] = from_f<bf16>(v[q]);
+          out[q] = from_f<bf16>(gelu_f(v[q], gelu_tanh));
+        }
+      } else if (EPI == EPI_GELU_BWD) {
+        bf16 pre[8];
+        const bf16* ap = static_cast<const bf16*>(P.aux) + (int64_t)m * P.ldaux + n;
+        if (full && P.vec_out) {
+          *reinterpret_cast<uint4*>(pre) = *reinterpret_cast<const uint4*>(ap);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) pre[q] = n + q < P.N ? ap[q] : from_f<bf16>(0.f);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) out[q] = from_f<bf16>(v[q] * gelu_grad_f(to_f(pre[q]), gelu_tanh));
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) out[q] = from_f<bf16>(v[q]);
+      }
+      bf16* dst = static_cast<bf16*>(P.out) + o;
+      if (full && P.vec_out) {
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(out);
+        if (EPI == EPI_GELU)
+          *reinterpret_cast<uint4*>(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n) =
+              *reinterpret_cast<const uint4*>(out2);
+      } else {
+        for (int q = 0; q < 8 && n + q < P.N; ++q) {
+          dst[q] = out[q];
+          if (EPI == EPI_GELU) static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + q] = out2[q];
+        }
+      }
+    }
+  }
+}
+
+// Workgroups are dispatched to the 8 XCDs round-robin by block id.  Map
+// block ids so that each XCD owns one contiguous range of tiles, and order
+// tiles inside a problem in bands of kGroupM tile rows, so that the tiles
+// sharing one XCD's L2 also share A row panels and B column panels.
+#ifndef FAL_GEMM_REMAP
+#define FAL_GEMM_REMAP 1
+#endif
+#ifndef FAL_GEMM_STAGE_EPI
+#define FAL_GEMM_STAGE_EPI 0
+#endif
+#ifndef FAL_GEMM_GROUP_M
+#define FAL_GEMM_GROUP_M 8
+#endif
+constexpr int kXcds = 8, kGroupM = FAL_GEMM_GROUP_M;
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
+  const int q = total / kXcds, r = total % kXcds;
+  const int xcd = bid % kXcds, slot = bid / kXcds;
+  return xcd < r ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
+}
+__device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int band = kGroupM * tiles_n;
+  const int first = (t / band) * kGroupM;
+  const int gs = min(kGroupM, tiles_m - first);
+  const int in = t % band;
+  tm = first + in % gs;
+  tn = in / gs;
+}
+
 // BM x BN output tile per 256-thread workgroup, 2 x 2 wavefronts of
 // (BM/2) x (BN/2), K staged through two LDS buffers 64 at a time.
 template <int AK, int BKM, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh) {
   constexpr int FM = BM / 32, FN = BN / 32;  // 16x16 fragments per wavefront
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * LDK];
-  const GemmProblem P = find_problem(g, blockIdx.x);
+  // one LDS block: two stages of A, two of B; reused for the epilogue
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (BM + BN) * LDK];
+  auto sA = [&](int st) { return smem + st * BM * LDK; };
+  auto sB = [&](int st) { return smem + 2 * BM * LDK + st * BN * LDK; };
+#if FAL_GEMM_REMAP
+  const int bid = xcd_remap(blockIdx.x, g.total_tiles);
+#else
+  const int bid = blockIdx.x;
+#endif
+  const GemmProblem P = find_problem(g, bid);
   const int per_split = P.tiles_m * P.tiles_n;
-  const int local = (blockIdx.x - P.tile_start) % per_split;
-  const int split = (blockIdx.x - P.tile_start) / per_split;
-  const int m0 = (local / P.tiles_n) * BM, n0 = (local % P.tiles_n) * BN;
+  const int local = (bid - P.tile_start) % per_split;
+  const int split = (bid - P.tile_start) / per_split;
+  int tmi, tni;
+#if FAL_GEMM_REMAP
+  grouped_tile(local, P.tiles_m, P.tiles_n, tmi, tni);
+#else
+  tmi = local / P.tiles_n;
+  tni = local % P.tiles_n;
+#endif
+  const int m0 = tmi * BM, n0 = tni * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
@@ -284,25 +432,25 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
 
   if (nt > 0) {
     fetch(0);
-    sa.store(sA[0], tid);
-    sb.store(sB[0], tid);
+    sa.store(sA(0), tid);
+    sb.store(sB(0), tid);
   }
   __syncthreads();
   for (int t = 0; t < nt; ++t) {
     const int cur = t & 1;
     if (t + 1 < nt) fetch(t + 1);
-    const bf16* a_s = sA[cur];
-    const bf16* b_s = sB[cur];
+    const bf16* a_s = sA(cur);
+    const bf16* b_s = sB(cur);
 #pragma unroll
     for (int ks = 0; ks < KT / 32; ++ks) {
       bf16x8_t a[FM], b[FN];
       const int koff = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + (wm * (BM / 2) + i * 16 + (lane & 15)) * LDK + koff);
+        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + lds_off(wm * (BM / 2) + i * 16 + (lane & 15), koff));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + (wn * (BN / 2) + j * 16 + (lane & 15)) * LDK + koff);
+        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + lds_off(wn * (BN / 2) + j * 16 + (lane & 15), koff));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -310,8 +458,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     if (t + 1 < nt) {
-      sa.store(sA[cur ^ 1], tid);
-      sb.store(sB[cur ^ 1], tid);
+      sa.store(sA(cur ^ 1), tid);
+      sb.store(sB(cur ^ 1), tid);
     }
     __syncthreads();
   }
@@ -334,6 +482,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     }
     return;
   }
+#if !FAL_GEMM_STAGE_EPI
   switch (P.epi) {
     case EPI_STORE:
       if (P.out_f32) store_tiles<EPI_STORE, 1, FM, FN>(P, acc, mb, nb, gelu_tanh);
@@ -342,6 +491,34 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     case EPI_GELU: store_tiles<EPI_GELU, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
     case EPI_RESID: store_tiles<EPI_RESID, 1, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
     case EPI_GELU_BWD: store_tiles<EPI_GELU_BWD, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
+  }
+  return;
+#endif
+  // Stage each wavefront's (BM/2) x (BN/2) block through LDS (the operand
+  // buffers are free after the final barrier), then write rows with 16-byte
+  // stores.
+  constexpr int WR = BM / 2, WC = BN / 2;
+  static_assert(4 * WR * WC * 4 <= (int)sizeof(smem), "epilogue staging does not fit");
+  float* stage = reinterpret_cast<float*>(smem) + wave * WR * WC;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = i * 16 + (lane >> 4) * 4 + r, col = j * 16 + (lane & 15);
+        stage[row * WC + (col ^ ((row & 7) << 2))] = acc[i][j][r];
+      }
+  __syncthreads();
+  const int rm0 = m0 + wm * WR, cn0 = n0 + wn * WC;
+  switch (P.epi) {
+    case EPI_STORE:
+      if (P.out_f32) store_rows<EPI_STORE, 1, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh);
+      else store_rows<EPI_STORE, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh);
+      break;
+    case EPI_GELU: store_rows<EPI_GELU, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
+    case EPI_RESID: store_rows<EPI_RESID, 1, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
+    case EPI_GELU_BWD: store_rows<EPI_GELU_BWD, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
   }
 }
 
@@ -403,11 +580,22 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     P.tile_start = total;
     P.splits = 1;
     P.part = nullptr;
+    {
+      // 16-byte epilogue stores need 16-byte aligned rows of every output
+      const int el = (P.epi == EPI_RESID || (P.epi == EPI_STORE && P.out_f32)) ? 4 : 2;
+      const int per16 = 16 / el;
+      bool ok = P.out && aligned16(P.out) && P.ldo % per16 == 0;
+      if (P.epi == EPI_RESID) ok = ok && aligned16(P.resid) && P.ldr % 4 == 0;
+      if (P.epi == EPI_GELU) ok = ok && P.out2 && aligned16(P.out2) && P.ldo2 % 8 == 0;
+      if (P.epi == EPI_GELU_BWD) ok = ok && P.aux && aligned16(P.aux) && P.ldaux % 8 == 0;
+      P.vec_out = ok ? 1 : 0;
+    }
     total += P.tiles_m * P.tiles_n;
   }
-  // Split K for launches that would leave compute units idle: aim for two
-  // resident workgroups per CU with at least 512 of K per slice.
-  if (dt == BF16 && splitk_scratch && g.n == 1) {
+  // Split K for launches that would leave compute units idle (fewer tiles
+  // than CUs): aim for two resident workgroups per CU with at least 512 of K
+  // per slice.
+  if (dt == BF16 && splitk_scratch && g.n == 1 && g.p[0].tiles_m * g.p[0].tiles_n <= 256) {
     GemmProblem& P = g.p[0];
     const int tiles = P.tiles_m * P.tiles_n;
     const int want = (kSplitTarget + tiles - 1) / tiles;

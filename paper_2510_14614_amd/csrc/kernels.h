@@ -46,6 +46,7 @@ struct GemmProblem {
   // filled in by the launcher
   int tiles_m, tiles_n, tile_start;
   int splits;        // K split into this many slices (fp32 partials + reduce)
+  int vec_out;       // outputs (and residual / aux inputs) allow 16-byte rows
   float* part;       // [splits][M][N] fp32 partials when splits > 1
 };
 

@@ -126,51 +126,105 @@ __global__ __launch_bounds__(256) void ln_bwd_rows(LnBwdArgs a) {
   }
 }
 
-// Column partial sums for the LayerNorm parameter gradients: workgroup
-// (column chunk of 256, row block of kPartRows).  partials: [nblk][6][d].
+// Column partial sums for the LayerNorm parameter gradients.  Workgroup =
+// 256 columns x kPartRows rows: 64 threads across the columns (4 consecutive
+// columns each, 16-byte loads) times 4 row groups that each walk
+// kPartRows/4 rows in order; the 4 group sums are then added in a fixed
+// order through LDS.  partials: [nblk][6][d].
 constexpr int kPartRows = 64;
 
 template <typename S>
 __global__ __launch_bounds__(256) void ln_param_partials(LnBwdArgs a) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+  __shared__ float red[3][6][256];
+  const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int j = blockIdx.x * 256 + cl * 4;
   const int rb = blockIdx.y;
   const int d = a.d;
-  if (j >= d) return;
-  const int r0 = rb * kPartRows, r1 = min(a.M, r0 + kPartRows);
   const S* xF = static_cast<const S*>(a.xhatF);
-  float q[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int r = r0; r < r1; ++r) {
-    const int64_t o = (int64_t)r * d + j;
-    const float xh = (a.x[o] - a.mean[r]) * a.rstd[r];
-    if (a.dy1) {
-      const float dy = a.dy1[o];
-      q[0] += dy * xh;
-      q[1] += dy;
-    }
-    if (a.dy2) {
-      const float dy = a.dy2[o];
-      q[2] += dy * xh;
-      q[3] += dy;
-      if (xF) q[4] += dy * to_f(xF[o]);
+  float q[6][4] = {};
+  if (j < d) {
+    const int r0 = rb * kPartRows + rg * (kPartRows / 4);
+    const int r1 = min(a.M, r0 + kPartRows / 4);
+    for (int r = r0; r < r1; ++r) {
+      const int64_t o = (int64_t)r * d + j;
+      const float mu = a.mean[r], rs = a.rstd[r];
+      const float4 x = *reinterpret_cast<const float4*>(a.x + o);
+      const float xh[4] = {(x.x - mu) * rs, (x.y - mu) * rs, (x.z - mu) * rs, (x.w - mu) * rs};
+      if (a.dy1) {
+        const float4 g = *reinterpret_cast<const float4*>(a.dy1 + o);
+        const float gv[4] = {g.x, g.y, g.z, g.w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { q[0][c] += gv[c] * xh[c]; q[1][c] += gv[c]; }
+      }
+      if (a.dy2) {
+        const float4 g = *reinterpret_cast<const float4*>(a.dy2 + o);
+        const float gv[4] = {g.x, g.y, g.z, g.w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { q[2][c] += gv[c] * xh[c]; q[3][c] += gv[c]; }
+        if (xF) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) q[4][c] += gv[c] * to_f(xF[o + c]);
+        }
+      }
     }
   }
-  float* p = a.partials + (int64_t)rb * 6 * d;
+  if (rg > 0) {
 #pragma unroll
-  for (int k = 0; k < 6; ++k) p[(int64_t)k * d + j] = q[k];
+    for (int k = 0; k < 6; ++k)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) red[rg - 1][k][cl * 4 + c] = q[k][c];
+  }
+  __syncthreads();
+  if (rg == 0 && j < d) {
+    float* p = a.partials + (int64_t)rb * 6 * d + j;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      float v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        v[c] = ((q[k][c] + red[0][k][cl * 4 + c]) + red[1][k][cl * 4 + c]) + red[2][k][cl * 4 + c];
+      *reinterpret_cast<float4*>(p + (int64_t)k * d) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
 }
 
-// out[j] = sum_b part[b * stride + j], fixed order.
-__global__ __launch_bounds__(256) void col_reduce_kernel(const float* part, int nblk, int64_t stride,
-                                                         int d, float* out) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= d) return;
+// out_k[j] = sum_b part[b * stride + src_k * d + j] for up to 6 outputs, in
+// block order: 4 threads per column each sum every 4th partial, then the four
+// sums are added in a fixed order.
+struct ColReduceArgs {
+  const float* part;
+  int nblk;
+  int64_t stride;
+  int d;
+  float* out[6];
+  int src[6];
+};
+
+__global__ __launch_bounds__(256) void col_reduce_multi(ColReduceArgs a) {
+  __shared__ float red[4][64];
+  const int col = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int part = threadIdx.x >> 6;
+  const int k = blockIdx.y;
+  float* out = a.out[k];
+  if (!out) return;
   float s = 0.f;
-  for (int b = 0; b < nblk; ++b) s += part[(int64_t)b * stride + j];
-  out[j] = s;
+  if (col < a.d) {
+    const float* p = a.part + (int64_t)a.src[k] * a.d + col;
+    for (int b = part; b < a.nblk; b += 4) s += p[(int64_t)b * a.stride];
+  }
+  red[part][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (part == 0 && col < a.d) {
+    const int c = threadIdx.x & 63;
+    out[col] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+  }
 }
 
 hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(col_reduce_kernel, dim3(cdiv(d, 256)), dim3(256), 0, s, part, nblk, stride, d, out);
+  ColReduceArgs a{};
+  a.part = part; a.nblk = nblk; a.stride = stride; a.d = d;
+  a.out[0] = out; a.src[0] = 0;
+  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), 1), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -243,19 +297,19 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
   if (!any) return hipSuccess;
+  if (a.d % 4) return hipErrorInvalidValue;
   const int nblk = cdiv(a.M, kPartRows);
   const dim3 pgrid(cdiv(a.d, 256), nblk);
   if (dt == BF16) hipLaunchKernelGGL((ln_param_partials<bf16>), pgrid, block, 0, s, a);
   else hipLaunchKernelGGL((ln_param_partials<float>), pgrid, block, 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  ColReduceArgs r{};
+  r.part = a.partials; r.nblk = nblk; r.stride = (int64_t)6 * a.d; r.d = a.d;
   float* outs[6] = {a.dg1, a.db1, a.dg2, a.db2, a.dgF, a.dbF};
   const int src[6] = {0, 1, 2, 3, 4, 3};  // dbF == db2 == sum dy2
-  for (int k = 0; k < 6; ++k) {
-    if (!outs[k]) continue;
-    e = col_reduce(a.partials + (int64_t)src[k] * a.d, nblk, (int64_t)6 * a.d, a.d, outs[k], s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  for (int k = 0; k < 6; ++k) { r.out[k] = outs[k]; r.src[k] = src[k]; }
+  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(256), 0, s, r);
+  return hipGetLastError();
 }
 
 hipError_t norm_bwd(const float* A, const float* mean, const float* rstd, const float* dxhat, int M,
@@ -269,22 +323,43 @@ hipError_t norm_bwd(const float* A, const float* mean, const float* rstd, const 
 }
 
 // ------------------------------------------------------------- col_sum --
-constexpr int kColRows = 128;
+// Bias gradients: column sums in row blocks of kColRows (256 columns x 4
+// row groups per workgroup, rows in order, groups combined in fixed order),
+// then the fixed-order block reduce.
+constexpr int kColRows = 64;
 
 template <typename S>
 __global__ __launch_bounds__(256) void col_sum_partials(const S* x, int64_t ld, int M, int N, float* part) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= N) return;
-  const int r0 = blockIdx.y * kColRows, r1 = min(M, r0 + kColRows);
-  float s = 0.f;
-  for (int r = r0; r < r1; ++r) s += to_f(x[(int64_t)r * ld + j]);
-  part[(int64_t)blockIdx.y * N + j] = s;
+  __shared__ float red[3][256];
+  const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int j = blockIdx.x * 256 + cl * 4;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < N) {
+    const int r0 = blockIdx.y * kColRows + rg * (kColRows / 4), r1 = min(M, r0 + kColRows / 4);
+    for (int r = r0; r < r1; ++r) {
+      const S* p = x + (int64_t)r * ld + j;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) s[c] += to_f(p[c]);
+    }
+  }
+  if (rg > 0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) red[rg - 1][cl * 4 + c] = s[c];
+  }
+  __syncthreads();
+  if (rg == 0 && j < N) {
+    float v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = ((s[c] + red[0][cl * 4 + c]) + red[1][cl * 4 + c]) + red[2][cl * 4 + c];
+    *reinterpret_cast<float4*>(part + (int64_t)blockIdx.y * N + j) = make_float4(v[0], v[1], v[2], v[3]);
+  }
 }
 
 int64_t col_sum_scratch(int M, int N) { return (int64_t)cdiv(M, kColRows) * N; }
 
 hipError_t col_sum(DType dt, int in_f32, const void* x, int64_t ld, int M, int N, float* out,
                    float* scratch, hipStream_t s) {
+  if (N % 4 || ld % 4) return hipErrorInvalidValue;
   const int nblk = cdiv(M, kColRows);
   const dim3 grid(cdiv(N, 256), nblk), block(256);
   if (in_f32 || dt == F32)
