@@ -43,21 +43,30 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return s;
 }
 
-// GELU (MLP non-linearity).  tanh form: 0.5 x (1 + tanh(sqrt(2/pi)(x + 0.044715 x^3)));
-// erf form: x * Phi(x).  Library tanhf / erff.
+// GELU (MLP non-linearity).  tanh form 0.5 x (1 + tanh(u)) with
+// u = sqrt(2/pi) (x + 0.044715 x^3), evaluated through the identity
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)) (one exp2 and one reciprocal);
+// derivative s + 2 x s (1 - s) u' with s = 1 / (1 + exp(-2u)).
+// erf form x * Phi(x) uses the library erff.
+__device__ __forceinline__ float gelu_sig_arg(float x) {
+  // -2u * log2(e)
+  const float c2 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  return c2 * (x + 0.044715f * x * x * x);
+}
+
 __device__ __forceinline__ float gelu_f(float x, int tanh_form) {
   if (tanh_form) {
-    const float c = 0.7978845608028654f;
-    return 0.5f * x * (1.f + tanhf(c * (x + 0.044715f * x * x * x)));
+    const float s = __builtin_amdgcn_rcpf(1.f + exp2f(gelu_sig_arg(x)));
+    return x * s;
   }
   return 0.5f * x * (1.f + erff(x * 0.7071067811865476f));
 }
 
 __device__ __forceinline__ float gelu_grad_f(float x, int tanh_form) {
   if (tanh_form) {
-    const float c = 0.7978845608028654f;
-    const float t = tanhf(c * (x + 0.044715f * x * x * x));
-    return 0.5f * (1.f + t) + 0.5f * x * (1.f - t * t) * c * (1.f + 3.f * 0.044715f * x * x);
+    const float s = __builtin_amdgcn_rcpf(1.f + exp2f(gelu_sig_arg(x)));
+    const float du = 0.7978845608028654f * (1.f + 3.f * 0.044715f * x * x);
+    return s + 2.f * x * s * (1.f - s) * du;
   }
   const float cdf = 0.5f * (1.f + erff(x * 0.7071067811865476f));
   const float pdf = 0.3989422804014327f * expf(-0.5f * x * x);

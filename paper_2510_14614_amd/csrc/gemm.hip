@@ -134,60 +134,118 @@ __device__ __forceinline__ int lds_off(int row, int k) {
   return row * LDK + ((((k >> 3) ^ f)) << 3) + (k & 7);
 }
 
-// Global -> register staging of one operand tile (R rows of the output
-// dimension x KT of k).  Loads are unconditional (out-of-range chunks read a
-// clamped in-bounds address) so that every load of a tile is in flight at
-// once; the validity of each chunk is applied when the registers are written
-// to LDS, after the MFMA phase has given the loads time to land.
+// Operand staging through buffer loads.  Each thread's chunk offsets (32-bit,
+// bytes from the tile's first row or column) are computed once per K
+// segment; the k-tile advance goes into the scalar offset, so the steady
+// state issues loads with no per-load address arithmetic.  Rows past the
+// matrix are clamped to an in-bounds row when the offsets are built and
+// zeroed when written to LDS (edge tiles only); k past the segment is
+// checked only in the tail tile.  The resource's range is the operand's
+// extent, so even a clamped offset cannot leave the buffer.
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family buffer descriptor word 3
+
 template <int R, int KMAJ>
-struct Stage {
-  // k-contiguous: R*KT/8 chunks of 8; mn-contiguous: units of 4 k x 8 mn.
+struct BStage {
   static constexpr int NC = KMAJ ? R * KT / 8 / 256 : 4 * (R * KT / 32) / 256;
   uint4 v[NC];
-  int nvalid[NC];  // valid elements of the chunk (k-contiguous) or 0/8
+  uint32_t voff[NC];
+  uint32_t rowbad;
+  int kpart[NC];
+  uint64_t base;   // byte address of the tile's first row / column
+  int nbytes;      // extent of the operand from base
+  uint32_t kstep;
 
-  __device__ __forceinline__ void load(const bf16* X, int64_t ld, int r0, int Rmax, int k0, int K, int tid) {
+  __device__ __forceinline__ void init(const bf16* X, int64_t ld, int r0, int Rmax, int Kseg, int tid) {
+    base = reinterpret_cast<uint64_t>(KMAJ ? X + (int64_t)r0 * ld : X + r0);
+    const int64_t ext = KMAJ ? (int64_t)(Rmax - r0) * ld * 2 : ((int64_t)Kseg * ld - r0) * 2;
+    nbytes = (int)min<int64_t>(ext, 0x7fffffff);
+    rowbad = 0;
     if (KMAJ) {
+      kstep = 2;
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
         const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
-        const int gr = r0 + row, gk = k0 + kc;
-        const bool ok = gr < Rmax && gk < K;
-        nvalid[i] = ok ? min(8, K - gk) : 0;
-        const bf16* p = ok ? X + (int64_t)gr * ld + gk : X;
-        v[i] = *reinterpret_cast<const uint4*>(p);
+        int rr = row;
+        if (r0 + row >= Rmax) { rowbad |= 1u << i; rr = Rmax - 1 - r0; }
+        voff[i] = (uint32_t)(((int64_t)rr * ld + kc) * 2);
       }
     } else {
-      // unit u: 4 consecutive k rows x 8 consecutive columns
+      kstep = (uint32_t)(ld * 2);
 #pragma unroll
       for (int u = 0; u < NC / 4; ++u) {
         const int id = tid + 256 * u;
         const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
+        int cc = mc;
+        const bool bad = r0 + mc >= Rmax;
+        if (bad) cc = ((Rmax - r0 - 1) / 8) * 8;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int gk = k0 + kg + j, gr = r0 + mc;
-          const bool ok = gk < K && gr < Rmax;
-          nvalid[4 * u + j] = ok ? 8 : 0;
-          const bf16* p = ok ? X + (int64_t)gk * ld + gr : X;
-          v[4 * u + j] = *reinterpret_cast<const uint4*>(p);
+          if (bad) rowbad |= 1u << (4 * u + j);
+          voff[4 * u + j] = (uint32_t)(((int64_t)(kg + j) * ld + cc) * 2);
         }
       }
     }
   }
 
-  __device__ __forceinline__ void store(bf16* s, int tid) const {
+  // The descriptor is wave-uniform: rebuild it from readfirstlane'd scalars at
+  // the load so it lives in scalar registers (no waterfall loops).
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc() const {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)base);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
+    const int n = __builtin_amdgcn_readfirstlane(nbytes);
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)hi << 32) | lo), (short)0, n,
+                                             kRsrcWord3);
+  }
+  __device__ __forceinline__ uint4 ld16(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t soff) const {
+    typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+    const u32x4v r = __builtin_amdgcn_raw_buffer_load_b128(rs, off, soff, 0);
+    return make_uint4(r[0], r[1], r[2], r[3]);
+  }
+
+  __device__ __forceinline__ uint32_t soff(int k0) const {
+    return __builtin_amdgcn_readfirstlane((uint32_t)k0 * kstep);
+  }
+  // Full tile at k0 (relative to the segment).
+  __device__ __forceinline__ void load_full(__amdgpu_buffer_rsrc_t rs, uint32_t so) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) v[i] = ld16(rs, voff[i], so);
+  }
+  // Tail tile: chunks past K are not read.
+  __device__ __forceinline__ void load_tail(__amdgpu_buffer_rsrc_t rs, uint32_t so, int k0, int K, int tid) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      int kk;
+      if (KMAJ) {
+        kk = k0 + ((tid + 256 * i) & 7) * 8;
+        kpart[i] = max(0, min(8, K - kk));
+      } else {
+        const int id = tid + 256 * (i / 4);
+        kk = k0 + (id % (KT / 4)) * 4 + (i % 4);
+        kpart[i] = kk < K ? 8 : 0;
+      }
+      v[i] = kpart[i] > 0 ? ld16(rs, voff[i], so) : make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  __device__ __forceinline__ uint4 masked(int i, bool tail) const {
+    uint4 w = v[i];
+    if (rowbad & (1u << i)) return make_uint4(0, 0, 0, 0);
+    if (tail && kpart[i] < 8) {
+      uint16_t* e = reinterpret_cast<uint16_t*>(&w);
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (q >= kpart[i]) e[q] = 0;
+    }
+    return w;
+  }
+
+  // check: edge tile or tail tile (uniform); otherwise stores go straight in.
+  __device__ __forceinline__ void store(bf16* s, int tid, bool check, bool tail) const {
     if (KMAJ) {
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
         const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
-        uint4 w = v[i];
-        if (nvalid[i] < 8) {
-          uint16_t* e = reinterpret_cast<uint16_t*>(&w);
-#pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (q >= nvalid[i]) e[q] = 0;
-        }
-        *reinterpret_cast<uint4*>(s + lds_off(row, kc)) = w;
+        *reinterpret_cast<uint4*>(s + lds_off(row, kc)) = check ? masked(i, tail) : v[i];
       }
     } else {
 #pragma unroll
@@ -197,10 +255,9 @@ struct Stage {
         uint32_t w[4][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint4 x = nvalid[4 * u + j] ? v[4 * u + j] : make_uint4(0, 0, 0, 0);
+          const uint4 x = check ? masked(4 * u + j, tail) : v[4 * u + j];
           w[j][0] = x.x; w[j][1] = x.y; w[j][2] = x.z; w[j][3] = x.w;
         }
-        // transpose 4 (k) x 8 (mn) into 8 k-contiguous rows of 4
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           uint2 lo, hi;
@@ -416,31 +473,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     tbeg = split * per;
     nt = max(0, min(nt1, tbeg + per) - tbeg);
   }
-  Stage<BM, AK> sa;
-  Stage<BN, BKM> sb;
-  auto fetch = [&](int tt) {
-    const int t = tt + tbeg;
-    const bool seg = t >= nt1;
-    const bf16* A = static_cast<const bf16*>(seg ? P.A2 : P.A);
-    const bf16* B = static_cast<const bf16*>(seg ? P.B2 : P.B);
-    const int64_t lda = seg ? P.lda2 : P.lda, ldb = seg ? P.ldb2 : P.ldb;
-    const int K = seg ? P.K2 : P.K;
-    const int k0 = (seg ? t - nt1 : t) * KT;
-    sa.load(A, lda, m0, P.M, k0, K, tid);
-    sb.load(B, ldb, n0, P.N, k0, K, tid);
-  };
-
-  if (nt > 0) {
-    fetch(0);
-    sa.store(sA(0), tid);
-    sb.store(sB(0), tid);
-  }
-  __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < nt) fetch(t + 1);
-    const bf16* a_s = sA(cur);
-    const bf16* b_s = sB(cur);
+  auto compute = [&](const bf16* a_s, const bf16* b_s) {
 #pragma unroll
     for (int ks = 0; ks < KT / 32; ++ks) {
       bf16x8_t a[FM], b[FN];
@@ -457,9 +490,50 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+  };
+  const bool edge = (m0 + BM > P.M) || (n0 + BN > P.N);
+  BStage<BM, AK> sa;
+  BStage<BN, BKM> sb;
+  int fseg = 0, fk = 0, fK = P.K;
+  auto seg_init = [&](int seg, int k0) {
+    fseg = seg;
+    fK = seg ? P.K2 : P.K;
+    fk = k0;
+    sa.init(static_cast<const bf16*>(seg ? P.A2 : P.A), seg ? P.lda2 : P.lda, m0, P.M, fK, tid);
+    sb.init(static_cast<const bf16*>(seg ? P.B2 : P.B), seg ? P.ldb2 : P.ldb, n0, P.N, fK, tid);
+  };
+  // Issues every load of the next tile of both operands (one branch, so no
+  // wait is forced between them); returns whether it is a tail tile.
+  auto fetch_next = [&]() {
+    if (fk >= fK) seg_init(1, 0);
+    const bool tail = fk + KT > fK;
+    const __amdgpu_buffer_rsrc_t ra = sa.rsrc(), rb = sb.rsrc();
+    const uint32_t oa = sa.soff(fk), ob = sb.soff(fk);
+    if (!tail) {
+      sa.load_full(ra, oa);
+      sb.load_full(rb, ob);
+    } else {
+      sa.load_tail(ra, oa, fk, fK, tid);
+      sb.load_tail(rb, ob, fk, fK, tid);
+    }
+    fk += KT;
+    return tail;
+  };
+  bool tail_next = false;
+  if (nt > 0) {
+    seg_init(tbeg >= nt1 ? 1 : 0, (tbeg >= nt1 ? tbeg - nt1 : tbeg) * KT);
+    const bool tail = fetch_next();
+    sa.store(sA(0), tid, edge || tail, tail);
+    sb.store(sB(0), tid, edge || tail, tail);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < nt) tail_next = fetch_next();
+    compute(sA(cur), sB(cur));
     if (t + 1 < nt) {
-      sa.store(sA(cur ^ 1), tid);
-      sb.store(sB(cur ^ 1), tid);
+      sa.store(sA(cur ^ 1), tid, edge || tail_next, tail_next);
+      sb.store(sB(cur ^ 1), tid, edge || tail_next, tail_next);
     }
     __syncthreads();
   }
