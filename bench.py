@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="gpt2-small")
     ap.add_argument("--arch", default="fal", choices=["gpt", "fal", "falplus", "fal+"])
-    ap.add_argument("--sched", default="merged", choices=["seq", "streams", "merged"])
+    ap.add_argument("--sched", default="streams_merged", choices=["seq", "streams", "merged", "streams_merged"])
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=1)

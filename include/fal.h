@@ -68,9 +68,15 @@ typedef enum { FAL_F32 = 0, FAL_BF16 = 1 } fal_dtype_t;
  *  MERGED  : the independent GEMMs of the two branches are issued as one
  *            grouped launch, and FAL's output projection and down-projection
  *            as one GEMM over the concatenated inner dimension.
+ *  STREAMS_MERGED : the branches on two streams as in STREAMS (forward:
+ *            QKV and attention on main, FFN-up on aux; backward: the MHA and
+ *            MLP chains), and after the join the output and down
+ *            projections as one GEMM over the concatenated inner dimension.
  * GPT and FAL+ blocks have no independent branches; the schedule only
  * affects FAL blocks. */
-typedef enum { FAL_SCHED_SEQ = 0, FAL_SCHED_STREAMS = 1, FAL_SCHED_MERGED = 2 } fal_sched_t;
+typedef enum {
+  FAL_SCHED_SEQ = 0, FAL_SCHED_STREAMS = 1, FAL_SCHED_MERGED = 2, FAL_SCHED_STREAMS_MERGED = 3
+} fal_sched_t;
 
 typedef struct {
   int32_t n_layer;        /* L >= 1                                           */

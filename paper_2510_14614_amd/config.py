@@ -11,8 +11,9 @@ import dataclasses
 ARCH_GPT, ARCH_FAL, ARCH_FALPLUS = 0, 1, 2
 ARCH_NAMES = {"gpt": ARCH_GPT, "fal": ARCH_FAL, "falplus": ARCH_FALPLUS, "fal+": ARCH_FALPLUS}
 DTYPE_F32, DTYPE_BF16 = 0, 1
-SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED = 0, 1, 2
-SCHED_NAMES = {"seq": SCHED_SEQ, "streams": SCHED_STREAMS, "merged": SCHED_MERGED}
+SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED, SCHED_STREAMS_MERGED = 0, 1, 2, 3
+SCHED_NAMES = {"seq": SCHED_SEQ, "streams": SCHED_STREAMS, "merged": SCHED_MERGED,
+               "streams_merged": SCHED_STREAMS_MERGED}
 
 
 @dataclasses.dataclass

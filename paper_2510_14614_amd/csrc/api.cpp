@@ -67,7 +67,7 @@ const char* validate(const fal_config_t* c) {
   if (c->seq_len < 1 || c->batch < 1) return "seq_len and batch must be >= 1";
   if (c->arch < FAL_ARCH_GPT || c->arch > FAL_ARCH_FALPLUS) return "unknown arch";
   if (c->dtype != FAL_F32 && c->dtype != FAL_BF16) return "unknown dtype";
-  if (c->sched < FAL_SCHED_SEQ || c->sched > FAL_SCHED_MERGED) return "unknown sched";
+  if (c->sched < FAL_SCHED_SEQ || c->sched > FAL_SCHED_STREAMS_MERGED) return "unknown sched";
   if (!(c->ln_eps > 0.f)) return "ln_eps must be > 0";
   if (c->gelu_tanh != 0 && c->gelu_tanh != 1) return "gelu_tanh must be 0 or 1";
   if (c->has_embed_head != 0 && c->has_embed_head != 1) return "has_embed_head must be 0 or 1";
@@ -417,8 +417,14 @@ struct Run {
     FAL_TRY(hipEventRecord(ctx->ev_join, ctx->sa));
     FAL_TRY(hipStreamWaitEvent(ctx->sm, ctx->ev_join, 0));
   }
-  bool streams() const { return ctx->cfg.sched == FAL_SCHED_STREAMS && ctx->sa != ctx->sm; }
+  bool streams() const {
+    return (ctx->cfg.sched == FAL_SCHED_STREAMS || ctx->cfg.sched == FAL_SCHED_STREAMS_MERGED) &&
+           ctx->sa != ctx->sm;
+  }
   bool merged() const { return ctx->cfg.sched == FAL_SCHED_MERGED; }
+  bool merged_out() const {
+    return ctx->cfg.sched == FAL_SCHED_MERGED || ctx->cfg.sched == FAL_SCHED_STREAMS_MERGED;
+  }
 
   void block_fwd(int layer, const void* bp, const float* x, float* y, void* first) {
     const Dims& D = ctx->D;
@@ -445,6 +451,15 @@ struct Run {
       gemm1(1, 0, fc_prob(S, bp), s2);
       gemm1(1, 0, qkv_prob(S, bp), sm);
       attention_fwd(S, sm);
+      if (merged_out()) {
+        if (streams()) join();
+        GemmProblem p = oproj_prob(S, bp);
+        const GemmProblem q = down_prob(S, bp);
+        p.A2 = q.A; p.lda2 = q.lda; p.B2 = q.B; p.ldb2 = q.ldb; p.K2 = q.K; p.bias2 = q.bias;
+        p.epi = EPI_RESID; p.resid = x; p.ldr = D.d; p.out = y; p.ldo = D.d;
+        gemm1(1, 0, p, sm);
+        return;
+      }
       GemmProblem po = oproj_prob(S, bp);
       po.epi = EPI_RESID; po.resid = x; po.ldr = D.d; po.out = y; po.ldo = D.d;
       gemm1(1, 0, po, sm);

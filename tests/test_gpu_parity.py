@@ -8,14 +8,14 @@ import pytest
 import oracle
 from paper_2510_14614_amd import fal, get_config, synth
 from paper_2510_14614_amd.config import (ARCH_FAL, ARCH_FALPLUS, ARCH_GPT, SCHED_MERGED, SCHED_SEQ,
-                                         SCHED_STREAMS, Config)
+                                         SCHED_STREAMS, SCHED_STREAMS_MERGED, Config)
 
 from gpu_helpers import compare_step, gpu_model_step, gpu_stack_step, log
 
 pytestmark = pytest.mark.gpu
 
 ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS]
-SCHEDS = [SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED]
+SCHEDS = [SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED, SCHED_STREAMS_MERGED]
 
 
 def _ref(cfg, g, blocks, tok):
@@ -89,3 +89,39 @@ def test_long_sequence_multi_block_attention(arch, hd):
     tok = synth.make_tokens(cfg, seed=9, dist="zipf")
     compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
                  label=f"long a{arch} hd{hd}")
+
+
+def _all_outputs(out):
+    arrs = [np.array([out["loss"]]), out["logits"]]
+    arrs += [out["grads_global"][k] for k in sorted(out["grads_global"])]
+    for blk in out["grads_blocks"]:
+        arrs += [blk[k] for k in sorted(blk)]
+    return arrs
+
+
+@pytest.mark.parametrize("pair", [(SCHED_SEQ, SCHED_STREAMS), (SCHED_MERGED, SCHED_STREAMS_MERGED)])
+def test_stream_schedules_bitwise_equal(pair):
+    # the two-stream schedules run the same kernels on disjoint buffers as
+    # their one-stream counterparts, so every output must agree bitwise
+    a, b = pair
+    base = _ragged(ARCH_FAL, 1, n_layer=3)
+    g, blocks = synth.make_params(base, seed=10)
+    tok = synth.make_tokens(base, seed=11, dist="zipf")
+    log(f"bitwise schedules {a} vs {b}")
+    oa = gpu_model_step(base.replace(sched=a), g, blocks, tok)
+    ob = gpu_model_step(base.replace(sched=b), g, blocks, tok)
+    for x, y in zip(_all_outputs(oa), _all_outputs(ob)):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_run_to_run_deterministic():
+    cfg = _ragged(ARCH_FALPLUS, 1, sched=SCHED_STREAMS)
+    g, blocks = synth.make_params(cfg, seed=12)
+    tok = synth.make_tokens(cfg, seed=13, dist="zipf")
+    log("determinism")
+    F = fal.Fal(cfg)
+    o1 = gpu_model_step(cfg, g, blocks, tok, ctx=F)
+    o2 = gpu_model_step(cfg, g, blocks, tok, ctx=F)
+    F.close()
+    for x, y in zip(_all_outputs(o1), _all_outputs(o2)):
+        np.testing.assert_array_equal(x, y)
