@@ -1,7 +1,8 @@
 """Training-step throughput of the FAL hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config gpt2-small]
-                    [--arch fal] [--sched merged] [--no-compare] [--no-cpu-baseline]
+                    [--arch fal] [--sched streams_merged] [--no-compare] [--no-cpu-baseline]
+                    [--single-stream]
 
 One step = one full forward + backward of the language model (embedding,
 every block, final LayerNorm, tied LM head, cross-entropy) through
@@ -13,7 +14,9 @@ synchronisation.  Prints one JSON line.
 Also reported, from the same process:
   * roofline of the dominant kernel class (the bf16 MFMA GEMMs): algorithmic
     FLOPs / summed launch time, both from HIP events the library records on
-    the stream each GEMM runs on during a profiled run of K more steps;
+    the stream each GEMM runs on, during K more steps of the same schedule
+    run with the aux stream equal to the main stream (identical launches,
+    no overlap between kernels, so each span times one kernel);
   * the same-kernel sequential GPT baseline and FAL+ on the same config
     (tokens/s and the ratio to it);
   * cpu_baseline: the fp64 CPU oracle timed on this host on a bounded sample
@@ -47,6 +50,8 @@ def parse():
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=1)
+    ap.add_argument("--single-stream", action="store_true",
+                    help="run the timed steps with the aux stream equal to the main stream")
     return ap.parse_args()
 
 
@@ -57,13 +62,14 @@ def describe(cfg, arch_name, sched_name):
 
 
 class Runner:
-    def __init__(self, cfg):
+    def __init__(self, cfg, single_stream=False):
         import torch
 
         from paper_2510_14614_amd import fal, synth
         self.torch = torch
         self.cfg = cfg
-        self.F = fal.Fal(cfg)
+        main = torch.cuda.current_stream()
+        self.F = fal.Fal(cfg, stream_main=main, stream_aux=main if single_stream else None)
         g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
         self.F.load_params(g, blocks)
         if cfg.has_embed_head:
@@ -153,10 +159,15 @@ def main():
     sched = SCHED_NAMES[args.sched]
     cfg = get_config(args.config, arch=arch, sched=sched, dtype=1)
 
-    r = Runner(cfg)
+    r = Runner(cfg, single_stream=args.single_stream)
     ms, wall = r.time(args.steps, args.warmup)
-    prof = r.profile(args.steps)
     r.close()
+    # Kernel roofline from a serialized pass (aux stream = main stream: the
+    # same launches without overlap, so each event span is one kernel alone).
+    rp = Runner(cfg, single_stream=True)
+    rp.time(1, 1)
+    prof = rp.profile(args.steps)
+    rp.close()
     tokens_per_s = cfg.tokens / (ms / 1000.0)
     flops_step = cfg.train_flops_per_token() * cfg.tokens
 
