@@ -25,8 +25,10 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
   __shared__ float Vs[ABR][HD + 1];
-  const int qb = gridDim.x - 1 - blockIdx.x;  // long (late) query blocks first
-  const int h = blockIdx.y, b = blockIdx.z;
+  // grid (H, B, blocks): causal block index slowest (even XCD mix), the
+  // longest (latest) query blocks first
+  const int qb = gridDim.z - 1 - blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
@@ -124,7 +126,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S*
   __shared__ float Qs[ABR][HD + 1];
   __shared__ float dOs[ABR][HD + 1];
   __shared__ float Ls[ABR], Ds[ABR];
-  const int kb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int kb = blockIdx.z, h = blockIdx.x, b = blockIdx.y;  // causal block index slowest
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
@@ -196,8 +198,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* d
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
   __shared__ float Vs[ABR][HD + 1];
-  const int qb = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // grid (H, B, blocks): the causal block index varies slowest, so the
+  // round-robin dispatch over XCDs gives every XCD the same mix of long and
+  // short blocks; the longest (latest) query blocks are dispatched first.
+  const int qb = gridDim.z - 1 - blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
@@ -270,7 +275,7 @@ hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, c
 hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
                     float* lse, hipStream_t s) {
   if (dt == BF16 && attn_mfma_supported(hd)) return attn_fwd_mfma_launch(qkv, B, T, H, hd, O, ldo, lse, s);
-  const dim3 grid(cdiv(T, ABR), H, B), block(256);
+  const dim3 grid(H, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
     if (dt == BF16)
@@ -298,7 +303,7 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
   if (e != hipSuccess) return e;
   if (dt == BF16 && attn_mfma_supported(hd))
     return attn_bwd_mfma_launch(qkv, dO, lddo, lse, Dvec, B, T, H, hd, dqkv, s);
-  const dim3 grid(cdiv(T, ABR), H, B), block(256);
+  const dim3 grid(H, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
     if (dt == BF16) {

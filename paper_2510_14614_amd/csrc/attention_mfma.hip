@@ -62,47 +62,78 @@ __device__ __forceinline__ bf16x8v pack8(const f32x16v& v, int base) {
 // Row r of the 32x32 accumulator tile held by lane group g.
 __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
-// Copy AT rows (row0..row0+AT-1, zero past T) of a head slice into LDS,
-// row-major [row][HD + 8].
+// Tiles of AT rows (row0.., zero past T) of a head slice, staged through
+// registers: load() issues the global loads (rows past T read a clamped
+// row), store() writes LDS (zeroing rows past T).  Loading the next tile
+// before computing on the current one keeps its memory latency behind the
+// MFMA work.  RowTile stores row-major [row][HD + 8]; TTile stores the tile
+// transposed, [dim][AT + 8], each thread moving 4 rows x 8 dims.
 template <int HD>
-__device__ __forceinline__ void tile_rows(bf16* s, const bf16* src, int64_t ld, int row0, int T, int tid) {
-  constexpr int CH = HD / 8;
-  for (int i = tid; i < AT * CH; i += 256) {
-    const int r = i / CH, c = (i % CH) * 8, row = row0 + r;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (row < T) v = *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c);
-    *reinterpret_cast<uint4*>(s + r * (HD + 8) + c) = v;
+struct RowTile {
+  static constexpr int CH = HD / 8, N = (AT * CH + 255) / 256;
+  uint4 v[N];
+  __device__ __forceinline__ void load(const bf16* src, int64_t ld, int row0, int T, int tid) {
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int i = tid + 256 * k;
+      const int r = i / CH, c = (i % CH) * 8;
+      const int row = min(row0 + r, T - 1);
+      if (i < AT * CH) v[k] = *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c);
+    }
   }
-}
+  __device__ __forceinline__ void store(bf16* s, int row0, int T, int tid) const {
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int i = tid + 256 * k;
+      if (i >= AT * CH) continue;
+      const int r = i / CH, c = (i % CH) * 8;
+      *reinterpret_cast<uint4*>(s + r * (HD + 8) + c) = row0 + r < T ? v[k] : make_uint4(0, 0, 0, 0);
+    }
+  }
+};
 
-// Same rows, stored transposed: [dim][AT + 8].  Each unit is 4 rows x 8 dims.
 template <int HD>
-__device__ __forceinline__ void tile_rows_t(bf16* s, const bf16* src, int64_t ld, int row0, int T, int tid) {
-  constexpr int CH = HD / 8;
-  for (int i = tid; i < (AT / 4) * CH; i += 256) {
-    const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
-    uint4 v[4];
+struct TTile {
+  static constexpr int CH = HD / 8, U = (AT / 4) * CH, N = (U + 255) / 256;
+  uint4 v[N][4];
+  __device__ __forceinline__ void load(const bf16* src, int64_t ld, int row0, int T, int tid) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = row0 + rg + j;
-      v[j] = row < T ? *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c) : make_uint4(0, 0, 0, 0);
-    }
-    const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
-    const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
-    const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
-    const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
+    for (int k = 0; k < N; ++k) {
+      const int i = tid + 256 * k;
+      if (i >= U) continue;
+      const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint2 lo, hi;
-      lo.x = (w0[q] & 0xFFFFu) | (w1[q] << 16);
-      lo.y = (w2[q] & 0xFFFFu) | (w3[q] << 16);
-      hi.x = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
-      hi.y = (w2[q] >> 16) | (w3[q] & 0xFFFF0000u);
-      *reinterpret_cast<uint2*>(s + (c + 2 * q) * ATP + rg) = lo;
-      *reinterpret_cast<uint2*>(s + (c + 2 * q + 1) * ATP + rg) = hi;
+      for (int j = 0; j < 4; ++j) {
+        const int row = min(row0 + rg + j, T - 1);
+        v[k][j] = *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c);
+      }
     }
   }
-}
+  __device__ __forceinline__ void store(bf16* s, int row0, int T, int tid) const {
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int i = tid + 256 * k;
+      if (i >= U) continue;
+      const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
+      uint32_t w[4][4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint4 x = row0 + rg + j < T ? v[k][j] : make_uint4(0, 0, 0, 0);
+        w[j][0] = x.x; w[j][1] = x.y; w[j][2] = x.z; w[j][3] = x.w;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint2 lo, hi;
+        lo.x = (w[0][q] & 0xFFFFu) | (w[1][q] << 16);
+        lo.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
+        hi.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
+        hi.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
+        *reinterpret_cast<uint2*>(s + (c + 2 * q) * ATP + rg) = lo;
+        *reinterpret_cast<uint2*>(s + (c + 2 * q + 1) * ATP + rg) = hi;
+      }
+    }
+  }
+};
 
 // A or B operand fragment from a row-major LDS tile: row `row`, dims
 // 16*kk + 8*g .. +7.
@@ -137,8 +168,11 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sVt[HD * ATP];
-  const int qb = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // grid (H, B, blocks): the causal block index varies slowest, so the
+  // round-robin dispatch over XCDs gives every XCD the same mix of long and
+  // short blocks; the longest (latest) query blocks are dispatched first.
+  const int qb = gridDim.z - 1 - blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
@@ -159,11 +193,19 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int
 
   const int kend = min(T, qb * 128 + 128);
   const int wave_kend = min(T, q0 + 32);
+  RowTile<HD> rk;
+  TTile<HD> rv;
+  rk.load(Kg, ld, 0, T, tid);
+  rv.load(Vg, ld, 0, T, tid);
   for (int k0 = 0; k0 < kend; k0 += AT) {
     __syncthreads();
-    tile_rows<HD>(sK, Kg, ld, k0, T, tid);
-    tile_rows_t<HD>(sVt, Vg, ld, k0, T, tid);
+    rk.store(sK, k0, T, tid);
+    rv.store(sVt, k0, T, tid);
     __syncthreads();
+    if (k0 + AT < kend) {
+      rk.load(Kg, ld, k0 + AT, T, tid);
+      rv.load(Vg, ld, k0 + AT, T, tid);
+    }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
       const int kb = k0 + 32 * sub;
@@ -230,8 +272,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
   __shared__ __attribute__((aligned(16))) bf16 sQt[HD * ATP];
   __shared__ __attribute__((aligned(16))) bf16 sdOt[HD * ATP];
   __shared__ float sL[AT], sD[AT];
-  const int kb0 = blockIdx.x * 128;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // grid (H, B, blocks): causal block index slowest (even XCD mix); the
+  // earliest key blocks see the most queries and are dispatched first
+  const int kb0 = blockIdx.z * 128;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
@@ -255,18 +299,32 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
 #pragma unroll
   for (int t = 0; t < NT; ++t) { dk[t] = zero16(); dv[t] = zero16(); }
 
+  RowTile<HD> rq, ro;
+  TTile<HD> rqt, rot;
+  if (kb0 < T) {
+    rq.load(Qg, ld, kb0, T, tid);
+    ro.load(dOg, lddo, kb0, T, tid);
+    rqt.load(Qg, ld, kb0, T, tid);
+    rot.load(dOg, lddo, kb0, T, tid);
+  }
   for (int q0 = kb0; q0 < T; q0 += AT) {
     __syncthreads();
-    tile_rows<HD>(sQ, Qg, ld, q0, T, tid);
-    tile_rows<HD>(sdO, dOg, lddo, q0, T, tid);
-    tile_rows_t<HD>(sQt, Qg, ld, q0, T, tid);
-    tile_rows_t<HD>(sdOt, dOg, lddo, q0, T, tid);
+    rq.store(sQ, q0, T, tid);
+    ro.store(sdO, q0, T, tid);
+    rqt.store(sQt, q0, T, tid);
+    rot.store(sdOt, q0, T, tid);
     if (tid < AT) {
       const int tq = q0 + tid;
       sL[tid] = tq < T ? Lg[tq] * kLog2e : 0.f;
       sD[tid] = tq < T ? Dg[tq] : 0.f;
     }
     __syncthreads();
+    if (q0 + AT < T) {
+      rq.load(Qg, ld, q0 + AT, T, tid);
+      ro.load(dOg, lddo, q0 + AT, T, tid);
+      rqt.load(Qg, ld, q0 + AT, T, tid);
+      rot.load(dOg, lddo, q0 + AT, T, tid);
+    }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
       const int qs = q0 + 32 * sub;
@@ -321,8 +379,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const b
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sKt[HD * ATP];
-  const int qb = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // grid (H, B, blocks): the causal block index varies slowest, so the
+  // round-robin dispatch over XCDs gives every XCD the same mix of long and
+  // short blocks; the longest (latest) query blocks are dispatched first.
+  const int qb = gridDim.z - 1 - blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int dA = H * HD;
   const int64_t ld = 3 * (int64_t)dA;
   const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
@@ -348,12 +409,22 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const b
 
   const int kend = min(T, qb * 128 + 128);
   const int wave_kend = min(T, q0 + 32);
+  RowTile<HD> rk, rv;
+  TTile<HD> rkt;
+  rk.load(Kg, ld, 0, T, tid);
+  rv.load(Vg, ld, 0, T, tid);
+  rkt.load(Kg, ld, 0, T, tid);
   for (int k0 = 0; k0 < kend; k0 += AT) {
     __syncthreads();
-    tile_rows<HD>(sK, Kg, ld, k0, T, tid);
-    tile_rows<HD>(sV, Vg, ld, k0, T, tid);
-    tile_rows_t<HD>(sKt, Kg, ld, k0, T, tid);
+    rk.store(sK, k0, T, tid);
+    rv.store(sV, k0, T, tid);
+    rkt.store(sKt, k0, T, tid);
     __syncthreads();
+    if (k0 + AT < kend) {
+      rk.load(Kg, ld, k0 + AT, T, tid);
+      rv.load(Vg, ld, k0 + AT, T, tid);
+      rkt.load(Kg, ld, k0 + AT, T, tid);
+    }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
       const int kb = k0 + 32 * sub;
@@ -398,7 +469,7 @@ bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
 
 hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
                                 hipStream_t s) {
-  const dim3 grid(cdiv(T, 128), H, B), block(256);
+  const dim3 grid(H, B, cdiv(T, 128)), block(256);
   const bf16* q = static_cast<const bf16*>(qkv);
   bf16* o = static_cast<bf16*>(O);
   if (hd == 64) hipLaunchKernelGGL((attn_fwd_mfma<64>), grid, block, 0, s, q, T, H, o, ldo, lse);
@@ -409,7 +480,7 @@ hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, vo
 
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, const float* lse, const float* Dvec,
                                 int B, int T, int H, int hd, void* dqkv, hipStream_t s) {
-  const dim3 grid(cdiv(T, 128), H, B), block(256);
+  const dim3 grid(H, B, cdiv(T, 128)), block(256);
   const bf16* q = static_cast<const bf16*>(qkv);
   const bf16* d = static_cast<const bf16*>(dO);
   bf16* o = static_cast<bf16*>(dqkv);
