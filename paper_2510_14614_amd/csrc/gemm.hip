@@ -5,7 +5,8 @@
 // Two kernels share one problem descriptor (kernels.h):
 //  * gemm_bf16_mfma: bf16 operands, fp32 accumulation on the gfx950 matrix
 //    cores (v_mfma_f32_16x16x32_bf16).  128x128 output tile per 256-thread
-//    workgroup, 2x2 wavefronts of 64x64, K staged through LDS 64 at a time
+//    workgroup (2x2 wavefronts of 64x64) or 256x256 per 512-thread
+//    workgroup (4x2 wavefronts of 64x128), K staged through LDS 64 at a time
 //    in k-contiguous rows.  Operands whose contraction dimension is strided
 //    (the weight of a forward layer, both operands of a weight gradient) are
 //    transposed in registers on their way into LDS.
@@ -144,9 +145,10 @@ __device__ __forceinline__ int lds_off(int row, int k) {
 // extent, so even a clamped offset cannot leave the buffer.
 constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family buffer descriptor word 3
 
-template <int R, int KMAJ>
+template <int R, int KMAJ, int NTH>
 struct BStage {
-  static constexpr int NC = KMAJ ? R * KT / 8 / 256 : 4 * (R * KT / 32) / 256;
+  static constexpr int NC = KMAJ ? R * KT / 8 / NTH : 4 * (R * KT / 32) / NTH;
+  static_assert(NC > 0, "tile too small for the thread count");
   uint4 v[NC];
   uint32_t voff[NC];
   uint32_t rowbad;
@@ -164,7 +166,7 @@ struct BStage {
       kstep = 2;
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
-        const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
+        const int c = tid + NTH * i, row = c >> 3, kc = (c & 7) * 8;
         int rr = row;
         if (r0 + row >= Rmax) { rowbad |= 1u << i; rr = Rmax - 1 - r0; }
         voff[i] = (uint32_t)(((int64_t)rr * ld + kc) * 2);
@@ -173,7 +175,7 @@ struct BStage {
       kstep = (uint32_t)(ld * 2);
 #pragma unroll
       for (int u = 0; u < NC / 4; ++u) {
-        const int id = tid + 256 * u;
+        const int id = tid + NTH * u;
         const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
         int cc = mc;
         const bool bad = r0 + mc >= Rmax;
@@ -216,10 +218,10 @@ struct BStage {
     for (int i = 0; i < NC; ++i) {
       int kk;
       if (KMAJ) {
-        kk = k0 + ((tid + 256 * i) & 7) * 8;
+        kk = k0 + ((tid + NTH * i) & 7) * 8;
         kpart[i] = max(0, min(8, K - kk));
       } else {
-        const int id = tid + 256 * (i / 4);
+        const int id = tid + NTH * (i / 4);
         kk = k0 + (id % (KT / 4)) * 4 + (i % 4);
         kpart[i] = kk < K ? 8 : 0;
       }
@@ -244,13 +246,13 @@ struct BStage {
     if (KMAJ) {
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
-        const int c = tid + 256 * i, row = c >> 3, kc = (c & 7) * 8;
+        const int c = tid + NTH * i, row = c >> 3, kc = (c & 7) * 8;
         *reinterpret_cast<uint4*>(s + lds_off(row, kc)) = check ? masked(i, tail) : v[i];
       }
     } else {
 #pragma unroll
       for (int u = 0; u < NC / 4; ++u) {
-        const int id = tid + 256 * u;
+        const int id = tid + NTH * u;
         const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
         uint32_t w[4][4];
 #pragma unroll
@@ -310,107 +312,8 @@ __device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t 
   }
 }
 
-// Epilogue of one wavefront's WR x WC block staged in LDS (fp32, columns
-// XOR-permuted in groups of 4 by row to spread banks).  Each lane handles 8
-// consecutive columns of a row: 8 lanes per row, 8 rows per pass.  One
-// instantiation per epilogue kind.
-template <int EPI, int F32OUT, int WR, int WC>
-__device__ __forceinline__ void store_rows(const GemmProblem& P, const float* stage, int rm0, int cn0, int lane,
-                                           int gelu_tanh) {
-  constexpr int LPR = WC / 8;       // lanes per row
-  constexpr int RPP = 64 / LPR;     // rows per pass
-  const bf16* bias = static_cast<const bf16*>(P.bias);
-  const bf16* bias2 = static_cast<const bf16*>(P.bias2);
-  const int c8 = (lane % LPR) * 8;
-  const int n = cn0 + c8;
-  if (n >= P.N) return;
-  const bool full = n + 8 <= P.N;
-  float bn[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    float b = 0.f;
-    if (n + q < P.N) {
-      if (bias) b += to_f(bias[n + q]);
-      if (bias2) b += to_f(bias2[n + q]);
-    }
-    bn[q] = b;
-  }
-#pragma unroll
-  for (int pass = 0; pass < WR / RPP; ++pass) {
-    const int row = pass * RPP + lane / LPR;
-    const int m = rm0 + row;
-    if (m >= P.M) continue;
-    float v[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = stage[row * WC + ((c8 + q) ^ ((row & 7) << 2))] + bn[q];
-    const int64_t o = (int64_t)m * P.ldo + n;
-    if (EPI == EPI_STORE && F32OUT) {
-      float* dst = static_cast<float*>(P.out) + o;
-      if (full && P.vec_out) {
-        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
-      } else {
-        for (int q = 0; q < 8 && n + q < P.N; ++q) dst[q] = v[q];
-      }
-    } else if (EPI == EPI_RESID) {
-      float* dst = static_cast<float*>(P.out) + o;
-      const float* res = P.resid + (int64_t)m * P.ldr + n;
-      if (full && P.vec_out) {
-        const float4 r0 = *reinterpret_cast<const float4*>(res);
-        const float4 r1 = *reinterpret_cast<const float4*>(res + 4);
-        *reinterpret_cast<float4*>(dst) = make_float4(v[0] + r0.x, v[1] + r0.y, v[2] + r0.z, v[3] + r0.w);
-        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4] + r1.x, v[5] + r1.y, v[6] + r1.z, v[7] + r1.w);
-      } else {
-        for (int q = 0; q < 8 && n + q < P.N; ++q) dst[q] = res[q] + v[q];
-      }
-    } else {
-      bf16 out[8], out2[8];
-      if (EPI == EPI_GELU) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          out2[q] = from_f<bf16>(v[q]);
-          out[q] = from_f<bf16>(gelu_f(v[q], gelu_tanh));
-        }
-      } else if (EPI == EPI_GELU_BWD) {
-        bf16 pre[8];
-        const bf16* ap = static_cast<const bf16*>(P.aux) + (int64_t)m * P.ldaux + n;
-        if (full && P.vec_out) {
-          *reinterpret_cast<uint4*>(pre) = *reinterpret_cast<const uint4*>(ap);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) pre[q] = n + q < P.N ? ap[q] : from_f<bf16>(0.f);
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) out[q] = from_f<bf16>(v[q] * gelu_grad_f(to_f(pre[q]), gelu_tanh));
-      } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) out[q] = from_f<bf16>(v[q]);
-      }
-      bf16* dst = static_cast<bf16*>(P.out) + o;
-      if (full && P.vec_out) {
-        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(out);
-        if (EPI == EPI_GELU)
-          *reinterpret_cast<uint4*>(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n) =
-              *reinterpret_cast<const uint4*>(out2);
-      } else {
-        for (int q = 0; q < 8 && n + q < P.N; ++q) {
-          dst[q] = out[q];
-          if (EPI == EPI_GELU) static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + q] = out2[q];
-        }
-      }
-    }
-  }
-}
-
-// Workgroups are dispatched to the 8 XCDs round-robin by block id.  Map
-// block ids so that each XCD owns one contiguous range of tiles, and order
-// tiles inside a problem in bands of kGroupM tile rows, so that the tiles
-// sharing one XCD's L2 also share A row panels and B column panels.
 #ifndef FAL_GEMM_REMAP
 #define FAL_GEMM_REMAP 1
-#endif
-#ifndef FAL_GEMM_STAGE_EPI
-#define FAL_GEMM_STAGE_EPI 0
 #endif
 #ifndef FAL_GEMM_GROUP_M
 #define FAL_GEMM_GROUP_M 8
@@ -430,11 +333,13 @@ __device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, in
   tn = in / gs;
 }
 
-// BM x BN output tile per 256-thread workgroup, 2 x 2 wavefronts of
-// (BM/2) x (BN/2), K staged through two LDS buffers 64 at a time.
-template <int AK, int BKM, int BM, int BN>
-__global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh) {
-  constexpr int FM = BM / 32, FN = BN / 32;  // 16x16 fragments per wavefront
+// BM x BN output tile per workgroup of WGM x WGN wavefronts, each owning a
+// (BM/WGM) x (BN/WGN) block; K staged through two LDS buffers 64 at a time.
+template <int AK, int BKM, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh) {
+  constexpr int NTH = 64 * WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wavefront tile
+  constexpr int FM = WTM / 16, FN = WTN / 16;    // 16x16 fragments per wavefront
   // one LDS block: two stages of A, two of B; reused for the epilogue
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * (BM + BN) * LDK];
   auto sA = [&](int st) { return smem + st * BM * LDK; };
@@ -457,7 +362,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
 #endif
   const int m0 = tmi * BM, n0 = tni * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
   f32x4_t acc[FM][FN];
 #pragma unroll
@@ -480,10 +385,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
       const int koff = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + lds_off(wm * (BM / 2) + i * 16 + (lane & 15), koff));
+        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + lds_off(wm * WTM + i * 16 + (lane & 15), koff));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + lds_off(wn * (BN / 2) + j * 16 + (lane & 15), koff));
+        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + lds_off(wn * WTN + j * 16 + (lane & 15), koff));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -492,11 +397,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     }
   };
   const bool edge = (m0 + BM > P.M) || (n0 + BN > P.N);
-  BStage<BM, AK> sa;
-  BStage<BN, BKM> sb;
-  int fseg = 0, fk = 0, fK = P.K;
+  BStage<BM, AK, NTH> sa;
+  BStage<BN, BKM, NTH> sb;
+  int fk = 0, fK = P.K;
   auto seg_init = [&](int seg, int k0) {
-    fseg = seg;
     fK = seg ? P.K2 : P.K;
     fk = k0;
     sa.init(static_cast<const bf16*>(seg ? P.A2 : P.A), seg ? P.lda2 : P.lda, m0, P.M, fK, tid);
@@ -539,7 +443,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
   }
 
   // acc[i][j][r] holds C[row 4*(lane/16) + r][col lane%16] of 16x16 tile (i, j).
-  const int mb = m0 + wm * (BM / 2) + (lane >> 4) * 4, nb = n0 + wn * (BN / 2) + (lane & 15);
+  const int mb = m0 + wm * WTM + (lane >> 4) * 4, nb = n0 + wn * WTN + (lane & 15);
   if (P.splits > 1) {
     float* part = P.part + (int64_t)split * P.M * P.N;
 #pragma unroll
@@ -556,7 +460,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     }
     return;
   }
-#if !FAL_GEMM_STAGE_EPI
   switch (P.epi) {
     case EPI_STORE:
       if (P.out_f32) store_tiles<EPI_STORE, 1, FM, FN>(P, acc, mb, nb, gelu_tanh);
@@ -565,34 +468,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(GemmGroup g, int gelu_tanh
     case EPI_GELU: store_tiles<EPI_GELU, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
     case EPI_RESID: store_tiles<EPI_RESID, 1, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
     case EPI_GELU_BWD: store_tiles<EPI_GELU_BWD, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
-  }
-  return;
-#endif
-  // Stage each wavefront's (BM/2) x (BN/2) block through LDS (the operand
-  // buffers are free after the final barrier), then write rows with 16-byte
-  // stores.
-  constexpr int WR = BM / 2, WC = BN / 2;
-  static_assert(4 * WR * WC * 4 <= (int)sizeof(smem), "epilogue staging does not fit");
-  float* stage = reinterpret_cast<float*>(smem) + wave * WR * WC;
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = i * 16 + (lane >> 4) * 4 + r, col = j * 16 + (lane & 15);
-        stage[row * WC + (col ^ ((row & 7) << 2))] = acc[i][j][r];
-      }
-  __syncthreads();
-  const int rm0 = m0 + wm * WR, cn0 = n0 + wn * WC;
-  switch (P.epi) {
-    case EPI_STORE:
-      if (P.out_f32) store_rows<EPI_STORE, 1, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh);
-      else store_rows<EPI_STORE, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh);
-      break;
-    case EPI_GELU: store_rows<EPI_GELU, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
-    case EPI_RESID: store_rows<EPI_RESID, 1, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
-    case EPI_GELU_BWD: store_rows<EPI_GELU_BWD, 0, WR, WC>(P, stage, rm0, cn0, lane, gelu_tanh); break;
   }
 }
 
@@ -611,13 +486,30 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* part, int spli
 }
 
 // ------------------------------------------------------------- launcher --
-#ifndef FAL_GEMM_BM
-#define FAL_GEMM_BM 128
+// Two block shapes: 128x128 with 2x2 wavefronts (two workgroups per CU) and
+// 256x256 with 4x2 wavefronts of 64x128 (one per CU; half the global traffic
+// per FLOP, a quarter less LDS traffic per MFMA, the same two wavefronts per
+// SIMD).  The larger tile does about 1.25x more MFMA work per CU per unit
+// time on large launches but quantises the grid four times coarser, so the
+// launcher picks the shape with the smaller estimated time in waves.
+#ifndef FAL_GEMM_BIG_GAIN
+#define FAL_GEMM_BIG_GAIN 1.25
 #endif
-#ifndef FAL_GEMM_BN
-#define FAL_GEMM_BN 128
-#endif
-constexpr int kBM = FAL_GEMM_BM, kBN = FAL_GEMM_BN;
+constexpr int kSmall = 128, kBig = 256, kCUs = 256;
+
+static bool use_big_tiles(const GemmGroup& g) {
+  if (FAL_GEMM_BIG_GAIN <= 0.0) return false;
+  int64_t tb = 0, ts = 0;
+  for (int i = 0; i < g.n; ++i) {
+    tb += (int64_t)((g.p[i].M + kBig - 1) / kBig) * ((g.p[i].N + kBig - 1) / kBig);
+    ts += (int64_t)((g.p[i].M + kSmall - 1) / kSmall) * ((g.p[i].N + kSmall - 1) / kSmall);
+  }
+  // time in units of one 128x128 tile on a full CU
+  const double t_small = (double)((ts + 2 * kCUs - 1) / (2 * kCUs)) * 2.0;
+  const double t_big = (double)((tb + kCUs - 1) / kCUs) * 4.0 / FAL_GEMM_BIG_GAIN;
+  return t_big < t_small;
+}
+
 constexpr int kSplitTarget = 512;  // workgroups to aim for (2 per CU on 256 CUs)
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -637,7 +529,9 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
                 const char** why, float* splitk_scratch, int64_t splitk_floats) {
   *why = nullptr;
   if (g.n < 1 || g.n > kMaxGroup) { *why = "bad GEMM group size"; return hipErrorInvalidValue; }
-  const int tm = dt == BF16 ? kBM : ST, tn = dt == BF16 ? kBN : ST;
+  const bool big = dt == BF16 && use_big_tiles(g);
+  const int tsz = dt == BF16 ? (big ? kBig : kSmall) : ST;
+  const int tm = tsz, tn = tsz;
   int total = 0;
   for (int i = 0; i < g.n; ++i) {
     GemmProblem& P = g.p[i];
@@ -669,7 +563,7 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
   // Split K for launches that would leave compute units idle (fewer tiles
   // than CUs): aim for two resident workgroups per CU with at least 512 of K
   // per slice.
-  if (dt == BF16 && splitk_scratch && g.n == 1 && g.p[0].tiles_m * g.p[0].tiles_n <= 256) {
+  if (dt == BF16 && !big && splitk_scratch && g.n == 1 && g.p[0].tiles_m * g.p[0].tiles_n <= kCUs) {
     GemmProblem& P = g.p[0];
     const int tiles = P.tiles_m * P.tiles_n;
     const int want = (kSplitTarget + tiles - 1) / tiles;
@@ -682,12 +576,19 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     }
   }
   g.total_tiles = total;
-  const dim3 grid(total), block(256);
+  const dim3 grid(total), block(dt == BF16 && big ? 512 : 256);
   if (dt == BF16) {
-    if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 1, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
-    else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 0, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
-    else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<0, 1, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
-    else hipLaunchKernelGGL((gemm_bf16_mfma<0, 0, kBM, kBN>), grid, block, 0, s, g, gelu_tanh);
+#define FAL_GEMM_LAUNCH(BM, BN, WGM, WGN)                                                                      \
+  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 1, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh); \
+  else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 0, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);      \
+  else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<0, 1, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);      \
+  else hipLaunchKernelGGL((gemm_bf16_mfma<0, 0, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);
+    if (big) {
+      FAL_GEMM_LAUNCH(kBig, kBig, 4, 2)
+    } else {
+      FAL_GEMM_LAUNCH(kSmall, kSmall, 2, 2)
+    }
+#undef FAL_GEMM_LAUNCH
     const GemmProblem& P = g.p[0];
     if (g.n == 1 && P.splits > 1) {
       hipError_t e = hipGetLastError();
