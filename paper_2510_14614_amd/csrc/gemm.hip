@@ -9,7 +9,9 @@
 //    workgroup (4x2 wavefronts of 64x128), K staged through LDS 64 at a time
 //    in k-contiguous rows.  Operands whose contraction dimension is strided
 //    (the weight of a forward layer, both operands of a weight gradient) are
-//    transposed in registers on their way into LDS.
+//    transposed in registers on their way into LDS.  The epilogue (bias,
+//    GELU, residual add, GELU derivative) runs on row segments staged
+//    through LDS so every global access is a whole wavefront-tile row.
 //  * gemm_simt: fp32 FMA kernel (fp32 parity mode).
 // Both launch every problem of a group in one grid, so the independent
 // GEMMs of FAL's two branches can share a launch.
@@ -275,42 +277,133 @@ struct BStage {
   }
 };
 
-// Direct epilogue from the accumulator registers (one element per store).
-template <int EPI, int F32OUT, int FM, int FN>
-__device__ __forceinline__ void store_tiles(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], int mb, int nb,
-                                            int gelu_tanh) {
+__device__ __forceinline__ void ld4(const bf16* p, float (&v)[4]) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xFFFF0000u);
+}
+__device__ __forceinline__ void st4(bf16* p, const float (&v)[4]) {
+  union { bf16 h[4]; uint2 w; } u;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) u.h[c] = from_f<bf16>(v[c]);
+  *reinterpret_cast<uint2*>(p) = u.w;
+}
+
+// Epilogue of one row segment of four columns: v = accumulator (+ bias),
+// row m, columns n..n+3 (those < N).  full: all four in range and the rows
+// allow vector access.
+template <int EPI, int F32OUT>
+__device__ __forceinline__ void apply4(const GemmProblem& P, int m, int n, float (&v)[4], bool full, int gelu_tanh) {
+  const int64_t o = (int64_t)m * P.ldo + n;
+  if (full) {
+    if (EPI == EPI_STORE) {
+      if (F32OUT) *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) = make_float4(v[0], v[1], v[2], v[3]);
+      else st4(static_cast<bf16*>(P.out) + o, v);
+    } else if (EPI == EPI_GELU) {
+      st4(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n, v);
+      float g[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) g[c] = gelu_f(v[c], gelu_tanh);
+      st4(static_cast<bf16*>(P.out) + o, g);
+    } else if (EPI == EPI_RESID) {
+      const float4 r = *reinterpret_cast<const float4*>(P.resid + (int64_t)m * P.ldr + n);
+      *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) =
+          make_float4(r.x + v[0], r.y + v[1], r.z + v[2], r.w + v[3]);
+    } else {
+      float pre[4];
+      ld4(static_cast<const bf16*>(P.aux) + (int64_t)m * P.ldaux + n, pre);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[c] *= gelu_grad_f(pre[c], gelu_tanh);
+      st4(static_cast<bf16*>(P.out) + o, v);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      if (n + c >= P.N) continue;
+      const int64_t oc = o + c;
+      if (EPI == EPI_STORE) {
+        if (F32OUT) static_cast<float*>(P.out)[oc] = v[c];
+        else static_cast<bf16*>(P.out)[oc] = from_f<bf16>(v[c]);
+      } else if (EPI == EPI_GELU) {
+        static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + c] = from_f<bf16>(v[c]);
+        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(gelu_f(v[c], gelu_tanh));
+      } else if (EPI == EPI_RESID) {
+        static_cast<float*>(P.out)[oc] = P.resid[(int64_t)m * P.ldr + n + c] + v[c];
+      } else {
+        const float pre = to_f(static_cast<const bf16*>(P.aux)[(int64_t)m * P.ldaux + n + c]);
+        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(v[c] * gelu_grad_f(pre, gelu_tanh));
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void bias4(const GemmProblem& P, int n, bool full, float (&bn)[4]) {
   const bf16* bias = static_cast<const bf16*>(P.bias);
   const bf16* bias2 = static_cast<const bf16*>(P.bias2);
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = nb + j * 16;
-    if (n >= P.N) continue;
-    float bn = 0.f;
-    if (bias) bn += to_f(bias[n]);
-    if (bias2) bn += to_f(bias2[n]);
+  for (int c = 0; c < 4; ++c) bn[c] = 0.f;
+  if (full) {
+    float t[4];
+    if (bias) { ld4(bias + n, t); for (int c = 0; c < 4; ++c) bn[c] += t[c]; }
+    if (bias2) { ld4(bias2 + n, t); for (int c = 0; c < 4; ++c) bn[c] += t[c]; }
+  } else {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = mb + i * 16 + r;
-        if (m >= P.M) continue;
-        const float v = acc[i][j][r] + bn;
-        const int64_t o = (int64_t)m * P.ldo + n;
-        if (EPI == EPI_STORE) {
-          if (F32OUT) static_cast<float*>(P.out)[o] = v;
-          else static_cast<bf16*>(P.out)[o] = from_f<bf16>(v);
-        } else if (EPI == EPI_GELU) {
-          static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n] = from_f<bf16>(v);
-          static_cast<bf16*>(P.out)[o] = from_f<bf16>(gelu_f(v, gelu_tanh));
-        } else if (EPI == EPI_RESID) {
-          static_cast<float*>(P.out)[o] = P.resid[(int64_t)m * P.ldr + n] + v;
-        } else {
-          const float pre = to_f(static_cast<const bf16*>(P.aux)[(int64_t)m * P.ldaux + n]);
-          static_cast<bf16*>(P.out)[o] = from_f<bf16>(v * gelu_grad_f(pre, gelu_tanh));
-        }
-      }
+    for (int c = 0; c < 4; ++c)
+      if (n + c < P.N) bn[c] = (bias ? to_f(bias[n + c]) : 0.f) + (bias2 ? to_f(bias2[n + c]) : 0.f);
   }
 }
+
+// Orders this wavefront's LDS writes before its later reads (and reads
+// before later writes) without a workgroup barrier: LDS executes one
+// wavefront's instructions in order, so only compiler motion must be stopped.
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Epilogue through a wavefront-private LDS strip.  One 16-row strip of the
+// wavefront tile at a time is written from the accumulators and read back
+// with consecutive lanes on consecutive columns, so every
+// global access (output, residual, pre-activation) covers whole row segments
+// of the wavefront tile (128 B of bf16 for a 64-column tile).
+template <int EPI, int F32OUT, int FM, int FN>
+__device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], float* stage,
+                                             int mw, int nw, int lane, int gelu_tanh) {
+  constexpr int WTN = FN * 16, PITCH = WTN + 4;
+  constexpr int LPR = WTN / 4, RPI = 64 / LPR;  // lanes per row, rows per access
+  const int rr = lane / LPR, cc = (lane % LPR) * 4;  // read-back position
+  const int n = nw + cc;
+  const bool full = P.vec_out && n + 4 <= P.N;
+  float bn[4];
+  bias4(P, n, full, bn);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    // straight from the MFMA layout: lane 16g+c holds rows 4g..4g+3 of
+    // column c (with the 4-float pad, 64 different banks per store)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) stage[((lane >> 4) * 4 + r) * PITCH + 16 * j + (lane & 15)] = acc[i][j][r];
+    wave_lds_order();
+    // kept rolled: unrolling it multiplies the epilogue code (one copy per
+    // output kind) several-fold, and the once-per-tile epilogue then runs
+    // out of the instruction cache
+#pragma unroll 1
+    for (int k = 0; k < 16 / RPI; ++k) {
+      const int r = k * RPI + rr;
+      const float4 t = *reinterpret_cast<const float4*>(stage + r * PITCH + cc);
+      const int m = mw + 16 * i + r;
+      if (m < P.M && n < P.N) {
+        float v[4] = {t.x + bn[0], t.y + bn[1], t.z + bn[2], t.w + bn[3]};
+        apply4<EPI, F32OUT>(P, m, n, v, full, gelu_tanh);
+      }
+    }
+    wave_lds_order();
+  }
+}
+
+
 
 #ifndef FAL_GEMM_REMAP
 #define FAL_GEMM_REMAP 1
@@ -443,31 +536,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
   }
 
   // acc[i][j][r] holds C[row 4*(lane/16) + r][col lane%16] of 16x16 tile (i, j).
-  const int mb = m0 + wm * WTM + (lane >> 4) * 4, nb = n0 + wn * WTN + (lane & 15);
-  if (P.splits > 1) {
-    float* part = P.part + (int64_t)split * P.M * P.N;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = nb + j * 16;
-      if (n >= P.N) continue;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = mb + i * 16 + r;
-          if (m < P.M) part[(int64_t)m * P.N + n] = acc[i][j][r];
-        }
-    }
+  // The main loop ended with a barrier, so the LDS tiles are free: each
+  // wavefront stages its strips in a private slice.
+  float* stage = reinterpret_cast<float*>(smem) + wave * 16 * (WTN + 4);
+  static_assert(WGM * WGN * 16 * (WTN + 4) * 4 <= (int)sizeof(smem), "epilogue staging exceeds LDS");
+  const int mw = m0 + wm * WTM, nw = n0 + wn * WTN;
+  if (P.splits > 1) {  // raw fp32 partial of this K slice, row pitch N
+    GemmProblem Q = P;
+    Q.out = P.part + (int64_t)split * P.M * P.N;
+    Q.ldo = P.N;
+    Q.bias = Q.bias2 = nullptr;
+    Q.vec_out = (P.N & 3) == 0;
+    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
     return;
   }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_tiles<EPI_STORE, 1, FM, FN>(P, acc, mb, nb, gelu_tanh);
-      else store_tiles<EPI_STORE, 0, FM, FN>(P, acc, mb, nb, gelu_tanh);
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
       break;
-    case EPI_GELU: store_tiles<EPI_GELU, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
-    case EPI_RESID: store_tiles<EPI_RESID, 1, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
-    case EPI_GELU_BWD: store_tiles<EPI_GELU_BWD, 0, FM, FN>(P, acc, mb, nb, gelu_tanh); break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_GELU_BWD: store_staged<EPI_GELU_BWD, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
@@ -549,13 +639,16 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     P.splits = 1;
     P.part = nullptr;
     {
-      // 16-byte epilogue stores need 16-byte aligned rows of every output
+      // The epilogue moves 4 consecutive columns at a time (8 bytes of bf16,
+      // 16 of fp32): every row it touches, and the bias, must be aligned to that.
+      auto al = [](const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0; };
       const int el = (P.epi == EPI_RESID || (P.epi == EPI_STORE && P.out_f32)) ? 4 : 2;
-      const int per16 = 16 / el;
-      bool ok = P.out && aligned16(P.out) && P.ldo % per16 == 0;
-      if (P.epi == EPI_RESID) ok = ok && aligned16(P.resid) && P.ldr % 4 == 0;
-      if (P.epi == EPI_GELU) ok = ok && P.out2 && aligned16(P.out2) && P.ldo2 % 8 == 0;
-      if (P.epi == EPI_GELU_BWD) ok = ok && P.aux && aligned16(P.aux) && P.ldaux % 8 == 0;
+      bool ok = P.out && al(P.out, 4 * el) && P.ldo % 4 == 0;
+      if (P.bias) ok = ok && al(P.bias, 8);
+      if (P.bias2) ok = ok && al(P.bias2, 8);
+      if (P.epi == EPI_RESID) ok = ok && al(P.resid, 16) && P.ldr % 4 == 0;
+      if (P.epi == EPI_GELU) ok = ok && P.out2 && al(P.out2, 8) && P.ldo2 % 4 == 0;
+      if (P.epi == EPI_GELU_BWD) ok = ok && P.aux && al(P.aux, 8) && P.ldaux % 4 == 0;
       P.vec_out = ok ? 1 : 0;
     }
     total += P.tiles_m * P.tiles_n;

@@ -46,7 +46,7 @@ struct GemmProblem {
   // filled in by the launcher
   int tiles_m, tiles_n, tile_start;
   int splits;        // K split into this many slices (fp32 partials + reduce)
-  int vec_out;       // outputs (and residual / aux inputs) allow 16-byte rows
+  int vec_out;       // rows of outputs / residual / aux (and the biases) allow 4-column vectors
   float* part;       // [splits][M][N] fp32 partials when splits > 1
 };
 

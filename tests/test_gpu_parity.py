@@ -91,6 +91,21 @@ def test_long_sequence_multi_block_attention(arch, hd):
                  label=f"long a{arch} hd{hd}")
 
 
+@pytest.mark.parametrize("arch", [ARCH_FAL, ARCH_FALPLUS])
+def test_large_tile_ragged_rows(arch):
+    # 2000 token rows (not a multiple of 256) with launches large enough for
+    # the 256x256 GEMM tile: the LM head (V=50257, ragged columns) and the
+    # FFN up / GELU-backward products (d_ff 8192) take it, with edge tiles in
+    # both dimensions and the staged epilogue of every output kind.
+    cfg = Config(n_layer=2, d_model=128, n_head=2, head_dim=64, d_ff=8192, vocab=50257, seq_len=1000,
+                 batch=2, arch=arch, dtype=1, sched=SCHED_STREAMS_MERGED)
+    log(f"large-tile ragged rows arch={arch}")
+    g, blocks = synth.make_params(cfg, seed=10)
+    tok = synth.make_tokens(cfg, seed=11)
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"large-tile a{arch}")
+
+
 def _all_outputs(out):
     arrs = [np.array([out["loss"]]), out["logits"]]
     arrs += [out["grads_global"][k] for k in sorted(out["grads_global"])]
