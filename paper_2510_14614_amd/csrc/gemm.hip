@@ -600,7 +600,26 @@ static bool use_big_tiles(const GemmGroup& g) {
   return t_big < t_small;
 }
 
-constexpr int kSplitTarget = 512;  // workgroups to aim for (2 per CU on 256 CUs)
+constexpr int kSlots = 2 * kCUs;    // resident 128x128 workgroups (two per CU)
+constexpr int kMaxSplits = 16;
+
+// Split-K factor for a launch of `tiles` 128x128 tiles over nt k-tiles:
+// minimises (rounds of all workgroup slots) x (k-tiles per slice) plus the
+// partials' extra write and read, about one k-tile round per split for
+// every 128 tiles.  1 = no split.
+static int choose_splits(int tiles, int nt, int64_t MN, int64_t scratch_floats) {
+  auto cost = [&](int sp) {
+    const double rounds = (double)((tiles * sp + kSlots - 1) / kSlots);
+    return rounds * ((nt + sp - 1) / sp) + (sp > 1 ? sp * tiles / 128.0 : 0.0);
+  };
+  int best = 1;
+  double cbest = cost(1);
+  for (int sp = 2; sp <= kMaxSplits && nt / sp >= 4 && (int64_t)sp * MN <= scratch_floats; ++sp) {
+    const double c = cost(sp);
+    if (c < cbest) { cbest = c; best = sp; }
+  }
+  return best;
+}
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 static const char* check_vec_operand(const void* X, int64_t ld, int kmaj, int rows, int K) {
@@ -654,15 +673,12 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     total += P.tiles_m * P.tiles_n;
   }
   // Split K for launches that would leave compute units idle (fewer tiles
-  // than CUs): aim for two resident workgroups per CU with at least 512 of K
-  // per slice.
+  // than CUs); fp32 plain outputs only (the weight gradients).
   if (dt == BF16 && !big && splitk_scratch && g.n == 1 && g.p[0].tiles_m * g.p[0].tiles_n <= kCUs) {
     GemmProblem& P = g.p[0];
     const int tiles = P.tiles_m * P.tiles_n;
-    const int want = (kSplitTarget + tiles - 1) / tiles;
-    int sp = std::min({want, P.K / 512, 8});
-    if (sp > 1 && P.K2 == 0 && P.epi == EPI_STORE && P.out_f32 &&
-        (int64_t)sp * P.M * P.N <= splitk_floats) {
+    const int sp = choose_splits(tiles, (P.K + KT - 1) / KT, (int64_t)P.M * P.N, splitk_floats);
+    if (sp > 1 && P.K2 == 0 && P.epi == EPI_STORE && P.out_f32) {
       P.splits = sp;
       P.part = splitk_scratch;
       total = tiles * sp;

@@ -141,46 +141,92 @@ hipError_t embed_bwd(const int32_t* tokens, int B, int T, int V, int d, const fl
 }
 
 // ---------------------------------------------------------- cross-entropy --
+// One 1024-thread workgroup per token row (Sec. 2: next-token cross-entropy
+// over the LM-head logits).  The row is read from HBM once, as float4 chunks
+// held in registers (chunk c on thread c % 1024); each thread reduces its
+// chunks to (max, sum of exp) and keeps exp(x - its max), so the gradient
+//   dlogits = (softmax(x) - onehot(target)) / n
+// needs one more exponential per thread, not per element.  Columns V..ldd of
+// the gradient row are written as zeros.
+constexpr int kCeThreads = 1024;
+
 template <typename S>
-__global__ __launch_bounds__(256) void ce_kernel(const float* logits, int64_t ldl, const int32_t* tok, int T,
-                                                 int V, float inv_n, S* dl, int64_t ldd, float* row_loss) {
-  __shared__ float sm[4], ss[4];
-  const int m = blockIdx.x, b = m / T, t = m % T;
+__device__ __forceinline__ void st4g(S* p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void st4g<float>(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+template <>
+__device__ __forceinline__ void st4g<bf16>(bf16* p, float a, float b, float c, float d) {
+  union { bf16 h[4]; uint2 w; } u;
+  u.h[0] = from_f<bf16>(a); u.h[1] = from_f<bf16>(b); u.h[2] = from_f<bf16>(c); u.h[3] = from_f<bf16>(d);
+  *reinterpret_cast<uint2*>(p) = u.w;
+}
+
+// (m1, s1) <- combination of two (max, sum exp(x - max)) pairs
+__device__ __forceinline__ void lse_combine(float& m1, float& s1, float m2, float s2) {
+  const float mm = fmaxf(m1, m2);
+  if (mm == -INFINITY) return;
+  s1 = (m1 == -INFINITY ? 0.f : s1 * __expf(m1 - mm)) + (m2 == -INFINITY ? 0.f : s2 * __expf(m2 - mm));
+  m1 = mm;
+}
+
+template <typename S, int NPT>
+__global__ __launch_bounds__(kCeThreads) void ce_rows(const float* logits, int64_t ldl, const int32_t* tok, int T,
+                                                      int V, float inv_n, S* dl, int64_t ldd, float* row_loss) {
+  __shared__ float rm[kCeThreads / FAL_WAVE], rs[kCeThreads / FAL_WAVE];
+  const int m = blockIdx.x, b = m / T, t = m % T, tid = threadIdx.x;
   int tgt = tok[(int64_t)b * (T + 1) + t + 1];
   tgt = min(max(tgt, 0), V - 1);
   const float* l = logits + (int64_t)m * ldl;
-  float mx = -INFINITY, sum = 0.f;
-  for (int j = threadIdx.x; j < V; j += 256) {
-    const float x = l[j];
-    if (x > mx) {
-      sum = sum * expf(mx - x) + 1.f;
-      mx = x;
+  const int nv = (V + 3) / 4, nd = (int)(ldd / 4);
+  float x[NPT][4];
+  float lm = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c = tid + kCeThreads * i;
+    if (c < nv) {
+      const float4 v = *reinterpret_cast<const float4*>(l + 4 * c);
+      x[i][0] = v.x; x[i][1] = 4 * c + 1 < V ? v.y : -INFINITY;
+      x[i][2] = 4 * c + 2 < V ? v.z : -INFINITY; x[i][3] = 4 * c + 3 < V ? v.w : -INFINITY;
     } else {
-      sum += expf(x - mx);
+      x[i][0] = x[i][1] = x[i][2] = x[i][3] = -INFINITY;
     }
-  }
-  // combine (max, sum) pairs across the wavefront, then across wavefronts
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float om = __shfl_xor(mx, o, FAL_WAVE), os = __shfl_xor(sum, o, FAL_WAVE);
-    const float nm = fmaxf(mx, om);
-    sum = (mx == -INFINITY ? 0.f : sum * expf(mx - nm)) + (om == -INFINITY ? 0.f : os * expf(om - nm));
-    mx = nm;
+    for (int e = 0; e < 4; ++e) lm = fmaxf(lm, x[i][e]);
   }
-  const int w = threadIdx.x / FAL_WAVE;
-  if (threadIdx.x % FAL_WAVE == 0) { sm[w] = mx; ss[w] = sum; }
+  float ls = 0.f;
+  if (lm != -INFINITY) {
+#pragma unroll
+    for (int i = 0; i < NPT; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[i][e] = __expf(x[i][e] - lm);  // exp(-inf) = 0 for masked columns
+        ls += x[i][e];
+      }
+  }
+  float gm = lm, gs = ls;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) lse_combine(gm, gs, __shfl_xor(gm, o, FAL_WAVE), __shfl_xor(gs, o, FAL_WAVE));
+  if ((tid & (FAL_WAVE - 1)) == 0) { rm[tid / FAL_WAVE] = gm; rs[tid / FAL_WAVE] = gs; }
   __syncthreads();
-  float gm = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
-  float gs = 0.f;
+  gm = rm[0]; gs = rs[0];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) gs += ss[i] * expf(sm[i] - gm);
-  const float lse = gm + logf(gs);
-  if (threadIdx.x == 0) row_loss[m] = lse - l[tgt];
+  for (int w = 1; w < kCeThreads / FAL_WAVE; ++w) lse_combine(gm, gs, rm[w], rs[w]);
+  const float lse = gm + __logf(gs);
+  if (tid == 0) row_loss[m] = lse - l[tgt];
+  const float sc = lm == -INFINITY ? 0.f : __expf(lm - lse) * inv_n;
   S* drow = dl + (int64_t)m * ldd;
-  for (int j = threadIdx.x; j < ldd; j += 256) {
-    float g = 0.f;
-    if (j < V) g = (expf(l[j] - lse) - (j == tgt ? 1.f : 0.f)) * inv_n;
-    drow[j] = from_f<S>(g);
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c = tid + kCeThreads * i;
+    if (c >= nd) continue;
+    float g[4] = {0.f, 0.f, 0.f, 0.f};
+    if (c < nv) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) g[e] = x[i][e] * sc - (4 * c + e == tgt ? inv_n : 0.f);
+    }
+    st4g<S>(drow + 4 * c, g[0], g[1], g[2], g[3]);
   }
 }
 
@@ -202,12 +248,25 @@ hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32
                          int V, void* dlogits, int64_t ldd, float* row_loss, float* loss, hipStream_t s) {
   const int M = B * T;
   const float inv_n = 1.f / (float)M;
-  if (dt == BF16)
-    hipLaunchKernelGGL((ce_kernel<bf16>), dim3(M), dim3(256), 0, s, logits, ldl, tokens, T, V, inv_n,
-                       static_cast<bf16*>(dlogits), ldd, row_loss);
-  else
-    hipLaunchKernelGGL((ce_kernel<float>), dim3(M), dim3(256), 0, s, logits, ldl, tokens, T, V, inv_n,
+  // float4 rows: leading dimensions multiples of 4 covering the vocabulary
+  if (ldl % 4 || ldd % 4 || ldl < V || ldd < V) return hipErrorInvalidValue;
+  const int64_t nd = ldd / 4;
+  const int need = (int)((nd + kCeThreads - 1) / kCeThreads);
+  const dim3 grid(M), block(kCeThreads);
+#define FAL_CE_LAUNCH(NPT)                                                                                    \
+  if (dt == BF16)                                                                                            \
+    hipLaunchKernelGGL((ce_rows<bf16, NPT>), grid, block, 0, s, logits, ldl, tokens, T, V, inv_n,              \
+                       static_cast<bf16*>(dlogits), ldd, row_loss);                                          \
+  else                                                                                                       \
+    hipLaunchKernelGGL((ce_rows<float, NPT>), grid, block, 0, s, logits, ldl, tokens, T, V, inv_n,             \
                        static_cast<float*>(dlogits), ldd, row_loss);
+  if (need <= 1) { FAL_CE_LAUNCH(1) }
+  else if (need <= 4) { FAL_CE_LAUNCH(4) }
+  else if (need <= 8) { FAL_CE_LAUNCH(8) }
+  else if (need <= 13) { FAL_CE_LAUNCH(13) }  // GPT-2 vocabulary (50257 padded to 50304)
+  else if (need <= 16) { FAL_CE_LAUNCH(16) }
+  else return hipErrorInvalidValue;
+#undef FAL_CE_LAUNCH
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (loss) {
