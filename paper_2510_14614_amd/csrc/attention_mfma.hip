@@ -11,12 +11,15 @@
 //    and the row max/sum need one cross-lane exchange (lane ^ 32).  The
 //    accumulator registers of S^T are exactly the B operand of O^T = V^T P^T
 //    (the contraction index order of A and B only has to agree), so P never
-//    leaves registers; V is transposed on its way into LDS.
+//    leaves registers.
 //  * dK/dV kernel computes S = Q K^T and dP = dO V^T per key block; P^T and
-//    dS^T feed dV += P^T dO and dK += dS^T Q straight from registers, with
-//    dO and Q transposed in LDS.
+//    dS^T feed dV += P^T dO and dK += dS^T Q straight from registers.
 //  * dQ kernel computes S^T and dP^T per query block and accumulates
 //    dQ^T += K^T dS^T.
+//  * Every tile sits in LDS row-major, as loaded.  Operands that contract
+//    over a tile's rows (V, dO, Q, K in the second products) are read with
+//    the gfx950 LDS transpose load (ds_read_b64_tr_b16), so no transposed
+//    copy is ever written.
 // Accumulator layout of one 32x32 tile: lane l, register r holds
 // C[8*(r/4) + 4*(l/32) + r%4][l%32].
 #include <math.h>
@@ -31,7 +34,6 @@ typedef __bf16 bf16x4v __attribute__((ext_vector_type(4)));
 typedef float f32x16v __attribute__((ext_vector_type(16)));
 
 constexpr int AT = 64;        // rows per LDS tile of the streamed dimension
-constexpr int ATP = AT + 8;   // padded row of a transposed tile ([dim][row])
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ f32x16v mfma32(bf16x8v a, bf16x8v b, f32x16v c) {
@@ -66,8 +68,7 @@ __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 *
 // registers: load() issues the global loads (rows past T read a clamped
 // row), store() writes LDS (zeroing rows past T).  Loading the next tile
 // before computing on the current one keeps its memory latency behind the
-// MFMA work.  RowTile stores row-major [row][HD + 8]; TTile stores the tile
-// transposed, [dim][AT + 8], each thread moving 4 rows x 8 dims.
+// MFMA work.  Tiles are stored row-major, [row][HD + 8].
 template <int HD>
 struct RowTile {
   static constexpr int CH = HD / 8, N = (AT * CH + 255) / 256;
@@ -92,49 +93,6 @@ struct RowTile {
   }
 };
 
-template <int HD>
-struct TTile {
-  static constexpr int CH = HD / 8, U = (AT / 4) * CH, N = (U + 255) / 256;
-  uint4 v[N][4];
-  __device__ __forceinline__ void load(const bf16* src, int64_t ld, int row0, int T, int tid) {
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const int i = tid + 256 * k;
-      if (i >= U) continue;
-      const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = min(row0 + rg + j, T - 1);
-        v[k][j] = *reinterpret_cast<const uint4*>(src + (int64_t)row * ld + c);
-      }
-    }
-  }
-  __device__ __forceinline__ void store(bf16* s, int row0, int T, int tid) const {
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const int i = tid + 256 * k;
-      if (i >= U) continue;
-      const int rg = (i % (AT / 4)) * 4, c = (i / (AT / 4)) * 8;
-      uint32_t w[4][4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint4 x = row0 + rg + j < T ? v[k][j] : make_uint4(0, 0, 0, 0);
-        w[j][0] = x.x; w[j][1] = x.y; w[j][2] = x.z; w[j][3] = x.w;
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint2 lo, hi;
-        lo.x = (w[0][q] & 0xFFFFu) | (w[1][q] << 16);
-        lo.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
-        hi.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
-        hi.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
-        *reinterpret_cast<uint2*>(s + (c + 2 * q) * ATP + rg) = lo;
-        *reinterpret_cast<uint2*>(s + (c + 2 * q + 1) * ATP + rg) = hi;
-      }
-    }
-  }
-};
-
 // A or B operand fragment from a row-major LDS tile: row `row`, dims
 // 16*kk + 8*g .. +7.
 template <int HD>
@@ -142,11 +100,29 @@ __device__ __forceinline__ bf16x8v frag_rows(const bf16* s, int row, int kk, int
   return *reinterpret_cast<const bf16x8v*>(s + row * (HD + 8) + 16 * kk + 8 * g);
 }
 
-// Operand fragment from a transposed LDS tile for a contraction over the
-// tile's rows: dim `dim`, rows {16*ks + 8*(j/4) + 4*g + j%4}.
-__device__ __forceinline__ bf16x8v frag_cols(const bf16* s, int dim, int rowbase, int ks, int g) {
-  const bf16* p = s + dim * ATP + rowbase + 16 * ks + 4 * g;
-  return ld_2x4(p, p + 8);
+// Operand fragment for a contraction over the rows of a row-major LDS tile
+// [row][HD + 8]: lane (c = lane % 32, g = lane / 32) gets column colbase + c
+// of rows rowbase + {4g..4g+3, 8+4g..8+4g+3}, the order in which the
+// accumulator registers of a 32x32 tile hold them.  ds_read_b64_tr_b16
+// hands lane i of each 16-lane group element i % 4 of the 8-byte chunks
+// addressed by lanes 4j + i / 4 (j = 0..3): lane L addresses row
+// rowbase + 4g + L / 4 (then + 8), columns 4 (L % 4)..+3 of its group's 16.
+typedef short i16x4v __attribute__((ext_vector_type(4)));
+template <int HD>
+__device__ __forceinline__ bf16x8v frag_tr(const bf16* s, int rowbase, int colbase, int lane) {
+  const int L = lane & 15;
+  const int col = colbase + 16 * ((lane >> 4) & 1) + 4 * (L & 3);
+  const int row = rowbase + 4 * (lane >> 5) + (L >> 2);
+  typedef __attribute__((address_space(3))) i16x4v lds_i16x4;
+  const lds_i16x4* p0 = reinterpret_cast<const lds_i16x4*>(
+      (__attribute__((address_space(3))) const char*)(s + row * (HD + 8) + col));
+  const lds_i16x4* p1 = reinterpret_cast<const lds_i16x4*>(
+      (__attribute__((address_space(3))) const char*)(s + (row + 8) * (HD + 8) + col));
+  const i16x4v a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(p0));
+  const i16x4v b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(p1));
+  const i16x4v* pa = &a;
+  const i16x4v* pb = &b;
+  return ld_2x4(reinterpret_cast<const bf16*>(pa), reinterpret_cast<const bf16*>(pb));
 }
 
 // Operand fragment straight from global memory (row of a head slice).
@@ -163,11 +139,11 @@ __device__ __forceinline__ bf16x8v frag_global(const bf16* src, int64_t ld, int 
 
 // ------------------------------------------------------------- forward --
 template <int HD>
-__global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int H, bf16* O, int64_t ldo,
+__global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, int H, bf16* O, int64_t ldo,
                                                      float* lse) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sVt[HD * ATP];
+  __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
   // grid (H, B, blocks): the causal block index varies slowest, so the
   // round-robin dispatch over XCDs gives every XCD the same mix of long and
   // short blocks; the longest (latest) query blocks are dispatched first.
@@ -193,14 +169,13 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int
 
   const int kend = min(T, qb * 128 + 128);
   const int wave_kend = min(T, q0 + 32);
-  RowTile<HD> rk;
-  TTile<HD> rv;
+  RowTile<HD> rk, rv;
   rk.load(Kg, ld, 0, T, tid);
   rv.load(Vg, ld, 0, T, tid);
   for (int k0 = 0; k0 < kend; k0 += AT) {
     __syncthreads();
     rk.store(sK, k0, T, tid);
-    rv.store(sVt, k0, T, tid);
+    rv.store(sV, k0, T, tid);
     __syncthreads();
     if (k0 + AT < kend) {
       rk.load(Kg, ld, k0 + AT, T, tid);
@@ -239,8 +214,8 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int
       const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        acc[t] = mfma32(frag_cols(sVt, 32 * t + c, 32 * sub, 0, g), p0, acc[t]);
-        acc[t] = mfma32(frag_cols(sVt, 32 * t + c, 32 * sub, 1, g), p1, acc[t]);
+        acc[t] = mfma32(frag_tr<HD>(sV, 32 * sub, 32 * t, lane), p0, acc[t]);
+        acc[t] = mfma32(frag_tr<HD>(sV, 32 * sub + 16, 32 * t, lane), p1, acc[t]);
       }
     }
   }
@@ -263,14 +238,13 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16* qkv, int T, int
 
 // ------------------------------------------------------- backward: dK dV --
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
-                                                          const float* lse, const float* Dvec, int T, int H,
-                                                          bf16* dqkv) {
+// two wavefronts per SIMD where the registers allow it (head_dim 64; at 128
+// the dK and dV accumulators alone take 64 registers per lane)
+__global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
+    const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, bf16* dqkv) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sQ[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sdO[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sQt[HD * ATP];
-  __shared__ __attribute__((aligned(16))) bf16 sdOt[HD * ATP];
   __shared__ float sL[AT], sD[AT];
   // grid (H, B, blocks): causal block index slowest (even XCD mix); the
   // earliest key blocks see the most queries and are dispatched first
@@ -300,19 +274,14 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
   for (int t = 0; t < NT; ++t) { dk[t] = zero16(); dv[t] = zero16(); }
 
   RowTile<HD> rq, ro;
-  TTile<HD> rqt, rot;
   if (kb0 < T) {
     rq.load(Qg, ld, kb0, T, tid);
     ro.load(dOg, lddo, kb0, T, tid);
-    rqt.load(Qg, ld, kb0, T, tid);
-    rot.load(dOg, lddo, kb0, T, tid);
   }
   for (int q0 = kb0; q0 < T; q0 += AT) {
     __syncthreads();
     rq.store(sQ, q0, T, tid);
     ro.store(sdO, q0, T, tid);
-    rqt.store(sQt, q0, T, tid);
-    rot.store(sdOt, q0, T, tid);
     if (tid < AT) {
       const int tq = q0 + tid;
       sL[tid] = tq < T ? Lg[tq] * kLog2e : 0.f;
@@ -322,8 +291,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
     if (q0 + AT < T) {
       rq.load(Qg, ld, q0 + AT, T, tid);
       ro.load(dOg, lddo, q0 + AT, T, tid);
-      rqt.load(Qg, ld, q0 + AT, T, tid);
-      rot.load(dOg, lddo, q0 + AT, T, tid);
     }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
@@ -348,10 +315,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
       const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        dv[t] = mfma32(p0, frag_cols(sdOt, 32 * t + c, 32 * sub, 0, g), dv[t]);
-        dv[t] = mfma32(p1, frag_cols(sdOt, 32 * t + c, 32 * sub, 1, g), dv[t]);
-        dk[t] = mfma32(d0, frag_cols(sQt, 32 * t + c, 32 * sub, 0, g), dk[t]);
-        dk[t] = mfma32(d1, frag_cols(sQt, 32 * t + c, 32 * sub, 1, g), dk[t]);
+        dv[t] = mfma32(p0, frag_tr<HD>(sdO, 32 * sub, 32 * t, lane), dv[t]);
+        dv[t] = mfma32(p1, frag_tr<HD>(sdO, 32 * sub + 16, 32 * t, lane), dv[t]);
+        dk[t] = mfma32(d0, frag_tr<HD>(sQ, 32 * sub, 32 * t, lane), dk[t]);
+        dk[t] = mfma32(d1, frag_tr<HD>(sQ, 32 * sub + 16, 32 * t, lane), dk[t]);
       }
     }
   }
@@ -372,13 +339,12 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_mfma(const bf16* qkv, const
 
 // ----------------------------------------------------------- backward: dQ --
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
                                                         const float* lse, const float* Dvec, int T, int H,
                                                         bf16* dqkv) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sKt[HD * ATP];
   // grid (H, B, blocks): the causal block index varies slowest, so the
   // round-robin dispatch over XCDs gives every XCD the same mix of long and
   // short blocks; the longest (latest) query blocks are dispatched first.
@@ -410,20 +376,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const b
   const int kend = min(T, qb * 128 + 128);
   const int wave_kend = min(T, q0 + 32);
   RowTile<HD> rk, rv;
-  TTile<HD> rkt;
   rk.load(Kg, ld, 0, T, tid);
   rv.load(Vg, ld, 0, T, tid);
-  rkt.load(Kg, ld, 0, T, tid);
   for (int k0 = 0; k0 < kend; k0 += AT) {
     __syncthreads();
     rk.store(sK, k0, T, tid);
     rv.store(sV, k0, T, tid);
-    rkt.store(sKt, k0, T, tid);
     __syncthreads();
     if (k0 + AT < kend) {
       rk.load(Kg, ld, k0 + AT, T, tid);
       rv.load(Vg, ld, k0 + AT, T, tid);
-      rkt.load(Kg, ld, k0 + AT, T, tid);
     }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
@@ -445,8 +407,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16* qkv, const b
       const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        dq[t] = mfma32(frag_cols(sKt, 32 * t + c, 32 * sub, 0, g), d0, dq[t]);
-        dq[t] = mfma32(frag_cols(sKt, 32 * t + c, 32 * sub, 1, g), d1, dq[t]);
+        dq[t] = mfma32(frag_tr<HD>(sK, 32 * sub, 32 * t, lane), d0, dq[t]);
+        dq[t] = mfma32(frag_tr<HD>(sK, 32 * sub + 16, 32 * t, lane), d1, dq[t]);
       }
     }
   }
