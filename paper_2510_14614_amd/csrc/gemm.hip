@@ -147,10 +147,31 @@ __device__ __forceinline__ int lds_off(int row, int k) {
 // extent, so even a clamped offset cannot leave the buffer.
 constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family buffer descriptor word 3
 
+// An operand whose contraction dimension is strided (MN-major: the weight of
+// a forward layer, both operands of a weight gradient) is staged as loaded,
+// [k][row] with rows padded by kTrPad elements, and read back with the gfx950
+// LDS transpose load.  ds_read_b64_tr_b16 gives lane i of each 16-lane
+// group element i % 4 of the 8-byte chunks addressed by lanes 4j + i / 4
+// (j = 0..3); lane L therefore addresses k-row kb + L / 4, rows 4 (L % 4)..+3
+// of the fragment, and two reads (kb, kb + 4) return the eight consecutive k
+// a 16x16x32 operand lane holds.  The pad of 16 keeps those reads at the
+// minimum number of LDS passes.
+constexpr int kTrPad = 16;
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+__device__ __forceinline__ i16x4_t lds_read_tr(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4_t*)((__attribute__((address_space(3))) char*)(const_cast<bf16*>(p))));
+}
+
 template <int R, int KMAJ, int NTH>
 struct BStage {
-  static constexpr int NC = KMAJ ? R * KT / 8 / NTH : 4 * (R * KT / 32) / NTH;
-  static_assert(NC > 0, "tile too small for the thread count");
+  static constexpr int CPR = R / 8;                         // 16-byte chunks per MN-major k-row
+  static constexpr int RP = R + kTrPad;                     // MN-major LDS row pitch
+  static constexpr int ELEMS = KMAJ ? R * KT : KT * RP;     // one LDS stage
+  static constexpr int NC = R * KT / 8 / NTH;               // 16-byte chunks per thread
+  static_assert(NC > 0 && NC <= 32, "tile / thread count mismatch");
   uint4 v[NC];
   uint32_t voff[NC];
   uint32_t rowbad;
@@ -159,34 +180,34 @@ struct BStage {
   int nbytes;      // extent of the operand from base
   uint32_t kstep;
 
+  // chunk i of this thread: k-contiguous rows (row, k) or MN-major (k, row)
+  __device__ __forceinline__ static void chunk(int i, int tid, int& row, int& k) {
+    const int c = tid + NTH * i;
+    if (KMAJ) { row = c >> 3; k = (c & 7) * 8; }
+    else { k = c / CPR; row = (c % CPR) * 8; }
+  }
+
   __device__ __forceinline__ void init(const bf16* X, int64_t ld, int r0, int Rmax, int Kseg, int tid) {
     base = reinterpret_cast<uint64_t>(KMAJ ? X + (int64_t)r0 * ld : X + r0);
     const int64_t ext = KMAJ ? (int64_t)(Rmax - r0) * ld * 2 : ((int64_t)Kseg * ld - r0) * 2;
     nbytes = (int)min<int64_t>(ext, 0x7fffffff);
     rowbad = 0;
-    if (KMAJ) {
-      kstep = 2;
+    kstep = KMAJ ? 2 : (uint32_t)(ld * 2);
 #pragma unroll
-      for (int i = 0; i < NC; ++i) {
-        const int c = tid + NTH * i, row = c >> 3, kc = (c & 7) * 8;
+    for (int i = 0; i < NC; ++i) {
+      int row, k;
+      chunk(i, tid, row, k);
+      if (KMAJ) {
         int rr = row;
         if (r0 + row >= Rmax) { rowbad |= 1u << i; rr = Rmax - 1 - r0; }
-        voff[i] = (uint32_t)(((int64_t)rr * ld + kc) * 2);
-      }
-    } else {
-      kstep = (uint32_t)(ld * 2);
-#pragma unroll
-      for (int u = 0; u < NC / 4; ++u) {
-        const int id = tid + NTH * u;
-        const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
-        int cc = mc;
-        const bool bad = r0 + mc >= Rmax;
-        if (bad) cc = ((Rmax - r0 - 1) / 8) * 8;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (bad) rowbad |= 1u << (4 * u + j);
-          voff[4 * u + j] = (uint32_t)(((int64_t)(kg + j) * ld + cc) * 2);
-        }
+        voff[i] = (uint32_t)(((int64_t)rr * ld + k) * 2);
+      } else {
+        // 8 consecutive rows per chunk; a chunk starting past the matrix is
+        // clamped (and zeroed in LDS).  Rows past the matrix inside a valid
+        // chunk only reach outputs that are never stored.
+        int cc = row;
+        if (r0 + row >= Rmax) { rowbad |= 1u << i; cc = ((Rmax - r0 - 1) / 8) * 8; }
+        voff[i] = (uint32_t)(((int64_t)k * ld + cc) * 2);
       }
     }
   }
@@ -218,15 +239,10 @@ struct BStage {
   __device__ __forceinline__ void load_tail(__amdgpu_buffer_rsrc_t rs, uint32_t so, int k0, int K, int tid) {
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
-      int kk;
-      if (KMAJ) {
-        kk = k0 + ((tid + NTH * i) & 7) * 8;
-        kpart[i] = max(0, min(8, K - kk));
-      } else {
-        const int id = tid + NTH * (i / 4);
-        kk = k0 + (id % (KT / 4)) * 4 + (i % 4);
-        kpart[i] = kk < K ? 8 : 0;
-      }
+      int row, k;
+      chunk(i, tid, row, k);
+      const int kk = k0 + k;
+      kpart[i] = KMAJ ? max(0, min(8, K - kk)) : (kk < K ? 8 : 0);
       v[i] = kpart[i] > 0 ? ld16(rs, voff[i], so) : make_uint4(0, 0, 0, 0);
     }
   }
@@ -245,35 +261,26 @@ struct BStage {
 
   // check: edge tile or tail tile (uniform); otherwise stores go straight in.
   __device__ __forceinline__ void store(bf16* s, int tid, bool check, bool tail) const {
-    if (KMAJ) {
 #pragma unroll
-      for (int i = 0; i < NC; ++i) {
-        const int c = tid + NTH * i, row = c >> 3, kc = (c & 7) * 8;
-        *reinterpret_cast<uint4*>(s + lds_off(row, kc)) = check ? masked(i, tail) : v[i];
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < NC / 4; ++u) {
-        const int id = tid + NTH * u;
-        const int kg = (id % (KT / 4)) * 4, mc = (id / (KT / 4)) * 8;
-        uint32_t w[4][4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint4 x = check ? masked(4 * u + j, tail) : v[4 * u + j];
-          w[j][0] = x.x; w[j][1] = x.y; w[j][2] = x.z; w[j][3] = x.w;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint2 lo, hi;
-          lo.x = (w[0][q] & 0xFFFFu) | (w[1][q] << 16);
-          lo.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
-          hi.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
-          hi.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
-          *reinterpret_cast<uint2*>(s + lds_off(mc + 2 * q, kg)) = lo;
-          *reinterpret_cast<uint2*>(s + lds_off(mc + 2 * q + 1, kg)) = hi;
-        }
-      }
+    for (int i = 0; i < NC; ++i) {
+      int row, k;
+      chunk(i, tid, row, k);
+      const int off = KMAJ ? lds_off(row, k) : k * RP + row;
+      *reinterpret_cast<uint4*>(s + off) = check ? masked(i, tail) : v[i];
     }
+  }
+
+  // Operand fragment of a 16x16x32 MFMA: rows row0 + lane % 16, k
+  // 32 ks + 8 (lane / 16) .. +7.
+  __device__ __forceinline__ static bf16x8_t frag(const bf16* s, int row0, int ks, int lane) {
+    if (KMAJ)
+      return *reinterpret_cast<const bf16x8_t*>(s + lds_off(row0 + (lane & 15), ks * 32 + (lane >> 4) * 8));
+    const int L = lane & 15;
+    const int k = ks * 32 + (lane >> 4) * 8 + (L >> 2);
+    const bf16* p = s + k * RP + row0 + 4 * (L & 3);
+    const i16x4_t lo = lds_read_tr(p), hi = lds_read_tr(p + 4 * RP);
+    const i16x4_t v8[2] = {lo, hi};
+    return *reinterpret_cast<const bf16x8_t*>(v8);
   }
 };
 
@@ -433,10 +440,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
   constexpr int NTH = 64 * WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wavefront tile
   constexpr int FM = WTM / 16, FN = WTN / 16;    // 16x16 fragments per wavefront
+  typedef BStage<BM, AK, NTH> StA;
+  typedef BStage<BN, BKM, NTH> StB;
   // one LDS block: two stages of A, two of B; reused for the epilogue
-  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (BM + BN) * LDK];
-  auto sA = [&](int st) { return smem + st * BM * LDK; };
-  auto sB = [&](int st) { return smem + 2 * BM * LDK + st * BN * LDK; };
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (StA::ELEMS + StB::ELEMS)];
+  auto sA = [&](int st) { return smem + st * StA::ELEMS; };
+  auto sB = [&](int st) { return smem + 2 * StA::ELEMS + st * StB::ELEMS; };
 #if FAL_GEMM_REMAP
   const int bid = xcd_remap(blockIdx.x, g.total_tiles);
 #else
@@ -475,13 +484,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
 #pragma unroll
     for (int ks = 0; ks < KT / 32; ++ks) {
       bf16x8_t a[FM], b[FN];
-      const int koff = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        a[i] = *reinterpret_cast<const bf16x8_t*>(a_s + lds_off(wm * WTM + i * 16 + (lane & 15), koff));
+      for (int i = 0; i < FM; ++i) a[i] = StA::frag(a_s, wm * WTM + i * 16, ks, lane);
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        b[j] = *reinterpret_cast<const bf16x8_t*>(b_s + lds_off(wn * WTN + j * 16 + (lane & 15), koff));
+      for (int j = 0; j < FN; ++j) b[j] = StB::frag(b_s, wn * WTN + j * 16, ks, lane);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -490,8 +496,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
     }
   };
   const bool edge = (m0 + BM > P.M) || (n0 + BN > P.N);
-  BStage<BM, AK, NTH> sa;
-  BStage<BN, BKM, NTH> sb;
+  StA sa;
+  StB sb;
   int fk = 0, fK = P.K;
   auto seg_init = [&](int seg, int k0) {
     fK = seg ? P.K2 : P.K;
