@@ -378,8 +378,9 @@ template <int EPI, int F32OUT, int FM, int FN>
 __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], float* stage,
                                              int mw, int nw, int lane, int gelu_tanh) {
   constexpr int WTN = FN * 16, PITCH = WTN + 4;
-  constexpr int LPR = WTN / 4, RPI = 64 / LPR;  // lanes per row, rows per access
-  const int rr = lane / LPR, cc = (lane % LPR) * 4;  // read-back position
+  constexpr int LPR = WTN / 4, RPI = 64 / LPR;    // lanes per row, rows per access
+  constexpr int NPASS = (16 + RPI - 1) / RPI;     // accesses per 16-row strip
+  const int rr = lane / LPR, cc = (lane % LPR) * 4;  // read-back position (rr >= RPI: idle)
   const int n = nw + cc;
   const bool full = P.vec_out && n + 4 <= P.N;
   float bn[4];
@@ -397,8 +398,9 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
     // output kind) several-fold, and the once-per-tile epilogue then runs
     // out of the instruction cache
 #pragma unroll 1
-    for (int k = 0; k < 16 / RPI; ++k) {
+    for (int k = 0; k < NPASS; ++k) {
       const int r = k * RPI + rr;
+      if (rr >= RPI || r >= 16) continue;
       const float4 t = *reinterpret_cast<const float4*>(stage + r * PITCH + cc);
       const int m = mw + 16 * i + r;
       if (m < P.M && n < P.N) {
@@ -582,31 +584,39 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* part, int spli
 }
 
 // ------------------------------------------------------------- launcher --
-// Two block shapes: 128x128 with 2x2 wavefronts (two workgroups per CU) and
-// 256x256 with 4x2 wavefronts of 64x128 (one per CU; half the global traffic
-// per FLOP, a quarter less LDS traffic per MFMA, the same two wavefronts per
-// SIMD).  The larger tile does about 1.25x more MFMA work per CU per unit
-// time on large launches but quantises the grid four times coarser, so the
-// launcher picks the shape with the smaller estimated time in waves.
-#ifndef FAL_GEMM_BIG_GAIN
-#define FAL_GEMM_BIG_GAIN 1.25
-#endif
-constexpr int kSmall = 128, kBig = 256, kCUs = 256;
+// Block shapes.  128x128 (2x2 wavefronts of 64x64) and 128x96 (2x2 of 64x48)
+// run two workgroups per CU; 256x256 (4x2 wavefronts of 64x128) runs one and
+// moves half the global traffic and a quarter less LDS traffic per MFMA.
+// Their throughput per CU differs (rate, relative to 128x128) and so does
+// how finely they quantise a launch into waves; the launcher picks the shape
+// with the smallest estimated time.  The 128x96 shape fills the chip exactly
+// for 768-wide outputs (8192 x 768 = 512 tiles).
+constexpr int kCUs = 256;
+struct TileShape { int bm, bn, per_cu; double rate; };
+enum { TILE_SQ = 0, TILE_NARROW = 1, TILE_BIG = 2, kTileShapes = 3 };
+constexpr TileShape kTile[kTileShapes] = {{128, 128, 2, 1.0}, {128, 96, 2, 0.92}, {256, 256, 1, 1.25}};
 
-static bool use_big_tiles(const GemmGroup& g) {
-  if (FAL_GEMM_BIG_GAIN <= 0.0) return false;
-  int64_t tb = 0, ts = 0;
-  for (int i = 0; i < g.n; ++i) {
-    tb += (int64_t)((g.p[i].M + kBig - 1) / kBig) * ((g.p[i].N + kBig - 1) / kBig);
-    ts += (int64_t)((g.p[i].M + kSmall - 1) / kSmall) * ((g.p[i].N + kSmall - 1) / kSmall);
-  }
-  // time in units of one 128x128 tile on a full CU
-  const double t_small = (double)((ts + 2 * kCUs - 1) / (2 * kCUs)) * 2.0;
-  const double t_big = (double)((tb + kCUs - 1) / kCUs) * 4.0 / FAL_GEMM_BIG_GAIN;
-  return t_big < t_small;
+static int64_t count_tiles(const GemmGroup& g, int bm, int bn) {
+  int64_t t = 0;
+  for (int i = 0; i < g.n; ++i) t += (int64_t)((g.p[i].M + bm - 1) / bm) * ((g.p[i].N + bn - 1) / bn);
+  return t;
 }
 
-constexpr int kSlots = 2 * kCUs;    // resident 128x128 workgroups (two per CU)
+static int choose_tile(const GemmGroup& g) {
+  int best = TILE_SQ;
+  double tbest = 0.0;
+  for (int c = 0; c < kTileShapes; ++c) {
+    const TileShape& t = kTile[c];
+    const int64_t slots = (int64_t)t.per_cu * kCUs;
+    const int64_t rounds = (count_tiles(g, t.bm, t.bn) + slots - 1) / slots;
+    // time in units of one 128x128 tile on a whole CU
+    const double time = (double)rounds * t.per_cu * (t.bm * t.bn) / (128.0 * 128.0) / t.rate;
+    if (c == 0 || time < tbest) { tbest = time; best = c; }
+  }
+  return best;
+}
+
+constexpr int kSlots = 2 * kCUs;    // resident 128x128 workgroups
 constexpr int kMaxSplits = 16;
 
 // Split-K factor for a launch of `tiles` 128x128 tiles over nt k-tiles:
@@ -644,9 +654,13 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
                 const char** why, float* splitk_scratch, int64_t splitk_floats) {
   *why = nullptr;
   if (g.n < 1 || g.n > kMaxGroup) { *why = "bad GEMM group size"; return hipErrorInvalidValue; }
-  const bool big = dt == BF16 && use_big_tiles(g);
-  const int tsz = dt == BF16 ? (big ? kBig : kSmall) : ST;
-  const int tm = tsz, tn = tsz;
+  // Weight gradients (one fp32 plain output, few 128x128 tiles) split K on
+  // 128x128 tiles; everything else picks its tile shape.
+  const GemmProblem& P0 = g.p[0];
+  const bool splittable = dt == BF16 && splitk_scratch && g.n == 1 && P0.K2 == 0 && P0.epi == EPI_STORE &&
+                          P0.out_f32 && count_tiles(g, 128, 128) <= kCUs;
+  const int shape = dt != BF16 ? TILE_SQ : splittable ? TILE_SQ : choose_tile(g);
+  const int tm = dt == BF16 ? kTile[shape].bm : ST, tn = dt == BF16 ? kTile[shape].bn : ST;
   int total = 0;
   for (int i = 0; i < g.n; ++i) {
     GemmProblem& P = g.p[i];
@@ -680,28 +694,30 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
   }
   // Split K for launches that would leave compute units idle (fewer tiles
   // than CUs); fp32 plain outputs only (the weight gradients).
-  if (dt == BF16 && !big && splitk_scratch && g.n == 1 && g.p[0].tiles_m * g.p[0].tiles_n <= kCUs) {
+  if (splittable) {
     GemmProblem& P = g.p[0];
     const int tiles = P.tiles_m * P.tiles_n;
     const int sp = choose_splits(tiles, (P.K + KT - 1) / KT, (int64_t)P.M * P.N, splitk_floats);
-    if (sp > 1 && P.K2 == 0 && P.epi == EPI_STORE && P.out_f32) {
+    if (sp > 1) {
       P.splits = sp;
       P.part = splitk_scratch;
       total = tiles * sp;
     }
   }
   g.total_tiles = total;
-  const dim3 grid(total), block(dt == BF16 && big ? 512 : 256);
+  const dim3 grid(total), block(dt == BF16 && shape == TILE_BIG ? 512 : 256);
   if (dt == BF16) {
 #define FAL_GEMM_LAUNCH(BM, BN, WGM, WGN)                                                                      \
   if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 1, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh); \
   else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<1, 0, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);      \
   else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_mfma<0, 1, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);      \
   else hipLaunchKernelGGL((gemm_bf16_mfma<0, 0, BM, BN, WGM, WGN>), grid, block, 0, s, g, gelu_tanh);
-    if (big) {
-      FAL_GEMM_LAUNCH(kBig, kBig, 4, 2)
+    if (shape == TILE_BIG) {
+      FAL_GEMM_LAUNCH(256, 256, 4, 2)
+    } else if (shape == TILE_NARROW) {
+      FAL_GEMM_LAUNCH(128, 96, 2, 2)
     } else {
-      FAL_GEMM_LAUNCH(kSmall, kSmall, 2, 2)
+      FAL_GEMM_LAUNCH(128, 128, 2, 2)
     }
 #undef FAL_GEMM_LAUNCH
     const GemmProblem& P = g.p[0];
