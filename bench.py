@@ -25,6 +25,8 @@ Also reported, from the same process:
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -35,6 +37,12 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "training tokens/s on 1 MI355X (FAL vs GPT baseline); MFMA util % of bf16 peak"
+# Measured HBM traffic of the GEMM calls of the default workload (rocprofv3
+# FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy); valid only while the
+# sources it was measured on are unchanged.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_mfma_gpt2-small_traffic.md")
+TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h",
+                   "paper_2510_14614_amd/csrc/api.cpp")
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
@@ -52,6 +60,15 @@ def parse():
     ap.add_argument("--cpu-sample-batch", type=int, default=1)
     ap.add_argument("--single-stream", action="store_true",
                     help="run the timed steps with the aux stream equal to the main stream")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "OUT_MD"),
+                    help="offline: write a kernel summary from a rocprofv3 --stats kernel_stats.csv")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "PROBE_MIB", "OUT_MD"),
+                    help="offline: write the GEMM traffic summary from two rocprofv3 --pmc counter_collection.csv "
+                         "of runs made with --copy-probe PROBE_MIB")
+    ap.add_argument("--cmd", action="append", default=[], help="command line(s) recorded in a summary")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the measurements, run one plain device copy of MIB MiB (fp32 x 2.0 into a second "
+                         "buffer): the known-size reference for HBM traffic counters")
     return ap.parse_args()
 
 
@@ -142,8 +159,104 @@ def cpu_baseline(cfg, sample_batch):
             "host_cpus": os.cpu_count()}
 
 
+def sources_hash():
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """Bytes per GEMM call from the committed counter summary, or None when
+    it is missing or was taken on different kernel sources."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    kv = {}
+    for ln in lines:
+        if ln.startswith("- `") and "`: " in ln:
+            k, v = ln[3:].split("`: ", 1)
+            kv[k] = v.strip()
+    if kv.get("gemm_sources_sha256") != sources_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+def summarize_stats(stats_csv, out_md, cmds):
+    rows = list(csv.DictReader(open(stats_csv)))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = ["# Kernel time, gpt2-small FAL training step (serialized launches)", "",
+             "Command (repository root on the GPU host, `TMPDIR=/tmp`):", ""]
+    lines += ["```", *cmds, "```", "",
+              f"All dispatches of the run; total GPU kernel time {tot / 1e6:.2f} ms.", "",
+              "| kernel | calls | avg us | total ms | % |", "|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        ms = float(r["TotalDurationNs"]) / 1e6
+        if ms < 0.05:
+            continue
+        name = r["Name"].replace("|", "/")[:110]
+        lines.append(f"| `{name}` | {int(r['Calls'])} | {float(r['AverageNs']) / 1e3:.1f} | {ms:.2f} | "
+                     f"{float(r['Percentage']):.1f} |")
+    gm = [r for r in rows if "gemm_bf16_mfma" in r["Name"]]
+    red = [r for r in rows if "splitk_reduce" in r["Name"]]
+    n = sum(int(r["Calls"]) for r in gm)
+    tg = sum(float(r["TotalDurationNs"]) for r in gm)
+    tr = sum(float(r["TotalDurationNs"]) for r in red)
+    lines += ["", f"gemm_bf16_mfma (all instantiations): {n} calls, average {tg / n / 1e3:.1f} us per call; "
+              f"with the split-K reduces they launch, {(tg + tr) / n / 1e3:.1f} us per call (the span bench.py "
+              f"times as one GEMM call)."]
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines[-3:]))
+
+
+def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
+    probe_bytes = int(probe_mib) * (1 << 20)
+
+    def load(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        probe = [r for r in rows if "MulFunctor" in r["Kernel_Name"]]
+        assert probe, "no copy-probe dispatch in " + path
+        calib = probe_bytes / (float(probe[-1]["Counter_Value"]) * 1024.0)
+        g = [float(r["Counter_Value"]) * 1024.0 for r in rows if "gemm_bf16_mfma" in r["Kernel_Name"]]
+        red = [float(r["Counter_Value"]) * 1024.0 for r in rows if "splitk_reduce" in r["Kernel_Name"]]
+        return calib, probe_bytes, float(probe[-1]["Counter_Value"]) * 1024.0, g, red, len(rows)
+    cf, pbf, rawf, gf, rf, _ = load(fetch_csv, "FETCH_SIZE")
+    cw, pbw, raww, gw, rw, _ = load(write_csv, "WRITE_SIZE")
+    n = len(gf)
+    assert n == len(gw) and n > 0
+    fetch = (sum(gf) + sum(rf)) * cf / n
+    write = (sum(gw) + sum(rw)) * cw / n
+    lines = ["# HBM traffic of gemm_bf16_mfma, gpt2-small FAL training step", "",
+             "Commands (repository root on the GPU host, `TMPDIR=/tmp`), one counter per run:", "",
+             "```", *cmds, "```", "",
+             "Each run ends with a plain elementwise copy (`--copy-probe`) that reads and writes a known number",
+             "of bytes; its counter reading calibrates the counter for this part:", "",
+             f"- FETCH_SIZE: copy of {pbf / 2**20:.0f} MiB read {rawf / 2**20:.1f} MiB -> factor {cf:.4f}",
+             f"- WRITE_SIZE: copy of {pbw / 2**20:.0f} MiB wrote {raww / 2**20:.1f} MiB -> factor {cw:.4f}", "",
+             f"Over {n} GEMM calls (each call = one gemm_bf16_mfma dispatch plus the split-K reduce it may launch):", "",
+             f"- `fetch_bytes_per_call`: {fetch:.0f}",
+             f"- `write_bytes_per_call`: {write:.0f}",
+             f"- `traffic_bytes_per_call`: {fetch + write:.0f}",
+             f"- `gemm_sources_sha256`: {sources_hash()}", "",
+             "bench.py reports `traffic_bytes_per_call` as roofline.traffic while the kernel sources hash to the",
+             "value above, and null otherwise."]
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats, args.cmd)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args.cmd)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
               f"(the hot path is single-GPU; see the sharding notes in DESIGN.md).", file=sys.stderr)
@@ -210,9 +323,11 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": gemm_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic() if args.config == "gpt2-small" and args.arch == "fal" else None,
+            "traffic_unit": "HBM bytes per GEMM call (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_ms": gemm_avg_ms,
             "avg_launch_gflop": g["flops"] / max(g["launches"], 1) / 1e9,
+            "avg_launch_alg_bytes": g["bytes"] / max(g["launches"], 1),
         },
         "kernels": kernels,
         "wall_s_timed": wall,
@@ -237,7 +352,23 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)
 
+    if args.copy_probe > 0:
+        out["copy_probe_bytes"] = copy_probe(args.copy_probe)
+
     print(json.dumps(out), flush=True)
+
+
+def copy_probe(mib):
+    """One elementwise kernel that reads and writes mib MiB each (a plain
+    copy with a scale, so it is a shader dispatch the counters see)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda", dtype=torch.float32)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 2.0, out=dst)
+    torch.cuda.synchronize()
+    return n * 4
 
 
 if __name__ == "__main__":

@@ -618,15 +618,18 @@ static int choose_tile(const GemmGroup& g) {
 
 constexpr int kSlots = 2 * kCUs;    // resident 128x128 workgroups
 constexpr int kMaxSplits = 16;
+// Partials' write and re-read per split, in k-tile rounds per 128 tiles
+// (measured: 3 slices beat 7 for the 768 x 3072 x 8192 weight gradient).
+constexpr double kSplitBeta = 3.0;
 
 // Split-K factor for a launch of `tiles` 128x128 tiles over nt k-tiles:
 // minimises (rounds of all workgroup slots) x (k-tiles per slice) plus the
-// partials' extra write and read, about one k-tile round per split for
-// every 128 tiles.  1 = no split.
+// partials' extra write and read (kSplitBeta k-tile rounds per split for
+// every 128 tiles).  1 = no split.
 static int choose_splits(int tiles, int nt, int64_t MN, int64_t scratch_floats) {
   auto cost = [&](int sp) {
     const double rounds = (double)((tiles * sp + kSlots - 1) / kSlots);
-    return rounds * ((nt + sp - 1) / sp) + (sp > 1 ? sp * tiles / 128.0 : 0.0);
+    return rounds * ((nt + sp - 1) / sp) + (sp > 1 ? kSplitBeta * sp * tiles / 128.0 : 0.0);
   };
   int best = 1;
   double cbest = cost(1);
