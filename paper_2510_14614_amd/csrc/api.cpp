@@ -141,7 +141,7 @@ struct Carve {
 
 struct LayerSlot {
   float *mean1, *rstd1, *mean2, *rstd2;
-  void *h1, *h2, *qkv, *og, *pre;
+  void *h1, *h2, *qkv, *og, *dgelu;  // dgelu: GELU' at the FFN pre-activation
   float *lse, *xm;
 };
 
@@ -180,7 +180,7 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
     s.h2 = cv.take<char>(M * d * es);
     s.qkv = cv.take<char>(M * 3 * D.dA * es);
     s.og = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
-    s.pre = cv.take<char>(M * D.f * es);
+    s.dgelu = cv.take<char>(M * D.f * es);
     s.lse = cv.take<float>((int64_t)D.B * D.H * D.T);
     if (need_xm || i == 0) {
       s.xm = cv.take<float>(M * d);
@@ -369,7 +369,7 @@ struct Run {
     GemmProblem p = prob(S.h2, D.d, P(bp, FAL_B_W_FC), D.f, D.M, D.f, D.d);
     p.epi = EPI_GELU; p.bias = P(bp, FAL_B_B_FC);
     p.out = off(S.og, D.dA); p.ldo = D.dA + D.f;
-    p.out2 = S.pre; p.ldo2 = D.f;
+    p.out2 = S.dgelu; p.ldo2 = D.f;
     return p;
   }
   // out-projection: A = O (first dA columns of og)
@@ -537,7 +537,7 @@ struct Run {
     Work& W = ctx->W;
     void* dP = off(W.dog, D.dA);
     GemmProblem pg = dgrad(dy_lp, D.d, P(bp, FAL_B_W_2), D.f, D.d, D.M);
-    pg.epi = EPI_GELU_BWD; pg.aux = S.pre; pg.ldaux = D.f; pg.out = dP; pg.ldo = D.dA + D.f;
+    pg.epi = EPI_MUL_AUX; pg.aux = S.dgelu; pg.ldaux = D.f; pg.out = dP; pg.ldo = D.dA + D.f;
     gemm1(1, 1, pg, s);
     gemm1(0, 0, wgrad(off(S.og, D.dA), D.dA + D.f, dy_lp, D.d, D.f, D.d, D.M, G(gb, FAL_B_W_2)), s);
     colsum(dy, 1, D.d, D.d, G(gb, FAL_B_B_2), part, s);

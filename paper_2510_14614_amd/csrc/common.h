@@ -54,23 +54,21 @@ __device__ __forceinline__ float gelu_sig_arg(float x) {
   return c2 * (x + 0.044715f * x * x * x);
 }
 
-__device__ __forceinline__ float gelu_f(float x, int tanh_form) {
-  if (tanh_form) {
-    const float s = __builtin_amdgcn_rcpf(1.f + exp2f(gelu_sig_arg(x)));
-    return x * s;
-  }
-  return 0.5f * x * (1.f + erff(x * 0.7071067811865476f));
-}
-
-__device__ __forceinline__ float gelu_grad_f(float x, int tanh_form) {
+// GELU and its derivative at x, sharing the exponential: tanh form
+// x * s with s = sigmoid(2u), u = sqrt(2/pi) (x + 0.044715 x^3), so
+// GELU' = s + 2 x s (1 - s) du/dx; erf form x Phi(x), GELU' = Phi + x phi.
+__device__ __forceinline__ void gelu_and_grad(float x, int tanh_form, float& g, float& dg) {
   if (tanh_form) {
     const float s = __builtin_amdgcn_rcpf(1.f + exp2f(gelu_sig_arg(x)));
     const float du = 0.7978845608028654f * (1.f + 3.f * 0.044715f * x * x);
-    return s + 2.f * x * s * (1.f - s) * du;
+    g = x * s;
+    dg = s + 2.f * x * s * (1.f - s) * du;
+    return;
   }
   const float cdf = 0.5f * (1.f + erff(x * 0.7071067811865476f));
   const float pdf = 0.3989422804014327f * expf(-0.5f * x * x);
-  return cdf + x * pdf;
+  g = x * cdf;
+  dg = cdf + x * pdf;
 }
 
 static inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }

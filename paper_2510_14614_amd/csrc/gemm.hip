@@ -34,18 +34,21 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int m, int n, flo
       else
         static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(v);
       break;
-    case EPI_GELU:
-      static_cast<S*>(P.out2)[(int64_t)m * P.ldo2 + n] = from_f<S>(v);
-      static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(gelu_f(v, gelu_tanh));
+    case EPI_GELU: {
+      float gv, dg;
+      gelu_and_grad(v, gelu_tanh, gv, dg);
+      static_cast<S*>(P.out2)[(int64_t)m * P.ldo2 + n] = from_f<S>(dg);
+      static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(gv);
       break;
+    }
     case EPI_RESID: {
       float* o = static_cast<float*>(P.out) + (int64_t)m * P.ldo + n;
       *o = P.resid[(int64_t)m * P.ldr + n] + v;
       break;
     }
-    case EPI_GELU_BWD: {
-      const float pre = to_f(static_cast<const S*>(P.aux)[(int64_t)m * P.ldaux + n]);
-      static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(v * gelu_grad_f(pre, gelu_tanh));
+    case EPI_MUL_AUX: {
+      const float a = to_f(static_cast<const S*>(P.aux)[(int64_t)m * P.ldaux + n]);
+      static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(v * a);
       break;
     }
   }
@@ -307,20 +310,20 @@ __device__ __forceinline__ void apply4(const GemmProblem& P, int m, int n, float
       if (F32OUT) *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) = make_float4(v[0], v[1], v[2], v[3]);
       else st4(static_cast<bf16*>(P.out) + o, v);
     } else if (EPI == EPI_GELU) {
-      st4(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n, v);
-      float g[4];
+      float g[4], dg[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) g[c] = gelu_f(v[c], gelu_tanh);
+      for (int c = 0; c < 4; ++c) gelu_and_grad(v[c], gelu_tanh, g[c], dg[c]);
+      st4(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n, dg);
       st4(static_cast<bf16*>(P.out) + o, g);
     } else if (EPI == EPI_RESID) {
       const float4 r = *reinterpret_cast<const float4*>(P.resid + (int64_t)m * P.ldr + n);
       *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) =
           make_float4(r.x + v[0], r.y + v[1], r.z + v[2], r.w + v[3]);
     } else {
-      float pre[4];
-      ld4(static_cast<const bf16*>(P.aux) + (int64_t)m * P.ldaux + n, pre);
+      float a[4];
+      ld4(static_cast<const bf16*>(P.aux) + (int64_t)m * P.ldaux + n, a);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) v[c] *= gelu_grad_f(pre[c], gelu_tanh);
+      for (int c = 0; c < 4; ++c) v[c] *= a[c];
       st4(static_cast<bf16*>(P.out) + o, v);
     }
   } else {
@@ -332,13 +335,15 @@ __device__ __forceinline__ void apply4(const GemmProblem& P, int m, int n, float
         if (F32OUT) static_cast<float*>(P.out)[oc] = v[c];
         else static_cast<bf16*>(P.out)[oc] = from_f<bf16>(v[c]);
       } else if (EPI == EPI_GELU) {
-        static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + c] = from_f<bf16>(v[c]);
-        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(gelu_f(v[c], gelu_tanh));
+        float g, dg;
+        gelu_and_grad(v[c], gelu_tanh, g, dg);
+        static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + c] = from_f<bf16>(dg);
+        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(g);
       } else if (EPI == EPI_RESID) {
         static_cast<float*>(P.out)[oc] = P.resid[(int64_t)m * P.ldr + n + c] + v[c];
       } else {
-        const float pre = to_f(static_cast<const bf16*>(P.aux)[(int64_t)m * P.ldaux + n + c]);
-        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(v[c] * gelu_grad_f(pre, gelu_tanh));
+        const float a = to_f(static_cast<const bf16*>(P.aux)[(int64_t)m * P.ldaux + n + c]);
+        static_cast<bf16*>(P.out)[oc] = from_f<bf16>(v[c] * a);
       }
     }
   }
@@ -565,7 +570,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
       break;
     case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
     case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_GELU_BWD: store_staged<EPI_GELU_BWD, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
@@ -690,7 +695,7 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       if (P.bias2) ok = ok && al(P.bias2, 8);
       if (P.epi == EPI_RESID) ok = ok && al(P.resid, 16) && P.ldr % 4 == 0;
       if (P.epi == EPI_GELU) ok = ok && P.out2 && al(P.out2, 8) && P.ldo2 % 4 == 0;
-      if (P.epi == EPI_GELU_BWD) ok = ok && P.aux && al(P.aux, 8) && P.ldaux % 4 == 0;
+      if (P.epi == EPI_MUL_AUX) ok = ok && P.aux && al(P.aux, 8) && P.ldaux % 4 == 0;
       P.vec_out = ok ? 1 : 0;
     }
     total += P.tiles_m * P.tiles_n;

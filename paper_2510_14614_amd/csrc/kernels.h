@@ -19,9 +19,9 @@ enum DType : int { F32 = 0, BF16 = 1 };
 // A and B hold the storage dtype of the launch; accumulation is fp32.
 enum Epi : int {
   EPI_STORE = 0,     // out = acc + bias (+ bias2)          (out: f32 or dtype)
-  EPI_GELU = 1,      // out2 = acc + bias (pre-activation), out = GELU(out2)  (dtype)
+  EPI_GELU = 1,      // v = acc + bias: out = GELU(v), out2 = GELU'(v)   (dtype)
   EPI_RESID = 2,     // out(f32) = resid(f32) + acc + bias   (resid may equal out)
-  EPI_GELU_BWD = 3,  // out = acc * GELU'(aux)                (aux, out: dtype)
+  EPI_MUL_AUX = 3,   // out = acc * aux (aux = GELU' saved by EPI_GELU)  (aux, out: dtype)
 };
 
 struct GemmProblem {
@@ -39,9 +39,9 @@ struct GemmProblem {
   int64_t ldr;
   void* out;
   int64_t ldo;
-  void* out2;         // EPI_GELU pre-activation output
+  void* out2;         // EPI_GELU: GELU derivative at the pre-activation
   int64_t ldo2;
-  const void* aux;    // EPI_GELU_BWD pre-activation input
+  const void* aux;    // EPI_MUL_AUX: elementwise factor
   int64_t ldaux;
   // filled in by the launcher
   int tiles_m, tiles_n, tile_start;
