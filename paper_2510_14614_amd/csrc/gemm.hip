@@ -152,14 +152,16 @@ constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family buffer descriptor word 3
 
 // An operand whose contraction dimension is strided (MN-major: the weight of
 // a forward layer, both operands of a weight gradient) is staged as loaded,
-// [k][row] with rows padded by kTrPad elements, and read back with the gfx950
-// LDS transpose load.  ds_read_b64_tr_b16 gives lane i of each 16-lane
-// group element i % 4 of the 8-byte chunks addressed by lanes 4j + i / 4
-// (j = 0..3); lane L therefore addresses k-row kb + L / 4, rows 4 (L % 4)..+3
-// of the fragment, and two reads (kb, kb + 4) return the eight consecutive k
-// a 16x16x32 operand lane holds.  The pad of 16 keeps those reads at the
-// minimum number of LDS passes.
-constexpr int kTrPad = 16;
+// [k][row], and read back with the gfx950 LDS transpose load.
+// ds_read_b64_tr_b16 gives lane i of each 16-lane group element i % 4 of the
+// 8-byte chunks addressed by lanes 4j + i / 4 (j = 0..3); lane L therefore
+// addresses k-row kb + L / 4, rows 4 (L % 4)..+3 of the fragment, and two
+// reads (kb, kb + 4) return the eight consecutive k a 16x16x32 operand lane
+// holds.  One such read spans the k-rows {kb + 8G + j} (G, j = 0..3).  Rows
+// are padded by 16 elements (the k-rows then start 32 bytes apart modulo
+// 256) and stored in the order sigma(k) = k ^ (((k >> 3) & 1) << 2): the 16
+// k-rows of a read then hit every 32-byte bank group exactly twice, the
+// minimum for 512 bytes, while each fragment's offset stays an immediate.
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
@@ -171,8 +173,10 @@ __device__ __forceinline__ i16x4_t lds_read_tr(const bf16* p) {
 template <int R, int KMAJ, int NTH>
 struct BStage {
   static constexpr int CPR = R / 8;                         // 16-byte chunks per MN-major k-row
-  static constexpr int RP = R + kTrPad;                     // MN-major LDS row pitch
-  static constexpr int ELEMS = KMAJ ? R * KT : KT * RP;     // one LDS stage
+  static constexpr int TP = R + 16;                         // MN-major LDS row pitch (elements)
+  static constexpr int ELEMS = KMAJ ? R * KT : KT * TP;     // one LDS stage
+  __device__ __forceinline__ static int mn_row(int k) { return k ^ (((k >> 3) & 1) << 2); }
+  __device__ __forceinline__ static int mn_off(int k, int r) { return mn_row(k) * TP + r; }
   static constexpr int NC = R * KT / 8 / NTH;               // 16-byte chunks per thread
   static_assert(NC > 0 && NC <= 32, "tile / thread count mismatch");
   uint4 v[NC];
@@ -268,7 +272,7 @@ struct BStage {
     for (int i = 0; i < NC; ++i) {
       int row, k;
       chunk(i, tid, row, k);
-      const int off = KMAJ ? lds_off(row, k) : k * RP + row;
+      const int off = KMAJ ? lds_off(row, k) : mn_off(k, row);
       *reinterpret_cast<uint4*>(s + off) = check ? masked(i, tail) : v[i];
     }
   }
@@ -280,8 +284,8 @@ struct BStage {
       return *reinterpret_cast<const bf16x8_t*>(s + lds_off(row0 + (lane & 15), ks * 32 + (lane >> 4) * 8));
     const int L = lane & 15;
     const int k = ks * 32 + (lane >> 4) * 8 + (L >> 2);
-    const bf16* p = s + k * RP + row0 + 4 * (L & 3);
-    const i16x4_t lo = lds_read_tr(p), hi = lds_read_tr(p + 4 * RP);
+    const bf16* p = s + row0 + 4 * (L & 3);
+    const i16x4_t lo = lds_read_tr(p + mn_row(k) * TP), hi = lds_read_tr(p + mn_row(k + 4) * TP);
     const i16x4_t v8[2] = {lo, hi};
     return *reinterpret_cast<const bf16x8_t*>(v8);
   }
