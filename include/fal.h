@@ -94,6 +94,13 @@ typedef struct {
   int32_t gelu_tanh;      /* 1: tanh-approximate GELU, 0: erf GELU            */
   int32_t has_embed_head; /* 1: embedding + final LN + tied head + CE loss;
                              0: block stack only (fal_stack_step)             */
+  int32_t fal_block1_mode; /* FAL only (0 for GPT and FAL+).  0: block 1 applies
+                             Eq. 2 like every later block, MLP_1(LN2(X_1) + F);
+                             1: block 1 is the standard Pre-LN block (Eq. 1) and
+                             only produces F = LN_F(A_1) for blocks >= 2 (the
+                             "preparation stage" reading of Sec. 4.1).  Any
+                             other value, or 1 with another arch, is
+                             FAL_ERR_INVALID_ARG.                             */
 } fal_config_t;
 
 /* Parameter tensors.  Global tensors (present only when has_embed_head):

@@ -28,6 +28,10 @@ Readings taken where the paper is silent (each listed in the design notes):
   - FAL uses one first-attention LayerNorm (its parameters live in block 0's
     lnF slot); FAL+ uses one per later block (block i's lnF slot) over one
     shared normalisation of A_1;
+  - FAL block 1 applies Eq. 2 like every other block (fal_block1_mode 0);
+    fal_block1_mode 1 keeps block 1 the standard block, which then only
+    produces F = LN_F(A_1) for the later blocks (the "preparation stage"
+    reading of Sec. 4.1);
   - FAL+ block 1 is the standard GPT block (the printed first case has a
     misplaced parenthesis);
   - GPT-2 conventions: tanh GELU, eps 1e-5, biases on every linear layer,
@@ -204,6 +208,10 @@ def mlp_backward(dm, p, cache, cfg):
 # Blocks
 # ---------------------------------------------------------------------------
 
+def _block1_standard(cfg):
+    return getattr(cfg, "fal_block1_mode", 0) == 1
+
+
 def block_forward(cfg, i, x, p, first):
     """One decoder block.  ``first`` is the state carried from block 0 to the
     later blocks: FAL stores F = LN_F(A_1) under "F"; FAL+ stores the shared
@@ -212,7 +220,13 @@ def block_forward(cfg, i, x, p, first):
     h1, ln1 = layer_norm(x, p["ln1_g"], p["ln1_b"], eps)
     a, mha = mha_forward(h1, p, cfg)
     c = {"ln1": ln1, "mha": mha}
-    if cfg.arch == ARCH_GPT or (cfg.arch == ARCH_FALPLUS and i == 0):
+    if cfg.arch == ARCH_FAL and i == 0 and _block1_standard(cfg):
+        # FAL with a standard first block: Eq. 1 in block 1, which also
+        # produces F = LN_F(A_1) for every later block.
+        first["F"], first["lnF"] = layer_norm(a, p["lnF_g"], p["lnF_b"], eps)
+        xm = x + a
+        u, c["ln2"] = layer_norm(xm, p["ln2_g"], p["ln2_b"], eps)
+    elif cfg.arch == ARCH_GPT or (cfg.arch == ARCH_FALPLUS and i == 0):
         # Eq. 1: the MLP reads LN(X_i + A_i).
         xm = x + a
         u, c["ln2"] = layer_norm(xm, p["ln2_g"], p["ln2_b"], eps)
@@ -245,7 +259,15 @@ def block_backward(cfg, i, dy, p, c, first, dfirst):
     grads = {k: np.zeros_like(v) for k, v in p.items()}
     du, g_mlp = mlp_backward(dy, p, c["mlp"], cfg)
     grads.update(g_mlp)
-    if cfg.arch == ARCH_GPT or (cfg.arch == ARCH_FALPLUS and i == 0):
+    if cfg.arch == ARCH_FAL and i == 0 and _block1_standard(cfg):
+        dxm_ln, grads["ln2_g"], grads["ln2_b"] = layer_norm_backward(du, c["ln2"], p["ln2_g"])
+        dxm = dy + dxm_ln
+        da = dxm
+        if "F" in dfirst:  # the later blocks' use of F
+            dA1, grads["lnF_g"], grads["lnF_b"] = layer_norm_backward(dfirst["F"], first["lnF"], p["lnF_g"])
+            da = da + dA1
+        dx = dxm
+    elif cfg.arch == ARCH_GPT or (cfg.arch == ARCH_FALPLUS and i == 0):
         dxm_ln, grads["ln2_g"], grads["ln2_b"] = layer_norm_backward(du, c["ln2"], p["ln2_g"])
         dxm = dy + dxm_ln
         da = dxm

@@ -32,6 +32,7 @@ class Config:
     ln_eps: float = 1e-5
     gelu_tanh: int = 1        # 1: tanh approximation, 0: erf form
     has_embed_head: int = 1   # 0: block stack only (no embedding, no LM head)
+    fal_block1_mode: int = 0  # FAL only: 0 Eq. 2 in block 1 too, 1 standard block 1 emitting F
 
     @property
     def d_attn(self) -> int:

@@ -71,6 +71,8 @@ const char* validate(const fal_config_t* c) {
   if (!(c->ln_eps > 0.f)) return "ln_eps must be > 0";
   if (c->gelu_tanh != 0 && c->gelu_tanh != 1) return "gelu_tanh must be 0 or 1";
   if (c->has_embed_head != 0 && c->has_embed_head != 1) return "has_embed_head must be 0 or 1";
+  if (c->fal_block1_mode != 0 && c->fal_block1_mode != 1) return "fal_block1_mode must be 0 or 1";
+  if (c->fal_block1_mode == 1 && c->arch != FAL_ARCH_FAL) return "fal_block1_mode 1 applies to FAL only";
   if (c->has_embed_head) {
     if (c->vocab < 1) return "vocab must be >= 1";
     if (c->vocab > 65535) return "vocab above 65535 is not supported";
@@ -422,6 +424,7 @@ struct Run {
            ctx->sa != ctx->sm;
   }
   bool merged() const { return ctx->cfg.sched == FAL_SCHED_MERGED; }
+  bool block1_standard() const { return ctx->cfg.fal_block1_mode == 1; }
   bool merged_out() const {
     return ctx->cfg.sched == FAL_SCHED_MERGED || ctx->cfg.sched == FAL_SCHED_STREAMS_MERGED;
   }
@@ -469,7 +472,8 @@ struct Run {
       gemm1(1, 0, pd, sm);
       return;
     }
-    // Sequential blocks: GPT, FAL+, and FAL block 0.
+    // Sequential blocks: GPT, FAL+, and FAL block 0 (which, with
+    // fal_block1_mode 1, is the standard block that only emits F).
     {
       LnFwdArgs a = lnargs(x, S.mean1, S.rstd1);
       a.g1 = P(bp, FAL_B_LN1_G); a.b1 = P(bp, FAL_B_LN1_B); a.y1 = S.h1;
@@ -494,8 +498,8 @@ struct Run {
       po.epi = EPI_RESID; po.resid = x; po.ldr = D.d; po.out = S.xm; po.ldo = D.d;
       gemm1(1, 0, po, sm);
     }
-    if (arch == FAL_ARCH_FAL) {
-      // block 0 of FAL: H2 = LN2(X_1) + F
+    if (arch == FAL_ARCH_FAL && !block1_standard()) {
+      // block 0 of FAL (Eq. 2 at i = 1): H2 = LN2(X_1) + F
       LnFwdArgs a = lnargs(x, S.mean2, S.rstd2);
       a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2; a.add2 = first;
       ln(a, sm);
@@ -590,7 +594,8 @@ struct Run {
     const int64_t Md = (int64_t)D.M * D.d;
     const bool last = layer == D.L - 1;
     // first-attention LayerNorm slot: zero unless used by this block
-    const bool uses_lnF = (arch == FAL_ARCH_FAL && layer == 0) || (arch == FAL_ARCH_FALPLUS && layer > 0);
+    const bool uses_lnF = (arch == FAL_ARCH_FAL && layer == 0 && (!block1_standard() || D.L > 1)) ||
+                          (arch == FAL_ARCH_FALPLUS && layer > 0);
     if (!uses_lnF) {
       FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_G), D.d, sm));
       FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_B), D.d, sm));
@@ -611,7 +616,7 @@ struct Run {
       lnbwd(a, sm);
       return;
     }
-    if (arch == FAL_ARCH_FAL) {  // block 0
+    if (arch == FAL_ARCH_FAL && !block1_standard()) {  // block 0, Eq. 2
       mlp_bwd(S, bp, dy_lp, dy, gb, sm, W.part_main);
       if (last) FAL_TRY(hipMemcpyAsync(dfirst, W.dh2, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
       else FAL_TRY(add_f32(dfirst, W.dh2, dfirst, Md, sm));
@@ -652,6 +657,16 @@ struct Run {
       FAL_TRY(hipMemcpyAsync(W.da, W.dxm, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
       FAL_TRY(norm_bwd(W.a1, W.meanF, W.rstdF, dfirst, D.M, D.d, W.da, 1, sm));
       FAL_TRY(cast_from_f32(dt, W.da, W.da_lp, Md, sm));
+      da_lp = W.da_lp;
+      da = W.da;
+    }
+    if (arch == FAL_ARCH_FAL && layer == 0 && D.L > 1) {
+      // standard block 1 of FAL: dA_1 = dXm + LN_F backward of the dF the
+      // later blocks accumulated (which also gives the LN_F gradients)
+      LnBwdArgs f = lnb(W.a1, W.meanF, W.rstdF);
+      f.dy1 = dfirst; f.g1 = P(bp, FAL_B_LNF1_G); f.dres = W.dxm; f.dx = W.da; f.dx_lp = W.da_lp;
+      f.dg1 = G(gb, FAL_B_LNF1_G); f.db1 = G(gb, FAL_B_LNF1_B);
+      lnbwd(f, sm);
       da_lp = W.da_lp;
       da = W.da;
     }

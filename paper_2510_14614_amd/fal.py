@@ -38,7 +38,7 @@ class fal_config_t(ctypes.Structure):
         ("n_layer", c_int32), ("d_model", c_int32), ("n_head", c_int32), ("head_dim", c_int32),
         ("d_ff", c_int32), ("vocab", c_int32), ("seq_len", c_int32), ("batch", c_int32),
         ("arch", c_int32), ("dtype", c_int32), ("sched", c_int32), ("ln_eps", c_float),
-        ("gelu_tanh", c_int32), ("has_embed_head", c_int32),
+        ("gelu_tanh", c_int32), ("has_embed_head", c_int32), ("fal_block1_mode", c_int32),
     ]
 
 
@@ -87,7 +87,7 @@ def lib():
 def to_c(cfg: Config) -> fal_config_t:
     return fal_config_t(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.head_dim, cfg.d_ff, cfg.vocab,
                         cfg.seq_len, cfg.batch, cfg.arch, cfg.dtype, cfg.sched, cfg.ln_eps,
-                        cfg.gelu_tanh, cfg.has_embed_head)
+                        cfg.gelu_tanh, cfg.has_embed_head, cfg.fal_block1_mode)
 
 
 def _check(status, ctx=None):

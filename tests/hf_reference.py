@@ -26,6 +26,8 @@ class _RoutedLN2(torch.nn.Module):
         if self.arch == ARCH_FAL:
             if self.i == 0:
                 st["F"] = self.lnF(st["A1"])              # LN of the first attention, once
+                if st["block1_standard"]:
+                    return self.ln2(h)                    # standard block 1 (only emits F)
             return self.ln2(st["x_in"][self.i]) + st["F"]  # LN(X_i) + LN(MHA_1(LN(X_1)))
         if self.arch == ARCH_FALPLUS and self.i > 0:
             return self.ln2(h) + self.lnF(st["A1"])       # LN(X_i + A_i) + LN_i(MHA_1(...))
@@ -48,7 +50,7 @@ def build(cfg, gparams, blocks):
         tr.wpe.weight.copy_(t(gparams["wpe"]))
         tr.ln_f.weight.copy_(t(gparams["lnf_g"]))
         tr.ln_f.bias.copy_(t(gparams["lnf_b"]))
-    state = {"x_in": {}}
+    state = {"x_in": {}, "block1_standard": getattr(cfg, "fal_block1_mode", 0) == 1}
     lnFs = []
     for i, (blk, p) in enumerate(zip(tr.h, blocks)):
         with torch.no_grad():

@@ -43,12 +43,20 @@ def test_named_configs_valid(name):
     (dict(dtype=3), fal.FAL_ERR_INVALID_ARG),
     (dict(sched=-1), fal.FAL_ERR_INVALID_ARG),
     (dict(ln_eps=0.0), fal.FAL_ERR_INVALID_ARG),
+    (dict(fal_block1_mode=2), fal.FAL_ERR_INVALID_ARG),
+    (dict(arch=0, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
+    (dict(arch=2, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
     (dict(head_dim=24), fal.FAL_ERR_UNSUPPORTED),
     (dict(vocab=70000), fal.FAL_ERR_UNSUPPORTED),
     (dict(d_model=8192), fal.FAL_ERR_UNSUPPORTED),
 ])
 def test_invalid_configs_rejected(bad, status):
     assert fal.validate_config(get_config("tiny", **bad)) == status
+
+
+def test_fal_block1_mode_accepted_for_fal():
+    cfg = get_config("tiny", arch=1, fal_block1_mode=1)
+    assert fal.validate_config(cfg) == fal.FAL_OK
 
 
 def test_param_layout_offsets():

@@ -44,6 +44,29 @@ def test_tiny_fal_schedules(sched, dtype):
                  label=f"tiny sched{sched} dt{dtype}")
 
 
+@pytest.mark.parametrize("sched", [SCHED_SEQ, SCHED_STREAMS_MERGED])
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_tiny_fal_standard_first_block(sched, dtype):
+    # fal_block1_mode 1: block 1 is the standard block and only emits F
+    cfg = get_config("tiny", arch=ARCH_FAL, dtype=dtype, sched=sched, n_layer=3, fal_block1_mode=1)
+    log(f"tiny FAL standard block 1 sched={sched} dtype={dtype}")
+    g, blocks = synth.make_params(cfg, seed=12)
+    tok = synth.make_tokens(cfg, seed=13)
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"tiny block1-std sched{sched} dt{dtype}")
+
+
+@pytest.mark.parametrize("n_layer", [1, 2])
+def test_ragged_fal_standard_first_block(n_layer):
+    # one block: F is produced but unused (zero LN_F gradients)
+    cfg = _ragged(ARCH_FAL, 1, n_layer=n_layer, fal_block1_mode=1, sched=SCHED_STREAMS_MERGED)
+    log(f"ragged FAL standard block 1 L={n_layer}")
+    g, blocks = synth.make_params(cfg, seed=14)
+    tok = synth.make_tokens(cfg, seed=15, dist="zipf")
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"ragged block1-std L{n_layer}")
+
+
 def _ragged(arch, dtype, **kw):
     # spans several GEMM tiles with ragged tails in every dimension
     base = dict(n_layer=2, d_model=192, n_head=3, head_dim=64, d_ff=328, vocab=1000, seq_len=100,

@@ -236,3 +236,73 @@ def test_finite_differences_sampled_tiny(arch):
     for i, b in enumerate(blocks):
         _fd_check(loss_fn, b, r["grads_blocks"][i], h=1e-5, rtol=1e-5, atol=1e-10,
                   max_per_tensor=4, rng=rng)
+
+
+# --- FAL with a standard first block (fal_block1_mode = 1) ------------------
+
+def test_fal_block1_standard_matches_hf():
+    cfg = _tiny(ARCH_FAL, n_layer=3, fal_block1_mode=1)
+    g, blocks = synth.make_params(cfg, seed=31, bf16=False)
+    tok = synth.make_tokens(cfg, seed=32)
+    r = oracle.train_step(cfg, g, blocks, tok)
+    loss, logits, gg, gb = hf_reference.run(cfg, g, blocks, tok)
+    assert abs(r["loss"] - loss) < 1e-12
+    assert _rel(r["logits"], logits) < 1e-11
+    for k in gg:
+        assert _rel(r["grads_global"][k], gg[k]) < 1e-9, k
+    for i in range(cfg.n_layer):
+        for k in gb[i]:
+            if np.abs(gb[i][k]).max() == 0.0:
+                assert np.abs(r["grads_blocks"][i][k]).max() == 0.0, (i, k)
+            else:
+                assert _rel(r["grads_blocks"][i][k], gb[i][k]) < 1e-9, (i, k)
+
+
+def test_fal_block1_standard_single_block_is_gpt_bitwise():
+    # with one block, the standard first block is exactly the GPT block; F is
+    # produced but nothing reads it, so its LayerNorm gets zero gradients
+    cfg = _tiny(ARCH_FAL, n_layer=1, fal_block1_mode=1)
+    g, blocks = synth.make_params(cfg, seed=33, bf16=False)
+    tok = synth.make_tokens(cfg, seed=34)
+    r = oracle.train_step(cfg, g, blocks, tok)
+    ref = oracle.train_step(cfg.replace(arch=ARCH_GPT, fal_block1_mode=0), g, blocks, tok)
+    assert r["loss"] == ref["loss"]
+    assert np.array_equal(r["logits"], ref["logits"])
+    for k in ref["grads_global"]:
+        assert np.array_equal(r["grads_global"][k], ref["grads_global"][k]), k
+    for k, v in ref["grads_blocks"][0].items():
+        if k in ("lnF_g", "lnF_b"):
+            assert not np.any(r["grads_blocks"][0][k])
+        else:
+            assert np.array_equal(r["grads_blocks"][0][k], v), k
+
+
+def test_fal_block1_modes_differ_only_from_block1_mlp_input():
+    # both modes feed blocks >= 2 the same F; they differ in block 1's MLP input
+    cfg0 = _tiny(ARCH_FAL, n_layer=2)
+    cfg1 = cfg0.replace(fal_block1_mode=1)
+    g, blocks = synth.make_params(cfg0, seed=35, bf16=False)
+    g = {k: v.astype(np.float64) for k, v in g.items()}
+    blocks = [{k: v.astype(np.float64) for k, v in b.items()} for b in blocks]
+    tok = synth.make_tokens(cfg0, seed=36)
+    assert oracle.train_step(cfg0, g, blocks, tok)["loss"] != oracle.train_step(cfg1, g, blocks, tok)["loss"]
+    # block 1 of mode 1 with W_fc = 0 and b_fc = 0 makes its MLP a constant
+    # b_2 in both modes, so the two models then agree bitwise
+    z = [dict(b) for b in blocks]
+    z[0]["w_fc"] = np.zeros_like(z[0]["w_fc"])
+    z[0]["b_fc"] = np.zeros_like(z[0]["b_fc"])
+    a0 = oracle.train_step(cfg0, g, z, tok)
+    a1 = oracle.train_step(cfg1, g, z, tok)
+    assert a0["loss"] == a1["loss"]
+    assert np.array_equal(a0["logits"], a1["logits"])
+
+
+def test_finite_differences_fal_block1_standard():
+    cfg = _micro(ARCH_FAL, fal_block1_mode=1)
+    g, blocks = _scaled_micro_params(cfg, seed=37)
+    tok = synth.make_tokens(cfg, seed=38, dist="uniform")
+    r = oracle.train_step(cfg, g, blocks, tok)
+    loss_fn = lambda: oracle.train_step(cfg, g, blocks, tok)["loss"]
+    _fd_check(loss_fn, g, r["grads_global"])
+    for i, b in enumerate(blocks):
+        _fd_check(loss_fn, b, r["grads_blocks"][i])
