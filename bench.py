@@ -41,8 +41,7 @@ METRIC = "training tokens/s on 1 MI355X (FAL vs GPT baseline); MFMA util % of bf
 # FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy); valid only while the
 # sources it was measured on are unchanged.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_mfma_gpt2-small_traffic.md")
-TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h",
-                   "paper_2510_14614_amd/csrc/api.cpp")
+TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h")
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
@@ -133,6 +132,39 @@ class Runner:
 
     def close(self):
         self.F.close()
+
+
+def measured_peaks():
+    """Sustained dense bf16 MFMA rate (register-only MFMA chains on every
+    SIMD, libfal_probe.so) and HBM copy rate (1 GiB read + 1 GiB written by
+    one elementwise kernel), both timed with HIP events."""
+    import ctypes
+
+    import torch
+    path = os.path.join(ROOT, "paper_2510_14614_amd", "libfal_probe.so")
+    L = ctypes.CDLL(path)
+    L.fal_probe_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    blocks, iters = 8 * 256, 4096
+    out = torch.empty(blocks * 256, device="cuda", dtype=torch.float32)
+    s = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for rep in range(2):  # first launch warms up
+        e0.record(s)
+        assert L.fal_probe_mfma_bf16(blocks, iters, ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s.cuda_stream)) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    flops = blocks * 4.0 * iters * L.fal_probe_mfma_chains() * 2 * 16 * 16 * 32
+    n = (1 << 30) // 4
+    src = torch.ones(n, device="cuda", dtype=torch.float32)
+    dst = torch.empty_like(src)
+    for rep in range(3):
+        e0.record(s)
+        torch.mul(src, 2.0, out=dst)
+        e1.record(s)
+        torch.cuda.synchronize()
+    cms = e0.elapsed_time(e1)
+    return {"mfma_bf16_tflops": flops / (ms / 1e3) / 1e12, "hbm_copy_gbs": 2.0 * n * 4 / (cms / 1e3) / 1e9}
 
 
 def cpu_baseline(cfg, sample_batch):
@@ -283,6 +315,7 @@ def main():
     rp.close()
     tokens_per_s = cfg.tokens / (ms / 1000.0)
     flops_step = cfg.train_flops_per_token() * cfg.tokens
+    peaks = measured_peaks()
 
     g = prof["gemm"]
     gemm_avg_ms = g["ms"] / max(g["launches"], 1)
@@ -328,7 +361,10 @@ def main():
             "avg_launch_ms": gemm_avg_ms,
             "avg_launch_gflop": g["flops"] / max(g["launches"], 1) / 1e9,
             "avg_launch_alg_bytes": g["bytes"] / max(g["launches"], 1),
+            "measured_peak": peaks["mfma_bf16_tflops"],
+            "frac_of_measured_peak": gemm_tflops / peaks["mfma_bf16_tflops"],
         },
+        "measured_peaks": peaks,
         "kernels": kernels,
         "wall_s_timed": wall,
     }

@@ -208,12 +208,15 @@ fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);
  * summed event time in ms, and the summed algorithmic FLOPs and bytes of
  * those launches (GEMM: 2*M*N*K; attention forward: 2*B*H*hd*T*(T+1), the
  * causal half of QK^T and PV; attention backward: twice that; norm: bytes
- * of the rows read and written).  fal_profile_enable(ctx, 0) turns timing
- * off; either call clears the counters.  Host memory only; no device
- * allocation. */
+ * of the rows read and written; cross-entropy: logits read and dlogits
+ * written; embedding: rows gathered and written forward, the position-
+ * gradient and scatter traffic backward; bias gradients: the column sums'
+ * input).  fal_profile_enable(ctx, 0) turns timing off; either call clears
+ * the counters.  Host memory only; no device allocation. */
 typedef enum {
   FAL_PROF_GEMM = 0, FAL_PROF_ATTN_FWD = 1, FAL_PROF_ATTN_BWD = 2, FAL_PROF_NORM = 3,
-  FAL_PROF_NCLASS = 4
+  FAL_PROF_CE = 4, FAL_PROF_EMBED = 5, FAL_PROF_BIAS = 6,
+  FAL_PROF_NCLASS = 7
 } fal_prof_class_t;
 fal_status_t fal_profile_enable(fal_ctx_t* ctx, int32_t enable);
 fal_status_t fal_profile_read(fal_ctx_t* ctx, int32_t cls, int64_t* launches, double* total_ms,

@@ -3,7 +3,9 @@
     python -m paper_2510_14614_amd.build
 
 Compiles every source under csrc/ with hipcc into _build/ (one object per
-source, in parallel) and links paper_2510_14614_amd/libfal.so.
+source, in parallel) and links paper_2510_14614_amd/libfal.so; also builds
+libfal_probe.so from probe/ (measured hardware ceilings for bench.py, not
+part of the training path).
 """
 from __future__ import annotations
 
@@ -18,6 +20,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfal.so")
+PROBE_SRC = os.path.join(HERE, "probe", "peak.hip")
+PROBE_LIB = os.path.join(HERE, "libfal_probe.so")
 ARCH = "gfx950"
 
 
@@ -66,8 +70,14 @@ def build(verbose: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), *COMMON_FLAGS, "-shared", PROBE_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("probe build failed:\n" + r.stdout + r.stderr)
+    os.replace(tmp, PROBE_LIB)
     if verbose:
-        print(f"built {LIB} from {len(srcs)} sources")
+        print(f"built {LIB} from {len(srcs)} sources and {PROBE_LIB}")
     return LIB
 
 

@@ -163,6 +163,7 @@ struct Work {
   void* first_in;              // first-attention tensor of the current step
   float* Dvec;
   float *part_main, *part_aux;
+  float* bias_part;  // packed column-sum partials of one block's bias gradients
   float *splitk_main, *splitk_aux;  // split-K partials, one region per stream
   int64_t splitk_floats;
   int32_t* keys;
@@ -222,11 +223,10 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.dog = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
   W.dqkv = cv.take<char>(M * 3 * D.dA * es);
   W.Dvec = cv.take<float>((int64_t)D.B * D.H * D.T);
-  const int64_t wmax = std::max<int64_t>({3 * (int64_t)D.dA, (int64_t)D.f, d, 1});
-  const int64_t part = std::max<int64_t>({ln_bwd_scratch((int)M, (int)d), col_sum_scratch((int)M, (int)wmax),
-                                          dot_scratch(M * d)});
+  const int64_t part = std::max<int64_t>({ln_bwd_scratch((int)M, (int)d), dot_scratch(M * d)});
   W.part_main = cv.take<float>(part);
   W.part_aux = cv.take<float>(part);
+  W.bias_part = cv.take<float>(col_sum_batch_scratch((int)M, (int)(2 * d + D.f + 3 * D.dA)));
   // a split is only chosen while fewer than 512 output tiles of 128x128
   // exist, so (512 + 512) tiles of partials bound every split decision
   W.splitk_floats = (int64_t)1024 * 128 * 128;
@@ -529,8 +529,27 @@ struct Run {
     p.epi = EPI_STORE; p.out_f32 = 1; p.out = dW; p.ldo = out;
     return p;
   }
-  void colsum(const void* x, int in_f32, int64_t ld, int N, float* out, float* part, hipStream_t s) {
-    FAL_TRY(col_sum(dt, in_f32, x, ld, ctx->D.M, N, out, part, s));
+  // Bias gradients are column sums of the layer's output gradient.  They are
+  // queued while a block's backward runs and computed together at its end
+  // (two launches per block); a second bias with the same gradient (b_o and
+  // b_2 of a FAL block) shares the sum.
+  ColSumBatch bias{};
+  void colsum(const void* x, int in_f32, int64_t ld, int N, float* out, float*, hipStream_t) {
+    for (int k = 0; k < bias.n; ++k) {
+      ColSumInput& in = bias.in[k];
+      if (in.x == x && in.ld == ld && in.N == N && !in.out2) { in.out2 = out; return; }
+    }
+    if (bias.n == kColSumMax) flush_bias(ctx->sm);
+    bias.in[bias.n++] = ColSumInput{x, ld, N, in_f32 || dt == F32 ? 1 : 0, out, nullptr};
+  }
+  void flush_bias(hipStream_t s) {
+    if (bias.n == 0) return;
+    bias.M = ctx->D.M;
+    double bytes = 0.0;
+    for (int k = 0; k < bias.n; ++k) bytes += (double)ctx->D.M * bias.in[k].N * (bias.in[k].f32 ? 4.0 : (double)ctx->D.es);
+    Span span(ctx, FAL_PROF_BIAS, s, 0.0, bytes);
+    FAL_TRY(col_sum_batch(dt, bias, ctx->W.bias_part, s));
+    bias = ColSumBatch{};
   }
 
   // MLP branch backward: from dM (lp copy, and fp32 for the bias) to dH2
@@ -586,6 +605,11 @@ struct Run {
   // dy: fp32 gradient of the block output; dy_lp: its dtype copy.
   void block_bwd(int layer, const void* bp, const float* x, const float* dy, const void* dy_lp,
                  float* dx, void* dx_lp, float* dfirst, float* gb) {
+    block_bwd_parts(layer, bp, x, dy, dy_lp, dx, dx_lp, dfirst, gb);
+    flush_bias(ctx->sm);  // after the join: the aux stream's gradients are complete
+  }
+  void block_bwd_parts(int layer, const void* bp, const float* x, const float* dy, const void* dy_lp,
+                       float* dx, void* dx_lp, float* dfirst, float* gb) {
     const Dims& D = ctx->D;
     Work& W = ctx->W;
     const LayerSlot& S = W.slots[layer];
@@ -846,7 +870,10 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
   W.first_in = W.first;
   try {
     Run r(ctx);
-    FAL_TRY(embed_fwd(r.dt, tokens, D.B, D.T, D.V, D.d, gparam(FAL_P_WTE), gparam(FAL_P_WPE), W.resid, sm));
+    {
+      Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * (2.0 * D.es + 4.0));
+      FAL_TRY(embed_fwd(r.dt, tokens, D.B, D.T, D.V, D.d, gparam(FAL_P_WTE), gparam(FAL_P_WPE), W.resid, sm));
+    }
     for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), W.resid + i * Md, W.resid + (i + 1) * Md, W.first);
     const float* xl = W.resid + (int64_t)D.L * Md;
     {
@@ -857,7 +884,10 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
     GemmProblem ph = Run::prob(W.hf, D.d, gparam(FAL_P_WTE), D.d, D.M, D.V, D.d);
     ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.logits; ph.ldo = D.Vp;
     r.gemm1(1, 1, ph, sm);
-    FAL_TRY(cross_entropy(r.dt, W.logits, D.Vp, tokens, D.B, D.T, D.V, W.dlogits, D.Vp, W.row_loss, loss, sm));
+    {
+      Span span(ctx, FAL_PROF_CE, sm, 0.0, (double)D.M * (4.0 * D.V + (double)D.es * D.Vp));
+      FAL_TRY(cross_entropy(r.dt, W.logits, D.Vp, tokens, D.B, D.T, D.V, W.dlogits, D.Vp, W.row_loss, loss, sm));
+    }
     if (logits)
       FAL_TRY(hipMemcpy2DAsync(logits, (size_t)D.V * 4, W.logits, (size_t)D.Vp * 4, (size_t)D.V * 4, D.M,
                                hipMemcpyDeviceToDevice, sm));
@@ -879,8 +909,12 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       std::swap(cur, nxt);
       std::swap(cur_lp, nxt_lp);
     }
-    FAL_TRY(embed_bwd(tokens, D.B, D.T, D.V, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE],
-                      W.keys, W.dh1, sm));
+    {
+      // dX read twice (position sums, scatter), touched wte-gradient rows read and written
+      Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * 16.0);
+      FAL_TRY(embed_bwd(tokens, D.B, D.T, D.V, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE],
+                        W.keys, W.dh1, sm));
+    }
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }

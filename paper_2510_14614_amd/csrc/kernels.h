@@ -140,12 +140,25 @@ hipError_t norm_bwd(const float* a, const float* mean, const float* rstd, const 
 // Sum `nblk` partial rows of width d: out[j] = sum_b part[b * stride + j].
 hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float* out, hipStream_t s);
 
-// Column sums of a [M, N] matrix (dtype or fp32) into fp32 out[N] (bias
-// gradients).  Deterministic two-stage reduction with `scratch` of
-// col_sum_scratch(M, N) floats.
-hipError_t col_sum(DType dt, int in_f32, const void* x, int64_t ld, int M, int N, float* out,
-                   float* scratch, hipStream_t s);
-int64_t col_sum_scratch(int M, int N);
+// Several bias gradients at once: out_i[j] = sum_m x_i[m, j] for up to
+// kColSumMax inputs of their own width N_i (multiple of 4) and storage
+// (fp32 or dtype), two kernels in all.  out2_i, if set, receives the same
+// sums (two biases with one gradient).  Fixed summation order.
+constexpr int kColSumMax = 4;
+struct ColSumInput {
+  const void* x;
+  int64_t ld;
+  int N, f32;
+  float* out;
+  float* out2;
+};
+struct ColSumBatch {
+  ColSumInput in[kColSumMax];
+  int n, M;
+};
+hipError_t col_sum_batch(DType dt, const ColSumBatch& b, float* scratch, hipStream_t s);
+// scratch floats for a batch whose widths add up to W
+int64_t col_sum_batch_scratch(int M, int W);
 
 // ------------------------------------------------------------ attention ----
 // Causal multi-head attention on the packed QKV activations [M, 3*dA]

@@ -9,7 +9,7 @@
 //    at once), plus a column kernel for gamma/beta gradients with a fixed
 //    reduction order.
 //  * norm_bwd: backward of the affine-free normalisation of A_1 (FAL+).
-//  * col_sum: bias gradients.
+//  * col_sum_batch: bias gradients, up to four matrices per pair of launches.
 // All of these are HBM-bound; rows are read with 64 consecutive elements
 // per wavefront instruction.
 #include "common.h"
@@ -328,18 +328,52 @@ hipError_t norm_bwd(const float* A, const float* mean, const float* rstd, const 
 // then the fixed-order block reduce.
 constexpr int kColRows = 64;
 
+// One partial launch over every input (grid z = input)
+// writing packed partial rows [block][W], W = sum of the widths, and one
+// reduce over the packed columns that scatters each segment to its outputs.
+struct ColSumPacked {
+  ColSumInput in[kColSumMax];
+  int off[kColSumMax + 1];  // packed column offset of each input; off[n] = W
+  int n, M;
+  float* part;
+};
+
+// Field by field with constant indices: any dynamic index into the by-value
+// kernel argument (or a select between whole structs) copies it to scratch.
+#define FAL_PICK(b, k, f) \
+  ((k) == 0 ? (b).in[0].f : (k) == 1 ? (b).in[1].f : (k) == 2 ? (b).in[2].f : (b).in[3].f)
+
 template <typename S>
-__global__ __launch_bounds__(256) void col_sum_partials(const S* x, int64_t ld, int M, int N, float* part) {
+__global__ __launch_bounds__(256) void col_sum_batch_partials(ColSumPacked b) {
   __shared__ float red[3][256];
+  static_assert(kColSumMax == 4, "update FAL_PICK");
+  const int k = blockIdx.z;
+  ColSumInput in;
+  in.x = FAL_PICK(b, k, x);
+  in.ld = FAL_PICK(b, k, ld);
+  in.N = FAL_PICK(b, k, N);
+  in.f32 = FAL_PICK(b, k, f32);
+  const int off = k == 0 ? b.off[0] : k == 1 ? b.off[1] : k == 2 ? b.off[2] : b.off[3];
+  const int W = b.n == 1 ? b.off[1] : b.n == 2 ? b.off[2] : b.n == 3 ? b.off[3] : b.off[4];
   const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
   const int j = blockIdx.x * 256 + cl * 4;
+  if (blockIdx.x * 256 >= in.N) return;  // uniform: this input is narrower
   float s[4] = {0.f, 0.f, 0.f, 0.f};
-  if (j < N) {
-    const int r0 = blockIdx.y * kColRows + rg * (kColRows / 4), r1 = min(M, r0 + kColRows / 4);
-    for (int r = r0; r < r1; ++r) {
-      const S* p = x + (int64_t)r * ld + j;
+  if (j < in.N) {
+    const int r0 = blockIdx.y * kColRows + rg * (kColRows / 4), r1 = min(b.M, r0 + kColRows / 4);
+    if (in.f32) {
+      const float* x = static_cast<const float*>(in.x);
+      for (int r = r0; r < r1; ++r) {
+        const float4 v = *reinterpret_cast<const float4*>(x + (int64_t)r * in.ld + j);
+        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+      }
+    } else {
+      const S* x = static_cast<const S*>(in.x);
+      for (int r = r0; r < r1; ++r) {
+        const S* p = x + (int64_t)r * in.ld + j;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) s[c] += to_f(p[c]);
+        for (int c = 0; c < 4; ++c) s[c] += to_f(p[c]);
+      }
     }
   }
   if (rg > 0) {
@@ -347,28 +381,67 @@ __global__ __launch_bounds__(256) void col_sum_partials(const S* x, int64_t ld, 
     for (int c = 0; c < 4; ++c) red[rg - 1][cl * 4 + c] = s[c];
   }
   __syncthreads();
-  if (rg == 0 && j < N) {
+  if (rg == 0 && j < in.N) {
     float v[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) v[c] = ((s[c] + red[0][cl * 4 + c]) + red[1][cl * 4 + c]) + red[2][cl * 4 + c];
-    *reinterpret_cast<float4*>(part + (int64_t)blockIdx.y * N + j) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(b.part + (int64_t)blockIdx.y * W + off + j) = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
-int64_t col_sum_scratch(int M, int N) { return (int64_t)cdiv(M, kColRows) * N; }
+__global__ __launch_bounds__(256) void col_reduce_batch(ColSumPacked b, int nblk) {
+  __shared__ float red[4][64];
+  const int W = b.n == 1 ? b.off[1] : b.n == 2 ? b.off[2] : b.n == 3 ? b.off[3] : b.off[4];
+  const int col = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int q = threadIdx.x >> 6;
+  float s = 0.f;
+  if (col < W)
+    for (int blk = q; blk < nblk; blk += 4) s += b.part[(int64_t)blk * W + col];
+  red[q][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (q == 0 && col < W) {
+    const int c = threadIdx.x & 63;
+    const float v = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+#pragma unroll
+    for (int k = 0; k < kColSumMax; ++k) {
+      if (k < b.n && col >= b.off[k] && col < b.off[k + 1]) {
+        float* o = b.in[k].out;
+        float* o2 = b.in[k].out2;
+        o[col - b.off[k]] = v;
+        if (o2) o2[col - b.off[k]] = v;
+      }
+    }
+  }
+}
 
-hipError_t col_sum(DType dt, int in_f32, const void* x, int64_t ld, int M, int N, float* out,
-                   float* scratch, hipStream_t s) {
-  if (N % 4 || ld % 4) return hipErrorInvalidValue;
-  const int nblk = cdiv(M, kColRows);
-  const dim3 grid(cdiv(N, 256), nblk), block(256);
-  if (in_f32 || dt == F32)
-    hipLaunchKernelGGL((col_sum_partials<float>), grid, block, 0, s, static_cast<const float*>(x), ld, M, N, scratch);
+int64_t col_sum_batch_scratch(int M, int W) { return (int64_t)cdiv(M, kColRows) * W; }
+
+hipError_t col_sum_batch(DType dt, const ColSumBatch& b, float* scratch, hipStream_t s) {
+  if (b.n < 1 || b.n > kColSumMax || !scratch) return hipErrorInvalidValue;
+  ColSumPacked p{};
+  p.n = b.n;
+  p.M = b.M;
+  p.part = scratch;
+  int w = 0, maxn = 0;
+  for (int k = 0; k < b.n; ++k) {
+    const ColSumInput& in = b.in[k];
+    if (!in.x || !in.out || in.N % 4 || in.ld % 4 || in.N < 1) return hipErrorInvalidValue;
+    p.in[k] = in;
+    p.off[k] = w;
+    w += in.N;
+    maxn = std::max(maxn, in.N);
+  }
+  p.off[b.n] = w;
+  const int nblk = cdiv(b.M, kColRows);
+  const dim3 grid(cdiv(maxn, 256), nblk, b.n), block(256);
+  if (dt == F32)
+    hipLaunchKernelGGL((col_sum_batch_partials<float>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((col_sum_partials<bf16>), grid, block, 0, s, static_cast<const bf16*>(x), ld, M, N, scratch);
+    hipLaunchKernelGGL((col_sum_batch_partials<bf16>), grid, block, 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return col_reduce(scratch, nblk, N, N, out, s);
+  hipLaunchKernelGGL(col_reduce_batch, dim3(cdiv(w, 64)), dim3(256), 0, s, p, nblk);
+  return hipGetLastError();
 }
 
 }  // namespace fal

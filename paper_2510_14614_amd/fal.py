@@ -29,8 +29,9 @@ ABI_FUNCTIONS = (
     "fal_block_fwd", "fal_block_bwd", "fal_model_step", "fal_stack_step", "fal_residual_out",
     "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error",
 )
-PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM = range(4)
-PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm"}
+PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM, PROF_CE, PROF_EMBED, PROF_BIAS = range(7)
+PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm",
+              PROF_CE: "cross_entropy", PROF_EMBED: "embedding", PROF_BIAS: "bias_grad"}
 
 
 class fal_config_t(ctypes.Structure):
