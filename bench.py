@@ -234,12 +234,12 @@ def summarize_stats(stats_csv, out_md, cmds):
         name = r["Name"].replace("|", "/")[:110]
         lines.append(f"| `{name}` | {int(r['Calls'])} | {float(r['AverageNs']) / 1e3:.1f} | {ms:.2f} | "
                      f"{float(r['Percentage']):.1f} |")
-    gm = [r for r in rows if "gemm_bf16_mfma" in r["Name"]]
+    gm = [r for r in rows if "gemm_bf16_" in r["Name"]]
     red = [r for r in rows if "splitk_reduce" in r["Name"]]
     n = sum(int(r["Calls"]) for r in gm)
     tg = sum(float(r["TotalDurationNs"]) for r in gm)
     tr = sum(float(r["TotalDurationNs"]) for r in red)
-    lines += ["", f"gemm_bf16_mfma (all instantiations): {n} calls, average {tg / n / 1e3:.1f} us per call; "
+    lines += ["", f"bf16 GEMM kernels (all instantiations): {n} calls, average {tg / n / 1e3:.1f} us per call; "
               f"with the split-K reduces they launch, {(tg + tr) / n / 1e3:.1f} us per call (the span bench.py "
               f"times as one GEMM call)."]
     open(out_md, "w").write("\n".join(lines) + "\n")
@@ -254,7 +254,7 @@ def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
         probe = [r for r in rows if "MulFunctor" in r["Kernel_Name"]]
         assert probe, "no copy-probe dispatch in " + path
         calib = probe_bytes / (float(probe[-1]["Counter_Value"]) * 1024.0)
-        g = [float(r["Counter_Value"]) * 1024.0 for r in rows if "gemm_bf16_mfma" in r["Kernel_Name"]]
+        g = [float(r["Counter_Value"]) * 1024.0 for r in rows if "gemm_bf16_" in r["Kernel_Name"]]
         red = [float(r["Counter_Value"]) * 1024.0 for r in rows if "splitk_reduce" in r["Kernel_Name"]]
         return calib, probe_bytes, float(probe[-1]["Counter_Value"]) * 1024.0, g, red, len(rows)
     cf, pbf, rawf, gf, rf, _ = load(fetch_csv, "FETCH_SIZE")
@@ -263,14 +263,14 @@ def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
     assert n == len(gw) and n > 0
     fetch = (sum(gf) + sum(rf)) * cf / n
     write = (sum(gw) + sum(rw)) * cw / n
-    lines = ["# HBM traffic of gemm_bf16_mfma, gpt2-small FAL training step", "",
+    lines = ["# HBM traffic of the bf16 GEMM kernels, gpt2-small FAL training step", "",
              "Commands (repository root on the GPU host, `TMPDIR=/tmp`), one counter per run:", "",
              "```", *cmds, "```", "",
              "Each run ends with a plain elementwise copy (`--copy-probe`) that reads and writes a known number",
              "of bytes; its counter reading calibrates the counter for this part:", "",
              f"- FETCH_SIZE: copy of {pbf / 2**20:.0f} MiB read {rawf / 2**20:.1f} MiB -> factor {cf:.4f}",
              f"- WRITE_SIZE: copy of {pbw / 2**20:.0f} MiB wrote {raww / 2**20:.1f} MiB -> factor {cw:.4f}", "",
-             f"Over {n} GEMM calls (each call = one gemm_bf16_mfma dispatch plus the split-K reduce it may launch):", "",
+             f"Over {n} GEMM calls (each call = one bf16 GEMM dispatch plus the split-K reduce it may launch):", "",
              f"- `fetch_bytes_per_call`: {fetch:.0f}",
              f"- `write_bytes_per_call`: {write:.0f}",
              f"- `traffic_bytes_per_call`: {fetch + write:.0f}",
@@ -351,7 +351,7 @@ def main():
         "mfu": flops_step / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS,
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm_bf16_mfma (all bf16 GEMM launches of the step)",
+            "kernel": "gemm_bf16_pipe / gemm_bf16_mfma (all bf16 GEMM launches of the step)",
             "achieved": gemm_tflops,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",

@@ -894,6 +894,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
     // head backward: dHf = dlogits wte ; dwte = dlogits^T Hf
     GemmProblem pd = Run::prob(W.dlogits, D.Vp, gparam(FAL_P_WTE), D.d, D.M, D.d, D.V);
     pd.epi = EPI_STORE; pd.out_f32 = 1; pd.out = W.dh1; pd.ldo = D.d;
+    pd.kpad = 1;  // dlogits columns V .. Vp-1 are written as zeros
     r.gemm1(1, 0, pd, sm);
     r.gemm1(0, 0, r.wgrad(W.dlogits, D.Vp, W.hf, D.d, D.V, D.d, D.M, grads + Lo.goff[FAL_P_WTE]), sm);
     {

@@ -423,6 +423,9 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
 
 
 
+#ifndef FAL_GEMM_PIPE
+#define FAL_GEMM_PIPE 1
+#endif
 #ifndef FAL_GEMM_REMAP
 #define FAL_GEMM_REMAP 1
 #endif
@@ -578,6 +581,364 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
   }
 }
 
+// ------------------------------------- MFMA (bf16), direct-to-LDS pipeline --
+// Four wavefronts (one per SIMD) own a BM x BN output tile as 2 x 2
+// wavefront tiles of (BM/2) x (BN/2).  K advances in slices of 32 (one
+// 16x16x32 MFMA step).  Each slice of both operands is copied from global
+// memory straight into one of four LDS stages by buffer loads with the LDS
+// destination (no registers, no LDS store instructions), three slices ahead
+// of the slice being multiplied; the fragments of slice s + 1 are read while
+// the MFMAs of slice s run.  One workgroup barrier per slice.
+//
+// LDS layout of one operand in one stage (R rows of the output dimension):
+//  * k-contiguous operand: R rows of 32 k (64 B), 16-byte chunk c of row r
+//    stored at chunk c ^ ((r >> 2) & 3): the 16 rows of a fragment read
+//    (one chunk each) fall in 16 different 16-byte bank groups.
+//  * MN-major operand: 32 k-rows of R elements, 32-byte segment q of k-row k
+//    stored at segment q ^ g(k), g(k) = (k & 3) | ((k >> 3) & 1) << 2: the
+//    16 k-rows touched by one transposing read hit each 32-byte bank group
+//    exactly twice (the minimum for 512 bytes).
+// A buffer load writes lane l's 16 bytes at LDS offset 16 l of its 1 KiB
+// block, so the swizzle is applied by choosing which global chunk each lane
+// fetches.  Rows past M / N and k past K read outside the buffer's range and
+// land as zeros; k past K inside a k-contiguous row is pointed out of range.
+namespace pipe {
+constexpr int KS = 32;
+constexpr int NS = 4;                       // LDS stages
+constexpr uint32_t kOob = 0x80000000u;      // offset beyond any buffer range (ranges are < 2^31)
+
+__device__ __forceinline__ int mn_g(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+__device__ __forceinline__ lds_void_t* lds_ptr(const void* p) {
+  return (lds_void_t*)((__attribute__((address_space(3))) char*)(const_cast<void*>(p)));
+}
+
+// One operand's loader (both K segments).  Load block i of this wavefront
+// is block 4 i + wave of the stage region; its global offset is a per-lane
+// part (which repeats with period NV in i) plus a wave-uniform step per i.
+template <int R, int KMAJ>
+struct Src {
+  static constexpr int BYTES = R * KS * 2;                 // one stage region
+  static constexpr int NINS = BYTES / 1024;                // 1 KiB load blocks per slice
+  static constexpr int IPW = NINS / 4;                     // per wavefront
+  static constexpr int CPR = R / 8;                        // MN-major: 16-byte chunks per k-row
+  static constexpr int RPI = KMAJ ? 16 : 1024 / (2 * R);   // rows / k-rows per block
+  // MN-major: the swizzle g(k) of a lane's k-row repeats every 16 k-rows
+  static constexpr int NV = KMAJ ? 1 : ((4 * RPI) % 16 == 0 ? 1 : 16 / (4 * RPI));
+  static_assert(NINS % 4 == 0 && IPW % NV == 0, "tile too small for four wavefronts");
+  uint32_t voff[2][NV];    // per segment
+  uint32_t istep[2];       // bytes from block i to block i + 1 of this wavefront
+  int kof;                 // k-contiguous: k offset of this lane's chunk within the slice
+  uint64_t base[2];
+  int nbytes[2];
+  uint32_t kstep[2];       // bytes per k (k-contiguous: 2; MN-major: 2 ld)
+
+  __device__ __forceinline__ void init(int seg, const bf16* X, int64_t ld, int r0, int Rmax, int Kseg, int wave,
+                                       int lane) {
+    base[seg] = reinterpret_cast<uint64_t>(KMAJ ? X + (int64_t)r0 * ld : X + r0);
+    const int64_t ext = KMAJ ? (int64_t)(Rmax - r0) * ld * 2 : ((int64_t)Kseg * ld - r0) * 2;
+    nbytes[seg] = (int)min<int64_t>(ext, 0x7fffffff);
+    kstep[seg] = KMAJ ? 2u : (uint32_t)(ld * 2);
+    istep[seg] = (uint32_t)(4 * RPI * ld * 2);
+    if (KMAJ) {
+      const int row = wave * 16 + (lane >> 2);
+      const int gc = (lane & 3) ^ ((row >> 2) & 3);
+      voff[seg][0] = (uint32_t)(((int64_t)row * ld + gc * 8) * 2);
+      kof = gc * 8;
+    } else {
+      kof = 0;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int k = (4 * v + wave) * RPI + lane / CPR;
+        const int gc = (lane % CPR) ^ (2 * mn_g(k));
+        voff[seg][v] = (uint32_t)(((int64_t)k * ld + gc * 8) * 2);
+      }
+    }
+  }
+  __device__ __forceinline__ void clear(int seg) {
+    base[seg] = base[0];
+    nbytes[seg] = 0;
+    kstep[seg] = istep[seg] = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) voff[seg][v] = kOob;
+  }
+
+  // Load state: the slice the next load() fetches.
+  uint32_t rlo, rhi;
+  int rn;
+  uint32_t so, is, ks;
+  uint32_t vo[NV];
+  // Point the state at the slice at k0 of segment seg; chunks at slice
+  // offset >= lim are pointed out of range (lim: 0 for a slice past the
+  // end, K - k0 in a k-contiguous tail slice, KS otherwise).
+  __device__ __forceinline__ void set(int seg, int k0, int lim) {
+    const uint64_t b = seg ? base[1] : base[0];
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    rlo = lo;
+    rhi = hi;
+    rn = __builtin_amdgcn_readfirstlane(seg ? nbytes[1] : nbytes[0]);
+    ks = __builtin_amdgcn_readfirstlane(seg ? kstep[1] : kstep[0]);
+    so = (uint32_t)k0 * ks;
+    is = __builtin_amdgcn_readfirstlane(seg ? istep[1] : istep[0]);
+    const bool bad = kof >= lim;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) vo[v] = bad ? kOob : (seg ? voff[1][v] : voff[0][v]);
+  }
+  // Next slice of the same segment (full and live).
+  __device__ __forceinline__ void advance() { so += KS * ks; }
+  // Issue this wavefront's loads of the current slice into the region at dst.
+  __device__ __forceinline__ void load(char* dst, int wave) const {
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(((uint64_t)rhi << 32) | rlo), (short)0, rn, kRsrcWord3);
+    // (the offsets go through locals: with member expressions as builtin
+    // arguments the host pass drops the kernel's launch stubs)
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const uint32_t v = vo[i % NV];
+      const uint32_t o = so + (uint32_t)(i - i % NV) * is;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds_ptr(dst + (i * 4 + wave) * 1024), 16, v, o, 0, 0);
+    }
+  }
+};
+
+// Fragment reads from one stage region (byte addresses precomputed per lane).
+template <int R, int KMAJ, int NF>
+struct Frag {
+  uint32_t off[KMAJ ? 1 : NF];
+  // row0: first row of fragment 0 within the region (the wavefront tile's base)
+  __device__ __forceinline__ void init(int row0, int lane) {
+    if (KMAJ) {
+      off[0] = (uint32_t)((row0 + (lane & 15)) * 64 + ((((lane >> 4) ^ ((lane >> 2) & 3))) << 4));
+    } else {
+      const int k = 8 * (lane >> 4) + ((lane & 15) >> 2);
+      const int g2 = 2 * mn_g(k);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        const int mn0 = row0 + 16 * f;
+        off[f] = (uint32_t)(k * 2 * R + (((((mn0 >> 3) ^ g2) + ((lane & 3) >> 1))) << 4) + 8 * (lane & 1));
+      }
+    }
+  }
+  __device__ __forceinline__ bf16x8_t read(const char* region, int f) const {
+    if (KMAJ) return *reinterpret_cast<const bf16x8_t*>(region + off[0] + f * 16 * 64);
+    const bf16* p = reinterpret_cast<const bf16*>(region + off[f]);
+    const i16x4_t lo = lds_read_tr(p), hi = lds_read_tr(p + 4 * R);
+    const i16x4_t v8[2] = {lo, hi};
+    return *reinterpret_cast<const bf16x8_t*>(v8);
+  }
+};
+
+// s_waitcnt with vmcnt(v) and lgkmcnt(l) (gfx9 encoding; expcnt not waited)
+#define FAL_WAITCNT(v, l) __builtin_amdgcn_s_waitcnt(((v) & 15) | (((v) >> 4) << 14) | (7 << 4) | ((l) << 8))
+__device__ __forceinline__ void bar() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+}  // namespace pipe
+
+template <int AK, int BKM, int BM, int BN, int OCC>
+__global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu_tanh) {
+  using namespace pipe;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  typedef Src<BM, AK> SA;
+  typedef Src<BN, BKM> SB;
+  constexpr int SBYTES = SA::BYTES + SB::BYTES;
+  constexpr int L = SA::IPW + SB::IPW;  // loads per wavefront per slice
+  static_assert(2 * L <= 63, "vmcnt range");
+  // one array per stage: the compiler tracks buffer-to-LDS loads per array
+  __shared__ __attribute__((aligned(1024))) char st0[SBYTES], st1[SBYTES], st2[SBYTES], st3[SBYTES];
+
+#if FAL_GEMM_REMAP
+  const int bid = xcd_remap(blockIdx.x, g.total_tiles);
+#else
+  const int bid = blockIdx.x;
+#endif
+  const GemmProblem P = find_problem(g, bid);
+  const int per_split = P.tiles_m * P.tiles_n;
+  const int local = (bid - P.tile_start) % per_split;
+  const int split = (bid - P.tile_start) / per_split;
+  int tmi, tni;
+  grouped_tile(local, P.tiles_m, P.tiles_n, tmi, tni);
+  const int m0 = tmi * BM, n0 = tni * BN;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // slices: segment 0 is [0, nt1), segment 1 is [nt1, nt)
+  const int nt1 = (P.K + KS - 1) / KS;
+  int sbeg = 0, send = nt1 + (P.K2 > 0 ? (P.K2 + KS - 1) / KS : 0);
+  if (P.splits > 1) {
+    const int per = (nt1 + P.splits - 1) / P.splits;
+    sbeg = min(nt1, split * per);
+    send = min(nt1, sbeg + per);
+  }
+  const int n = send - sbeg;
+
+  SA sa;
+  SB sb;
+  sa.init(0, static_cast<const bf16*>(P.A), P.lda, m0, P.M, P.K, wave, lane);
+  sb.init(0, static_cast<const bf16*>(P.B), P.ldb, n0, P.N, P.K, wave, lane);
+  if (P.K2 > 0) {
+    sa.init(1, static_cast<const bf16*>(P.A2), P.lda2, m0, P.M, P.K2, wave, lane);
+    sb.init(1, static_cast<const bf16*>(P.B2), P.ldb2, n0, P.N, P.K2, wave, lane);
+  } else {  // never selected; an empty range all the same
+    sa.clear(1);
+    sb.clear(1);
+  }
+  // Slices s with f_lo < s < f_hi are full, live and in the segment of the
+  // current load state: the loader only advances.  Others (segment start,
+  // k tail, past the end) recompute the state.
+  int f_lo = 0, f_hi = 0;
+  const int full0 = P.K / KS, full1 = nt1 + P.K2 / KS;
+  auto issue = [&](char* stage, int s) {
+    if (s > f_lo && s < f_hi) {
+      sa.advance();
+      sb.advance();
+    } else {
+      const bool live = s < send;
+      const int seg = live && s >= nt1 ? 1 : 0;
+      const int k0 = live ? (seg ? s - nt1 : s) * KS : 0;
+      const int Kseg = seg ? P.K2 : P.K;
+      // k-contiguous operands read whole 8-element chunks up to Kpad
+      const int Kpad = P.kpad ? (Kseg + 7) / 8 * 8 : Kseg;
+      const int lim = !live ? 0 : k0 + KS > Kpad ? Kpad - k0 : KS;
+      sa.set(seg, k0, AK ? lim : (live ? KS : 0));
+      sb.set(seg, k0, BKM ? lim : (live ? KS : 0));
+      f_lo = s;
+      f_hi = live && k0 + KS <= Kseg ? min(send, seg ? full1 : full0) : s;
+    }
+    sa.load(stage, wave);
+    sb.load(stage + SA::BYTES, wave);
+  };
+
+  Frag<BM, AK, FM> fa;
+  Frag<BN, BKM, FN> fb;
+  fa.init(wm * WTM, lane);
+  fb.init(wn * WTN, lane);
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  bf16x8_t ra[2][FM], rb[2][FN];
+
+  auto read = [&](const char* stage, int buf) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) ra[buf][i] = fa.read(stage, i);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) rb[buf][j] = fb.read(stage + SA::BYTES, j);
+  };
+  // MFMAs of the slice in buffer `cur` with the fragment reads of the next
+  // slice (from `stage`) into buffer cur ^ 1: B's fragments first, spread
+  // over the first MFMAs; A's fragment i right after the last MFMA that uses
+  // A's current fragment i, so the two can share registers.
+  auto step = [&](const char* stage, int cur) {
+    const int nxt = cur ^ 1;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) rb[nxt][j] = fb.read(stage + SA::BYTES, j);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[cur][i], rb[cur][j], acc[i][j], 0, 0, 0);
+      ra[nxt][i] = fa.read(stage, i);
+    }
+  };
+  // Issue order inside a step (scheduling groups, in order): per MFMA of
+  // slice s, then B's reads of slice s + 1 one per MFMA, A's read i after
+  // MFMA row i, and the loads of slice s + 3 spread evenly.
+  constexpr int NRB = BKM ? FN : 2 * FN;  // LDS read instructions for B
+  constexpr int RA = AK ? 1 : 2;          // per A fragment
+  constexpr int NMF = FM * FN;
+  constexpr int DMA_EVERY = NMF / L > 0 ? NMF / L : 1;
+  static_assert(NRB <= NMF, "more B reads than MFMAs");
+  auto interleave = [&]() {
+    int dma = 0;
+#pragma unroll
+    for (int q = 0; q < NMF; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if (q < NRB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (B)
+      if ((q + 1) % FN == 0) {
+#pragma unroll
+        for (int r = 0; r < RA; ++r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (A)
+      }
+      if (q % DMA_EVERY == 0 && dma < L) {
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // buffer load to LDS
+        ++dma;
+      }
+    }
+  };
+  // The last A reads of a step may still be in flight at the next step's
+  // barrier; reads of the slice before (whose stage is refilled after the
+  // barrier) are older and complete.
+  constexpr int LGK = FM * RA < 15 ? FM * RA : 15;
+
+  if (n > 0) {
+    // prologue: slices sbeg .. sbeg+2 into stages 0..2; slice sbeg's fragments
+    issue(st0, sbeg);
+    issue(st1, sbeg + 1);
+    issue(st2, sbeg + 2);
+    FAL_WAITCNT(2 * L, 0);
+    bar();
+    read(st0, 0);
+    // step s: wait for own loads of slice s + 1 and own reads of slice s - 1,
+    // barrier (slice s + 1 complete in LDS; slice s - 1's stage free), load
+    // slice s + 3 into that stage, MFMAs of slice s with slice s + 1's reads.
+#define FAL_PIPE_STEP(U, NXT, PRV)                 \
+  {                                                \
+    const int s = t + U;                           \
+    FAL_WAITCNT(L, LGK);                           \
+    bar();                                         \
+    __builtin_amdgcn_sched_barrier(0);             \
+    issue(PRV, s + 3);                             \
+    step(NXT, U & 1);                              \
+    interleave();                                  \
+    __builtin_amdgcn_sched_barrier(0);             \
+  }
+    // The slice count is rounded up to whole groups of NS: slices past the
+    // end load zeros in both operands and add nothing.
+    const int tend = sbeg + ((n + NS - 1) / NS) * NS;
+    for (int t = sbeg; t < tend; t += NS) {
+      FAL_PIPE_STEP(0, st1, st3)
+      FAL_PIPE_STEP(1, st2, st0)
+      FAL_PIPE_STEP(2, st3, st1)
+      FAL_PIPE_STEP(3, st0, st2)
+    }
+#undef FAL_PIPE_STEP
+  }
+  // every load (including those past the end) has landed and every
+  // wavefront is done with the stages before they are reused for staging
+  FAL_WAITCNT(0, 0);
+  bar();
+
+  float* stage = reinterpret_cast<float*>(wm ? st1 : st0) + wn * 16 * (WTN + 4);
+  static_assert(2 * 16 * (WTN + 4) * 4 <= SBYTES, "epilogue staging exceeds a stage");
+  const int mw = m0 + wm * WTM, nw = n0 + wn * WTN;
+  if (P.splits > 1) {
+    GemmProblem Q = P;
+    Q.out = P.part + (int64_t)split * P.M * P.N;
+    Q.ldo = P.N;
+    Q.bias = Q.bias2 = nullptr;
+    Q.vec_out = (P.N & 3) == 0;
+    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    return;
+  }
+  switch (P.epi) {
+    case EPI_STORE:
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+  }
+}
+
 // out[m, n] = sum_s part[s, m, n] (+ bias), s in order.
 __global__ __launch_bounds__(256) void splitk_reduce(const float* part, int splits, int M, int N, const bf16* bias,
                                                      const bf16* bias2, float* out, int64_t ldo) {
@@ -662,18 +1023,98 @@ static const char* check_vec_operand(const void* X, int64_t ld, int kmaj, int ro
   return nullptr;
 }
 
+// Pipelined kernel shapes (gemm_bf16_pipe): four wavefronts of (BM/2) x
+// (BN/2); per_cu resident workgroups per CU (LDS: 4 stages of (BM + BN) x
+// 64 bytes).  Launch time model, fitted to measurements on MI355X
+// (GPT-2-sized problems, 8192^3): a k-slice of one tile costs t1 us when
+// the tile has its CU alone and t2 us when per_cu tiles share it; each
+// round of tiles adds ovh us (prologue, epilogue, launch ramp).
+struct PipeShape { int bm, bn, per_cu; double t1, t2, ovh; };
+enum { PIPE_256x256 = 0, PIPE_256x128 = 1, PIPE_128x256 = 2, PIPE_128x128 = 3, kPipeShapes = 4 };
+constexpr PipeShape kPipe[kPipeShapes] = {{256, 256, 1, 0.85, 0.85, 10.0},
+                                          {256, 128, 1, 0.56, 0.56, 5.0},
+                                          {128, 256, 1, 0.56, 0.56, 5.0},
+                                          {128, 128, 2, 0.30, 0.54, 3.0}};
+constexpr int kPipeKS = 32;
+constexpr double kHbmBytesPerUs = 5.0e6;       // sustained HBM rate for operand re-reads
+constexpr double kPartialBytesPerUs = 8.0e6;   // split-K partials (written and re-read while cached)
+constexpr double kLaunchUs = 5.0;              // the split-K reduce launch
+constexpr double kCachedBytes = 128.0 * (1 << 20);  // operands below this are fetched from HBM once
+
+static int64_t count_tiles_shape(const GemmGroup& g, int bm, int bn) {
+  int64_t t = 0;
+  for (int i = 0; i < g.n; ++i) t += (int64_t)((g.p[i].M + bm - 1) / bm) * ((g.p[i].N + bn - 1) / bn);
+  return t;
+}
+
+// Estimated time (us) of the launch on shape c with K split sp ways.
+static double pipe_estimate(const GemmGroup& g, int c, int sp) {
+  const PipeShape& t = kPipe[c];
+  const int64_t tiles = count_tiles_shape(g, t.bm, t.bn) * sp;
+  int slices = 0;
+  double reread = 0.0;
+  for (int i = 0; i < g.n; ++i) {
+    const GemmProblem& P = g.p[i];
+    const int ns = (P.K + kPipeKS - 1) / kPipeKS + (P.K2 + kPipeKS - 1) / kPipeKS;
+    slices = std::max(slices, (ns + sp - 1) / sp);
+    const double a_bytes = 2.0 * P.M * (P.K + P.K2), b_bytes = 2.0 * P.N * (P.K + P.K2);
+    if (a_bytes > kCachedBytes) reread += a_bytes * ((P.N + t.bn - 1) / t.bn - 1);
+    if (b_bytes > kCachedBytes) reread += b_bytes * ((P.M + t.bm - 1) / t.bm - 1);
+  }
+  const int64_t slots = (int64_t)t.per_cu * kCUs;
+  const int64_t full = tiles / slots, rem = tiles % slots;
+  double us = (double)full * (t.ovh + slices * t.t2);
+  if (rem > 0) us += t.ovh + slices * (rem > kCUs ? t.t2 : t.t1);
+  us += reread / kHbmBytesPerUs;
+  if (sp > 1) us += (2.0 * sp + 1.0) * 4.0 * g.p[0].M * g.p[0].N / kPartialBytesPerUs + kLaunchUs;
+  return us;
+}
+
+// Shape (and split count for a splittable single problem) with the smallest
+// estimated time.
+static void choose_pipe(const GemmGroup& g, bool splittable, int64_t scratch_floats, int& shape, int& splits) {
+  double best = 0.0;
+  shape = PIPE_256x256;
+  splits = 1;
+  const int ns = (g.p[0].K + kPipeKS - 1) / kPipeKS;
+  for (int c = 0; c < kPipeShapes; ++c) {
+    const int maxsp = splittable ? kMaxSplits : 1;
+    for (int sp = 1; sp <= maxsp; ++sp) {
+      if (sp > 1 && (ns / sp < 8 || (int64_t)sp * g.p[0].M * g.p[0].N > scratch_floats)) break;
+      const double us = pipe_estimate(g, c, sp);
+      if ((c == 0 && sp == 1) || us < best) { best = us; shape = c; splits = sp; }
+    }
+  }
+}
+
+// The pipelined kernel reads whole 8-element chunks along K from
+// k-contiguous operands (K a multiple of 8, or zero-padded storage with an
+// MN-major partner) and addresses operands with 32-bit offsets.
+static bool pipe_ok(const GemmGroup& g, int a_kmaj, int b_kmaj) {
+  auto ext_ok = [](int64_t rows, int64_t ld, int64_t K, int kmaj) {
+    const int64_t bytes = kmaj ? rows * ld * 2 : (K + 2 * kPipeKS * 4) * ld * 2;
+    return bytes < ((int64_t)1 << 31) - (int64_t)(1 << 20);
+  };
+  for (int i = 0; i < g.n; ++i) {
+    const GemmProblem& P = g.p[i];
+    if ((a_kmaj || b_kmaj) && (P.K % 8 || P.K2 % 8)) {
+      if (!P.kpad || (a_kmaj && b_kmaj) || P.K2 > 0) return false;
+      const int64_t lda = a_kmaj ? P.lda : P.ldb;  // the k-contiguous operand's row pitch
+      if (lda < (P.K + 7) / 8 * 8) return false;
+    }
+    if (!ext_ok(P.M, P.lda, P.K, a_kmaj) || !ext_ok(P.N, P.ldb, P.K, b_kmaj)) return false;
+    if (P.K2 > 0 && (!ext_ok(P.M, P.lda2, P.K2, a_kmaj) || !ext_ok(P.N, P.ldb2, P.K2, b_kmaj))) return false;
+  }
+  return true;
+}
+
 hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
                 const char** why, float* splitk_scratch, int64_t splitk_floats) {
   *why = nullptr;
   if (g.n < 1 || g.n > kMaxGroup) { *why = "bad GEMM group size"; return hipErrorInvalidValue; }
-  // Weight gradients (one fp32 plain output, few 128x128 tiles) split K on
-  // 128x128 tiles; everything else picks its tile shape.
   const GemmProblem& P0 = g.p[0];
   const bool splittable = dt == BF16 && splitk_scratch && g.n == 1 && P0.K2 == 0 && P0.epi == EPI_STORE &&
-                          P0.out_f32 && count_tiles(g, 128, 128) <= kCUs;
-  const int shape = dt != BF16 ? TILE_SQ : splittable ? TILE_SQ : choose_tile(g);
-  const int tm = dt == BF16 ? kTile[shape].bm : ST, tn = dt == BF16 ? kTile[shape].bn : ST;
-  int total = 0;
+                          P0.out_f32;
   for (int i = 0; i < g.n; ++i) {
     GemmProblem& P = g.p[i];
     if (P.M <= 0 || P.N <= 0 || P.K <= 0 || P.K2 < 0) { *why = "bad GEMM shape"; return hipErrorInvalidValue; }
@@ -684,9 +1125,6 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       if (!e && P.K2 > 0) e = check_vec_operand(P.B2, P.ldb2, b_kmaj, P.N, P.K2);
       if (e) { *why = e; return hipErrorInvalidValue; }
     }
-    P.tiles_m = (P.M + tm - 1) / tm;
-    P.tiles_n = (P.N + tn - 1) / tn;
-    P.tile_start = total;
     P.splits = 1;
     P.part = nullptr;
     {
@@ -702,11 +1140,65 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       if (P.epi == EPI_MUL_AUX) ok = ok && P.aux && al(P.aux, 8) && P.ldaux % 4 == 0;
       P.vec_out = ok ? 1 : 0;
     }
-    total += P.tiles_m * P.tiles_n;
   }
+  auto set_tiles = [&](int tm, int tn) {
+    int total = 0;
+    for (int i = 0; i < g.n; ++i) {
+      GemmProblem& P = g.p[i];
+      P.tiles_m = (P.M + tm - 1) / tm;
+      P.tiles_n = (P.N + tn - 1) / tn;
+      P.tile_start = total;
+      total += P.tiles_m * P.tiles_n;
+    }
+    return total;
+  };
+  auto launch_reduce = [&]() -> hipError_t {
+    const GemmProblem& P = g.p[0];
+    if (g.n == 1 && P.splits > 1) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(splitk_reduce, dim3(cdiv((int64_t)P.M * P.N, 256)), dim3(256), 0, s, P.part, P.splits,
+                         P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
+                         static_cast<float*>(P.out), P.ldo);
+    }
+    return hipGetLastError();
+  };
+
+  if (FAL_GEMM_PIPE && dt == BF16 && pipe_ok(g, a_kmaj, b_kmaj)) {
+    int shape, sp;
+    choose_pipe(g, splittable, splitk_floats, shape, sp);
+    int total = set_tiles(kPipe[shape].bm, kPipe[shape].bn);
+    if (sp > 1) {
+      g.p[0].splits = sp;
+      g.p[0].part = splitk_scratch;
+      total *= sp;
+    }
+    g.total_tiles = total;
+    const dim3 grid(total), block(256);
+#define FAL_PIPE_LAUNCH(BM, BN, OCC)                                                                           \
+  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh); \
+  else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
+  else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<0, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
+  else hipLaunchKernelGGL((gemm_bf16_pipe<0, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);
+    switch (shape) {
+      case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1) break;
+      case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1) break;
+      case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1) break;
+      default: FAL_PIPE_LAUNCH(128, 128, 2) break;
+    }
+#undef FAL_PIPE_LAUNCH
+    return launch_reduce();
+  }
+
+  // Weight gradients (one fp32 plain output, few 128x128 tiles) split K on
+  // 128x128 tiles; everything else picks its tile shape.
+  const bool split_sq = splittable && count_tiles(g, 128, 128) <= kCUs;
+  const int shape = dt != BF16 ? TILE_SQ : split_sq ? TILE_SQ : choose_tile(g);
+  const int tm = dt == BF16 ? kTile[shape].bm : ST, tn = dt == BF16 ? kTile[shape].bn : ST;
+  int total = set_tiles(tm, tn);
   // Split K for launches that would leave compute units idle (fewer tiles
   // than CUs); fp32 plain outputs only (the weight gradients).
-  if (splittable) {
+  if (split_sq) {
     GemmProblem& P = g.p[0];
     const int tiles = P.tiles_m * P.tiles_n;
     const int sp = choose_splits(tiles, (P.K + KT - 1) / KT, (int64_t)P.M * P.N, splitk_floats);
@@ -732,20 +1224,12 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       FAL_GEMM_LAUNCH(128, 128, 2, 2)
     }
 #undef FAL_GEMM_LAUNCH
-    const GemmProblem& P = g.p[0];
-    if (g.n == 1 && P.splits > 1) {
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(splitk_reduce, dim3(cdiv((int64_t)P.M * P.N, 256)), dim3(256), 0, s, P.part, P.splits,
-                         P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
-                         static_cast<float*>(P.out), P.ldo);
-    }
-  } else {
-    if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 1>), grid, block, 0, s, g, gelu_tanh);
-    else if (a_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 0>), grid, block, 0, s, g, gelu_tanh);
-    else if (b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 0, 1>), grid, block, 0, s, g, gelu_tanh);
-    else hipLaunchKernelGGL((gemm_simt<float, 0, 0>), grid, block, 0, s, g, gelu_tanh);
+    return launch_reduce();
   }
+  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 1>), grid, block, 0, s, g, gelu_tanh);
+  else if (a_kmaj) hipLaunchKernelGGL((gemm_simt<float, 1, 0>), grid, block, 0, s, g, gelu_tanh);
+  else if (b_kmaj) hipLaunchKernelGGL((gemm_simt<float, 0, 1>), grid, block, 0, s, g, gelu_tanh);
+  else hipLaunchKernelGGL((gemm_simt<float, 0, 0>), grid, block, 0, s, g, gelu_tanh);
   return hipGetLastError();
 }
 

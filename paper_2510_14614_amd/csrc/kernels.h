@@ -43,6 +43,11 @@ struct GemmProblem {
   int64_t ldo2;
   const void* aux;    // EPI_MUL_AUX: elementwise factor
   int64_t ldaux;
+  // 1: the k-contiguous operand's rows hold finite values in columns
+  // K .. roundup(K, 8) - 1 (zero padding).  Lets a problem whose K is not a
+  // multiple of 8 run on the pipelined kernel when the other operand is
+  // MN-major (its rows past K read as zero).
+  int kpad;
   // filled in by the launcher
   int tiles_m, tiles_n, tile_start;
   int splits;        // K split into this many slices (fp32 partials + reduce)
