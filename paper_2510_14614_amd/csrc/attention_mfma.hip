@@ -165,7 +165,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
   f32x16v acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) acc[t] = zero16();
-  float m = -INFINITY, lsum = 0.f;
+  // Online softmax against a reference maximum mref (scaled scores, log2
+  // units) that moves only when a row's maximum exceeds it by more than
+  // kSlack: probabilities are exp2(s sl2 - mref) <= 2^kSlack, and acc and
+  // lsum share mref, so O = acc / lsum is unchanged by where mref sits.
+  constexpr float kSlack = 8.f;
+  float mref = -INFINITY, lsum = 0.f;
 
   const int kend = min(T, qb * 128 + 128);
   const int wave_kend = min(T, q0 + 32);
@@ -188,29 +193,36 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
       f32x16v s = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
-      float mx = -INFINITY;
+      // Only the sub-tile on the diagonal (kb == q0) holds keys after a
+      // query or past T; every earlier one is fully visible.
+      if (kb + 31 > q0) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb + acc_row(r, g);
-        const float v = (key <= tq && key < T) ? s[r] * sl2 : -INFINITY;
-        s[r] = v;
-        mx = fmaxf(mx, v);
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb + acc_row(r, g);
+          if (key > tq || key >= T) s[r] = -INFINITY;
+        }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m, mx);
-      const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
-      lsum *= alpha;
+      float mx = s[0];
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
+      if (__any(mx > mref + kSlack)) {
+        // the first sub-tile always lands here (mref = -inf; every row sees key 0)
+        const float mn = mx > mref + kSlack ? mx : mref;
+        const float alpha = __builtin_amdgcn_exp2f(mref - mn);
+        lsum *= alpha;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+        mref = mn;
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = (mn == -INFINITY) ? 0.f : exp2f(s[r] - mn);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -mref));
         s[r] = p;
         lsum += p;
       }
-      m = mn;
       const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
@@ -232,7 +244,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
         for (int j = 0; j < 4; ++j) o[j] = static_cast<bf16>(acc[t][4 * r4 + j] * inv);
         *reinterpret_cast<bf16x4v*>(orow + 32 * t + 8 * r4 + 4 * g) = o;
       }
-    if (g == 0) lse[((int64_t)b * H + h) * T + tq] = (m + log2f(l)) * 0.6931471805599453f;
+    if (g == 0) lse[((int64_t)b * H + h) * T + tq] = (mref + log2f(l)) * 0.6931471805599453f;
   }
 }
 
@@ -302,12 +314,15 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
         s = mfma32(frag_rows<HD>(sQ, 32 * sub + c, kk, g), kf[kk], s);
         dp = mfma32(frag_rows<HD>(sdO, 32 * sub + c, kk, g), vf[kk], dp);
       }
-      // s[r] = S[query qs + acc_row(r, g)][key]
+      // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
+      // Q and dO rows and zero L and D, so they add nothing; only the
+      // diagonal sub-tile (qs == kw) has queries before this wave's keys.
+      const bool diag = qs < kw + 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qr = 32 * sub + acc_row(r, g);
-        const int tq = q0 + qr;
-        const float p = (tq < T && key <= tq && key < T) ? exp2f(s[r] * sl2 - sL[qr]) : 0.f;
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -sL[qr]));
+        if (diag && key > q0 + qr) p = 0.f;
         s[r] = p;
         dp[r] = p * (dp[r] - sD[qr]);
       }
@@ -397,11 +412,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
         s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
         dp = mfma32(frag_rows<HD>(sV, 32 * sub + c, kk, g), of[kk], dp);
       }
-      // s[r] = S^T[key kb + acc_row(r, g)][query tq]
+      // s[r] = S^T[key kb + acc_row(r, g)][query tq].  Keys past T have
+      // zero K and V rows (dS there multiplies a zero K row); only the
+      // diagonal sub-tile (kb == q0) has keys after a query.
+      const bool diag = kb + 31 > q0;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int k = kb + acc_row(r, g);
-        const float p = (tq < T && k <= tq && k < T) ? exp2f(s[r] * sl2 - L2) : 0.f;
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -L2));
+        if (diag && kb + acc_row(r, g) > tq) p = 0.f;
         dp[r] = p * (dp[r] - Dq);
       }
       const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
