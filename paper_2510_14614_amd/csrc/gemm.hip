@@ -604,7 +604,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_mfma(GemmGroup g, in
 // land as zeros; k past K inside a k-contiguous row is pointed out of range.
 namespace pipe {
 constexpr int KS = 32;
-constexpr int NS = 4;                       // LDS stages
 constexpr uint32_t kOob = 0x80000000u;      // offset beyond any buffer range (ranges are < 2^31)
 
 __device__ __forceinline__ int mn_g(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
@@ -739,18 +738,35 @@ __device__ __forceinline__ void bar() {
 }
 }  // namespace pipe
 
-template <int AK, int BKM, int BM, int BN, int OCC>
+template <int AK, int BKM, int BM, int BN, int OCC, int NS>
 __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu_tanh) {
   using namespace pipe;
+  static_assert(NS >= 4 && NS <= 8, "stage count");
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int FM = WTM / 16, FN = WTN / 16;
   typedef Src<BM, AK> SA;
   typedef Src<BN, BKM> SB;
   constexpr int SBYTES = SA::BYTES + SB::BYTES;
   constexpr int L = SA::IPW + SB::IPW;  // loads per wavefront per slice
-  static_assert(2 * L <= 63, "vmcnt range");
+  static_assert(L * (NS - 2) <= 63, "vmcnt range");
   // one array per stage: the compiler tracks buffer-to-LDS loads per array
-  __shared__ __attribute__((aligned(1024))) char st0[SBYTES], st1[SBYTES], st2[SBYTES], st3[SBYTES];
+  // (arrays past NS are 16-byte placeholders)
+  constexpr int SB4 = NS > 4 ? SBYTES : 16, SB5 = NS > 5 ? SBYTES : 16, SB6 = NS > 6 ? SBYTES : 16,
+                SB7 = NS > 7 ? SBYTES : 16;
+  __shared__ __attribute__((aligned(1024))) char st0[SBYTES], st1[SBYTES], st2[SBYTES], st3[SBYTES], st4[SB4],
+      st5[SB5], st6[SB6], st7[SB7];
+  auto stage_ptr = [&](int k) -> char* {
+    switch (k) {
+      case 0: return st0;
+      case 1: return st1;
+      case 2: return st2;
+      case 3: return st3;
+      case 4: return st4;
+      case 5: return st5;
+      case 6: return st6;
+      default: return st7;
+    }
+  };
 
 #if FAL_GEMM_REMAP
   const int bid = xcd_remap(blockIdx.x, g.total_tiles);
@@ -879,37 +895,34 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
   constexpr int LGK = FM * RA < 15 ? FM * RA : 15;
 
   if (n > 0) {
-    // prologue: slices sbeg .. sbeg+2 into stages 0..2; slice sbeg's fragments
-    issue(st0, sbeg);
-    issue(st1, sbeg + 1);
-    issue(st2, sbeg + 2);
-    FAL_WAITCNT(2 * L, 0);
+    // prologue: slices sbeg .. sbeg+NS-2 into stages 0..NS-2; slice sbeg's fragments
+#pragma unroll
+    for (int k = 0; k < NS - 1; ++k) issue(stage_ptr(k), sbeg + k);
+    FAL_WAITCNT(L * (NS - 2), 0);
     bar();
     read(st0, 0);
     // step s: wait for own loads of slice s + 1 and own reads of slice s - 1,
     // barrier (slice s + 1 complete in LDS; slice s - 1's stage free), load
-    // slice s + 3 into that stage, MFMAs of slice s with slice s + 1's reads.
-#define FAL_PIPE_STEP(U, NXT, PRV)                 \
-  {                                                \
-    const int s = t + U;                           \
-    FAL_WAITCNT(L, LGK);                           \
-    bar();                                         \
-    __builtin_amdgcn_sched_barrier(0);             \
-    issue(PRV, s + 3);                             \
-    step(NXT, U & 1);                              \
-    interleave();                                  \
-    __builtin_amdgcn_sched_barrier(0);             \
-  }
-    // The slice count is rounded up to whole groups of NS: slices past the
-    // end load zeros in both operands and add nothing.
-    const int tend = sbeg + ((n + NS - 1) / NS) * NS;
-    for (int t = sbeg; t < tend; t += NS) {
-      FAL_PIPE_STEP(0, st1, st3)
-      FAL_PIPE_STEP(1, st2, st0)
-      FAL_PIPE_STEP(2, st3, st1)
-      FAL_PIPE_STEP(3, st0, st2)
+    // slice s + NS - 1 into that stage, MFMAs of slice s with slice s + 1's
+    // reads.  Unrolled over a whole number of stage cycles and register
+    // buffer pairs, so every stage and buffer index is a constant.
+    constexpr int UNR = NS % 2 ? 2 * NS : NS;
+    // The slice count is rounded up to whole unrolled groups: slices past
+    // the end load zeros in both operands and add nothing.
+    const int tend = sbeg + ((n + UNR - 1) / UNR) * UNR;
+    for (int t = sbeg; t < tend; t += UNR) {
+#pragma unroll
+      for (int U = 0; U < UNR; ++U) {
+        const int s = t + U;
+        FAL_WAITCNT(L * (NS - 3), LGK);
+        bar();
+        __builtin_amdgcn_sched_barrier(0);
+        issue(stage_ptr((U + NS - 1) % NS), s + NS - 1);
+        step(stage_ptr((U + 1) % NS), U & 1);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-#undef FAL_PIPE_STEP
   }
   // every load (including those past the end) has landed and every
   // wavefront is done with the stages before they are reused for staging
@@ -1175,16 +1188,19 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     }
     g.total_tiles = total;
     const dim3 grid(total), block(256);
-#define FAL_PIPE_LAUNCH(BM, BN, OCC)                                                                           \
-  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh); \
-  else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
-  else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<0, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
-  else hipLaunchKernelGGL((gemm_bf16_pipe<0, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);
+#define FAL_PIPE_LAUNCH(BM, BN, OCC, NS)                                                                           \
+  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 1, BM, BN, OCC, NS>), grid, block, 0, s, g, gelu_tanh); \
+  else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 0, BM, BN, OCC, NS>), grid, block, 0, s, g, gelu_tanh);      \
+  else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<0, 1, BM, BN, OCC, NS>), grid, block, 0, s, g, gelu_tanh);      \
+  else hipLaunchKernelGGL((gemm_bf16_pipe<0, 0, BM, BN, OCC, NS>), grid, block, 0, s, g, gelu_tanh);
+    // Four LDS stages (a three-slice load lead).  Deeper rings (five stages
+    // at 128 x 128, six at 256 x 128) measured no faster with operands
+    // coming from HBM and slightly slower with them in cache.
     switch (shape) {
-      case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1) break;
-      case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1) break;
-      case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1) break;
-      default: FAL_PIPE_LAUNCH(128, 128, 2) break;
+      case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1, 4) break;
+      case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1, 4) break;
+      case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1, 4) break;
+      default: FAL_PIPE_LAUNCH(128, 128, 2, 4) break;
     }
 #undef FAL_PIPE_LAUNCH
     return launch_reduce();

@@ -12,6 +12,8 @@
 //  * col_sum_batch: bias gradients, up to four matrices per pair of launches.
 // All of these are HBM-bound; rows are read with 64 consecutive elements
 // per wavefront instruction.
+#include <initializer_list>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -262,6 +264,197 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float* A, const flo
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same row kernels with 4-element chunks per lane (16-byte fp32 and
+// 8-byte bf16 accesses): lane l owns chunks l, l + 64, ... of its row.  Used
+// when d is a multiple of 4 and every row and parameter pointer is aligned
+// to its chunk; the scalar kernels above serve the rest.
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+template <typename S> __device__ __forceinline__ float4 ld4s(const S* p);
+template <> __device__ __forceinline__ float4 ld4s<float>(const float* p) { return ld4(p); }
+template <> __device__ __forceinline__ float4 ld4s<bf16>(const bf16* p) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u), __uint_as_float(w.y << 16),
+                     __uint_as_float(w.y & 0xFFFF0000u));
+}
+template <typename S> __device__ __forceinline__ void st4s(S* p, float4 v);
+template <> __device__ __forceinline__ void st4s<float>(float* p, float4 v) { st4(p, v); }
+template <> __device__ __forceinline__ void st4s<bf16>(bf16* p, float4 v) {
+  union { bf16 h[4]; uint2 w; } u;
+  u.h[0] = from_f<bf16>(v.x); u.h[1] = from_f<bf16>(v.y); u.h[2] = from_f<bf16>(v.z); u.h[3] = from_f<bf16>(v.w);
+  *reinterpret_cast<uint2*>(p) = u.w;
+}
+__device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); }
+__device__ __forceinline__ float4 operator+(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float4 operator-(float4 a, float4 b) { return make_float4(a.x - b.x, a.y - b.y, a.z - b.z, a.w - b.w); }
+__device__ __forceinline__ float4 operator*(float4 a, float4 b) { return make_float4(a.x * b.x, a.y * b.y, a.z * b.z, a.w * b.w); }
+__device__ __forceinline__ float hsum(float4 a) { return (a.x + a.y) + (a.z + a.w); }
+
+template <typename S, int NC>
+__global__ __launch_bounds__(256) void ln_fwd_v4(LnFwdArgs a) {
+  const int row = blockIdx.x * kRowsPerBlock + threadIdx.x / FAL_WAVE;
+  const int lane = threadIdx.x % FAL_WAVE;
+  if (row >= a.M) return;
+  const int d = a.d;
+  const int64_t off = (int64_t)row * d;
+  float4 v[NC];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    v[i] = j < d ? ld4(a.x + off + j) : f4(0.f);
+    s += hsum(v[i]);
+  }
+  const float mean = wave_sum(s) / d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    if (j < d) {
+      const float4 c = v[i] - f4(mean);
+      q += hsum(c * c);
+    }
+  }
+  const float var = wave_sum(q) / d;
+  const float rstd = 1.f / sqrtf(var + a.eps);
+  if (lane == 0) {
+    if (a.mean) a.mean[row] = mean;
+    if (a.rstd) a.rstd[row] = rstd;
+  }
+  const S* g1 = static_cast<const S*>(a.g1);
+  const S* b1 = static_cast<const S*>(a.b1);
+  const S* g2 = static_cast<const S*>(a.g2);
+  const S* b2 = static_cast<const S*>(a.b2);
+  const S* add2 = static_cast<const S*>(a.add2);
+  const S* xF = static_cast<const S*>(a.xhatF);
+  const S* gF = static_cast<const S*>(a.gF);
+  const S* bF = static_cast<const S*>(a.bF);
+  S* y1 = static_cast<S*>(a.y1);
+  S* y2 = static_cast<S*>(a.y2);
+  S* xo = static_cast<S*>(a.xhat_out);
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    if (j >= d) break;
+    const float4 xh = (v[i] - f4(mean)) * f4(rstd);
+    if (y1) st4s<S>(y1 + off + j, xh * ld4s<S>(g1 + j) + ld4s<S>(b1 + j));
+    if (y2) {
+      float4 o = xh * ld4s<S>(g2 + j) + ld4s<S>(b2 + j);
+      if (add2) o = o + ld4s<S>(add2 + off + j);
+      if (xF) o = o + (ld4s<S>(gF + j) * ld4s<S>(xF + off + j) + ld4s<S>(bF + j));
+      st4s<S>(y2 + off + j, o);
+    }
+    if (xo) st4s<S>(xo + off + j, xh);
+  }
+}
+
+template <typename S, int NC>
+__global__ __launch_bounds__(256) void ln_bwd_v4(LnBwdArgs a) {
+  const int row = blockIdx.x * kRowsPerBlock + threadIdx.x / FAL_WAVE;
+  const int lane = threadIdx.x % FAL_WAVE;
+  if (row >= a.M) return;
+  const int d = a.d;
+  const int64_t off = (int64_t)row * d;
+  const float mean = a.mean[row], rstd = a.rstd[row];
+  const S* g1 = static_cast<const S*>(a.g1);
+  const S* g2 = static_cast<const S*>(a.g2);
+  const S* gF = static_cast<const S*>(a.gF);
+  float4 xh[NC], dxh[NC];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    xh[i] = f4(0.f);
+    dxh[i] = f4(0.f);
+    if (j < d) {
+      xh[i] = (ld4(a.x + off + j) - f4(mean)) * f4(rstd);
+      float4 t = f4(0.f);
+      if (a.dy1) t = t + ld4(a.dy1 + off + j) * ld4s<S>(g1 + j);
+      if (a.dy2) {
+        const float4 dy2 = ld4(a.dy2 + off + j);
+        t = t + dy2 * ld4s<S>(g2 + j);
+        if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? dy2 : ld4(a.dacc + off + j) + dy2);
+        if (a.dxhatF_acc) {
+          const float4 c = ld4s<S>(gF + j) * dy2;
+          st4(a.dxhatF_acc + off + j, a.dxhatF_overwrite ? c : ld4(a.dxhatF_acc + off + j) + c);
+        }
+      }
+      dxh[i] = t;
+      s1 += hsum(t);
+      s2 += hsum(t * xh[i]);
+    }
+  }
+  s1 = wave_sum(s1) / d;
+  s2 = wave_sum(s2) / d;
+  S* lp = static_cast<S*>(a.dx_lp);
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    if (j >= d) break;
+    float4 dx = f4(rstd) * (dxh[i] - f4(s1) - xh[i] * f4(s2));
+    if (a.dres) dx = dx + ld4(a.dres + off + j);
+    st4(a.dx + off + j, dx);
+    if (lp) st4s<S>(lp + off + j, dx);
+  }
+}
+
+template <int NC>
+__global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* mean, const float* rstd,
+                                                  const float* dxhat, int M, int d, float* da, int accumulate) {
+  const int row = blockIdx.x * kRowsPerBlock + threadIdx.x / FAL_WAVE;
+  const int lane = threadIdx.x % FAL_WAVE;
+  if (row >= M) return;
+  const int64_t off = (int64_t)row * d;
+  const float mu = mean[row], rs = rstd[row];
+  float4 xh[NC], g[NC];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    xh[i] = f4(0.f);
+    g[i] = f4(0.f);
+    if (j < d) {
+      xh[i] = (ld4(A + off + j) - f4(mu)) * f4(rs);
+      g[i] = ld4(dxhat + off + j);
+      s1 += hsum(g[i]);
+      s2 += hsum(g[i] * xh[i]);
+    }
+  }
+  s1 = wave_sum(s1) / d;
+  s2 = wave_sum(s2) / d;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    if (j >= d) break;
+    const float4 v = f4(rs) * (g[i] - f4(s1) - xh[i] * f4(s2));
+    st4(da + off + j, accumulate ? ld4(da + off + j) + v : v);
+  }
+}
+
+// Chunks of 4 per lane for width d (a multiple of 4), 0 if too wide.
+template <typename F>
+static hipError_t dispatch_nc(int d, F&& f) {
+  if (d <= 256) return f(std::integral_constant<int, 1>{});
+  if (d <= 512) return f(std::integral_constant<int, 2>{});
+  if (d <= 768) return f(std::integral_constant<int, 3>{});
+  if (d <= 1024) return f(std::integral_constant<int, 4>{});
+  if (d <= 2048) return f(std::integral_constant<int, 8>{});
+  if (d <= 4096) return f(std::integral_constant<int, 16>{});
+  return hipErrorInvalidValue;
+}
+static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+static bool al8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0; }
+// fp32 row pointers 16-byte aligned, dtype ones 8-byte (4 bf16) or 16-byte (4 fp32); NULL passes
+static bool vec_ok(DType dt, int d, std::initializer_list<const void*> f32, std::initializer_list<const void*> lp) {
+  if (d % 4) return false;
+  for (const void* p : f32)
+    if (p && !al16(p)) return false;
+  for (const void* p : lp)
+    if (p && !(dt == BF16 ? al8(p) : al16(p))) return false;
+  return true;
+}
+
 template <typename F>
 static hipError_t dispatch_vpt(int d, F&& f) {
   if (d <= 64) return f(std::integral_constant<int, 1>{});
@@ -276,6 +469,13 @@ static hipError_t dispatch_vpt(int d, F&& f) {
 
 hipError_t ln_fwd(DType dt, const LnFwdArgs& a, hipStream_t s) {
   const dim3 grid(cdiv(a.M, kRowsPerBlock)), block(256);
+  if (vec_ok(dt, a.d, {a.x}, {a.g1, a.b1, a.y1, a.g2, a.b2, a.y2, a.add2, a.xhatF, a.gF, a.bF, a.xhat_out}))
+    return dispatch_nc(a.d, [&](auto nc) {
+      constexpr int C = decltype(nc)::value;
+      if (dt == BF16) hipLaunchKernelGGL((ln_fwd_v4<bf16, C>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((ln_fwd_v4<float, C>), grid, block, 0, s, a);
+      return hipGetLastError();
+    });
   return dispatch_vpt(a.d, [&](auto vpt) {
     constexpr int V = decltype(vpt)::value;
     if (dt == BF16) hipLaunchKernelGGL((ln_fwd_kernel<bf16, V>), grid, block, 0, s, a);
@@ -288,12 +488,21 @@ int64_t ln_bwd_scratch(int M, int d) { return (int64_t)cdiv(M, kPartRows) * 6 * 
 
 hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   const dim3 grid(cdiv(a.M, kRowsPerBlock)), block(256);
-  hipError_t e = dispatch_vpt(a.d, [&](auto vpt) {
-    constexpr int V = decltype(vpt)::value;
-    if (dt == BF16) hipLaunchKernelGGL((ln_bwd_rows<bf16, V>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((ln_bwd_rows<float, V>), grid, block, 0, s, a);
-    return hipGetLastError();
-  });
+  hipError_t e;
+  if (vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc}, {a.g1, a.g2, a.gF, a.dx_lp}))
+    e = dispatch_nc(a.d, [&](auto nc) {
+      constexpr int C = decltype(nc)::value;
+      if (dt == BF16) hipLaunchKernelGGL((ln_bwd_v4<bf16, C>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((ln_bwd_v4<float, C>), grid, block, 0, s, a);
+      return hipGetLastError();
+    });
+  else
+    e = dispatch_vpt(a.d, [&](auto vpt) {
+      constexpr int V = decltype(vpt)::value;
+      if (dt == BF16) hipLaunchKernelGGL((ln_bwd_rows<bf16, V>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((ln_bwd_rows<float, V>), grid, block, 0, s, a);
+      return hipGetLastError();
+    });
   if (e != hipSuccess) return e;
   const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
   if (!any) return hipSuccess;
@@ -315,6 +524,12 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
 hipError_t norm_bwd(const float* A, const float* mean, const float* rstd, const float* dxhat, int M,
                     int d, float* da, int accumulate, hipStream_t s) {
   const dim3 grid(cdiv(M, kRowsPerBlock)), block(256);
+  if (vec_ok(F32, d, {A, dxhat, da}, {}))
+    return dispatch_nc(d, [&](auto nc) {
+      constexpr int C = decltype(nc)::value;
+      hipLaunchKernelGGL((norm_bwd_v4<C>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, da, accumulate);
+      return hipGetLastError();
+    });
   return dispatch_vpt(d, [&](auto vpt) {
     constexpr int V = decltype(vpt)::value;
     hipLaunchKernelGGL((norm_bwd_kernel<V>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, da, accumulate);
