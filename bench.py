@@ -40,7 +40,7 @@ METRIC = "training tokens/s on 1 MI355X (FAL vs GPT baseline); MFMA util % of bf
 # Measured HBM traffic of the GEMM calls of the default workload (rocprofv3
 # FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy); valid only while the
 # sources it was measured on are unchanged.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_mfma_gpt2-small_traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_gpt2-small_traffic.md")
 TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h")
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
