@@ -426,6 +426,9 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
 #ifndef FAL_GEMM_PIPE
 #define FAL_GEMM_PIPE 1
 #endif
+#ifndef FAL_GEMM_DBL
+#define FAL_GEMM_DBL 1
+#endif
 #ifndef FAL_GEMM_REMAP
 #define FAL_GEMM_REMAP 1
 #endif
@@ -613,16 +616,26 @@ __device__ __forceinline__ lds_void_t* lds_ptr(const void* p) {
   return (lds_void_t*)((__attribute__((address_space(3))) char*)(const_cast<void*>(p)));
 }
 
-// One operand's loader (both K segments).  Load block i of this wavefront
-// is block 4 i + wave of the stage region; its global offset is a per-lane
-// part (which repeats with period NV in i) plus a wave-uniform step per i.
-template <int R, int KMAJ>
+// One operand's loader (both K segments) for slices W wide in K (32 or
+// 64).  Load block i of this wavefront is block 4 i + wave of the stage
+// region; its global offset is a per-lane part (which repeats with period
+// NV in i) plus a wave-uniform step per i.
+//  * k-contiguous: a block holds RPI = 1024 / 2W rows of W k; the 16-byte
+//    chunk c of row r sits at c ^ kswz(r), kswz(r) = (r >> 2) & 3 for
+//    64-byte rows and (r >> 1) & 7 for 128-byte rows.
+//  * MN-major: a block holds 1024 / 2R k-rows of R elements, 32-byte
+//    segment q of k-row k at q ^ g(k).
+template <int W>
+__device__ __forceinline__ int kswz(int r) { return W == 32 ? (r >> 2) & 3 : (r >> 1) & 7; }
+
+template <int R, int KMAJ, int W = KS>
 struct Src {
-  static constexpr int BYTES = R * KS * 2;                 // one stage region
+  static constexpr int BYTES = R * W * 2;                  // one stage region
   static constexpr int NINS = BYTES / 1024;                // 1 KiB load blocks per slice
   static constexpr int IPW = NINS / 4;                     // per wavefront
   static constexpr int CPR = R / 8;                        // MN-major: 16-byte chunks per k-row
-  static constexpr int RPI = KMAJ ? 16 : 1024 / (2 * R);   // rows / k-rows per block
+  static constexpr int CPRK = W / 8;                       // k-contiguous: 16-byte chunks per row
+  static constexpr int RPI = KMAJ ? 1024 / (2 * W) : 1024 / (2 * R);  // rows / k-rows per block
   // MN-major: the swizzle g(k) of a lane's k-row repeats every 16 k-rows
   static constexpr int NV = KMAJ ? 1 : ((4 * RPI) % 16 == 0 ? 1 : 16 / (4 * RPI));
   static_assert(NINS % 4 == 0 && IPW % NV == 0, "tile too small for four wavefronts");
@@ -641,8 +654,9 @@ struct Src {
     kstep[seg] = KMAJ ? 2u : (uint32_t)(ld * 2);
     istep[seg] = (uint32_t)(4 * RPI * ld * 2);
     if (KMAJ) {
-      const int row = wave * 16 + (lane >> 2);
-      const int gc = (lane & 3) ^ ((row >> 2) & 3);
+      // kswz(row) does not depend on the block index i (rows advance by 4 RPI)
+      const int row = wave * RPI + lane / CPRK;
+      const int gc = (lane % CPRK) ^ kswz<W>(row);
       voff[seg][0] = (uint32_t)(((int64_t)row * ld + gc * 8) * 2);
       kof = gc * 8;
     } else {
@@ -670,7 +684,7 @@ struct Src {
   uint32_t vo[NV];
   // Point the state at the slice at k0 of segment seg; chunks at slice
   // offset >= lim are pointed out of range (lim: 0 for a slice past the
-  // end, K - k0 in a k-contiguous tail slice, KS otherwise).
+  // end, K - k0 in a k-contiguous tail slice, W otherwise).
   __device__ __forceinline__ void set(int seg, int k0, int lim) {
     const uint64_t b = seg ? base[1] : base[0];
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
@@ -686,7 +700,7 @@ struct Src {
     for (int v = 0; v < NV; ++v) vo[v] = bad ? kOob : (seg ? voff[1][v] : voff[0][v]);
   }
   // Next slice of the same segment (full and live).
-  __device__ __forceinline__ void advance() { so += KS * ks; }
+  __device__ __forceinline__ void advance() { so += W * ks; }
   // Issue this wavefront's loads of the current slice into the region at dst.
   __device__ __forceinline__ void load(char* dst, int wave) const {
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -702,14 +716,19 @@ struct Src {
   }
 };
 
-// Fragment reads from one stage region (byte addresses precomputed per lane).
-template <int R, int KMAJ, int NF>
+// Fragment reads from one stage region (byte addresses precomputed per
+// lane); fragment f of MFMA k-step kk (0 .. W/32 - 1).
+template <int R, int KMAJ, int NF, int W = KS>
 struct Frag {
-  uint32_t off[KMAJ ? 1 : NF];
+  static constexpr int NKK = W / 32;
+  uint32_t off[KMAJ ? NKK : NF];
   // row0: first row of fragment 0 within the region (the wavefront tile's base)
   __device__ __forceinline__ void init(int row0, int lane) {
     if (KMAJ) {
-      off[0] = (uint32_t)((row0 + (lane & 15)) * 64 + ((((lane >> 4) ^ ((lane >> 2) & 3))) << 4));
+      const int row = row0 + (lane & 15);
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        off[kk] = (uint32_t)(row * 2 * W + ((((4 * kk + (lane >> 4)) ^ kswz<W>(row))) << 4));
     } else {
       const int k = 8 * (lane >> 4) + ((lane & 15) >> 2);
       const int g2 = 2 * mn_g(k);
@@ -720,9 +739,9 @@ struct Frag {
       }
     }
   }
-  __device__ __forceinline__ bf16x8_t read(const char* region, int f) const {
-    if (KMAJ) return *reinterpret_cast<const bf16x8_t*>(region + off[0] + f * 16 * 64);
-    const bf16* p = reinterpret_cast<const bf16*>(region + off[f]);
+  __device__ __forceinline__ bf16x8_t read(const char* region, int f, int kk = 0) const {
+    if (KMAJ) return *reinterpret_cast<const bf16x8_t*>(region + off[kk] + f * 16 * 2 * W);
+    const bf16* p = reinterpret_cast<const bf16*>(region + off[f]) + kk * 32 * R;
     const i16x4_t lo = lds_read_tr(p), hi = lds_read_tr(p + 4 * R);
     const i16x4_t v8[2] = {lo, hi};
     return *reinterpret_cast<const bf16x8_t*>(v8);
@@ -922,6 +941,193 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
         interleave();
         __builtin_amdgcn_sched_barrier(0);
       }
+    }
+  }
+  // every load (including those past the end) has landed and every
+  // wavefront is done with the stages before they are reused for staging
+  FAL_WAITCNT(0, 0);
+  bar();
+
+  float* stage = reinterpret_cast<float*>(wm ? st1 : st0) + wn * 16 * (WTN + 4);
+  static_assert(2 * 16 * (WTN + 4) * 4 <= SBYTES, "epilogue staging exceeds a stage");
+  const int mw = m0 + wm * WTM, nw = n0 + wn * WTN;
+  if (P.splits > 1) {
+    GemmProblem Q = P;
+    Q.out = P.part + (int64_t)split * P.M * P.N;
+    Q.ldo = P.N;
+    Q.bias = Q.bias2 = nullptr;
+    Q.vec_out = (P.N & 3) == 0;
+    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    return;
+  }
+  switch (P.epi) {
+    case EPI_STORE:
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+  }
+}
+
+// The same tile shapes with 64-wide K slices in two LDS stages.  A
+// k-contiguous operand then arrives as whole 128-byte lines per row (a
+// 32-wide slice takes half a line from twice as many rows per load, which
+// measured slow with operands coming from HBM).  Step s: wait for own
+// loads of slice s + 1 and own fragment reads of slice s, barrier, refill
+// slice s's stage with slice s + 2, then the MFMAs of slice s with every
+// fragment read of slice s + 1 issued among the first of them.  The load
+// lead is one step (two MFMA k-steps), the same time as the three-slice
+// lead of the four-stage kernel.
+template <int AK, int BKM, int BM, int BN, int OCC>
+__global__ __launch_bounds__(256, OCC) void gemm_bf16_dbl(GemmGroup g, int gelu_tanh) {
+  using namespace pipe;
+  constexpr int W = 64, NKK = W / 32;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  typedef Src<BM, AK, W> SA;
+  typedef Src<BN, BKM, W> SB;
+  constexpr int SBYTES = SA::BYTES + SB::BYTES;
+  constexpr int L = SA::IPW + SB::IPW;  // loads per wavefront per slice
+  static_assert(L <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char st0[SBYTES], st1[SBYTES];
+
+#if FAL_GEMM_REMAP
+  const int bid = xcd_remap(blockIdx.x, g.total_tiles);
+#else
+  const int bid = blockIdx.x;
+#endif
+  const GemmProblem P = find_problem(g, bid);
+  const int per_split = P.tiles_m * P.tiles_n;
+  const int local = (bid - P.tile_start) % per_split;
+  const int split = (bid - P.tile_start) / per_split;
+  int tmi, tni;
+  grouped_tile(local, P.tiles_m, P.tiles_n, tmi, tni);
+  const int m0 = tmi * BM, n0 = tni * BN;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // slices of W: segment 0 is [0, nt1), segment 1 is [nt1, nt)
+  const int nt1 = (P.K + W - 1) / W;
+  int sbeg = 0, send = nt1 + (P.K2 > 0 ? (P.K2 + W - 1) / W : 0);
+  if (P.splits > 1) {
+    const int per = (nt1 + P.splits - 1) / P.splits;
+    sbeg = min(nt1, split * per);
+    send = min(nt1, sbeg + per);
+  }
+  const int n = send - sbeg;
+
+  SA sa;
+  SB sb;
+  sa.init(0, static_cast<const bf16*>(P.A), P.lda, m0, P.M, P.K, wave, lane);
+  sb.init(0, static_cast<const bf16*>(P.B), P.ldb, n0, P.N, P.K, wave, lane);
+  if (P.K2 > 0) {
+    sa.init(1, static_cast<const bf16*>(P.A2), P.lda2, m0, P.M, P.K2, wave, lane);
+    sb.init(1, static_cast<const bf16*>(P.B2), P.ldb2, n0, P.N, P.K2, wave, lane);
+  } else {  // never selected; an empty range all the same
+    sa.clear(1);
+    sb.clear(1);
+  }
+  int f_lo = 0, f_hi = 0;
+  const int full0 = P.K / W, full1 = nt1 + P.K2 / W;
+  auto issue = [&](char* stage, int s) {
+    if (s > f_lo && s < f_hi) {
+      sa.advance();
+      sb.advance();
+    } else {
+      // slices past the end use segment 0 at k 0 with every chunk out of range
+      const bool live = s < send;
+      const int seg = live && s >= nt1 ? 1 : 0;
+      const int k0 = live ? (seg ? s - nt1 : s) * W : 0;
+      const int Kseg = seg ? P.K2 : P.K;
+      // k-contiguous operands read whole 8-element chunks up to Kpad
+      const int Kpad = P.kpad ? (Kseg + 7) / 8 * 8 : Kseg;
+      const int lim = !live ? 0 : k0 + W > Kpad ? Kpad - k0 : W;
+      sa.set(seg, k0, AK ? lim : (live ? W : 0));
+      sb.set(seg, k0, BKM ? lim : (live ? W : 0));
+      f_lo = s;
+      f_hi = live && k0 + W <= Kseg ? min(send, seg ? full1 : full0) : s;
+    }
+    sa.load(stage, wave);
+    sb.load(stage + SA::BYTES, wave);
+  };
+
+  Frag<BM, AK, FM, W> fa;
+  Frag<BN, BKM, FN, W> fb;
+  fa.init(wm * WTM, lane);
+  fb.init(wn * WTN, lane);
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  bf16x8_t ra[2][NKK][FM], rb[2][NKK][FN];
+  auto read = [&](const char* stage, int buf) {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) rb[buf][kk][j] = fb.read(stage + SA::BYTES, j, kk);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) ra[buf][kk][i] = fa.read(stage, i, kk);
+    }
+  };
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[buf][kk][i], rb[buf][kk][j], acc[i][j], 0, 0, 0);
+  };
+  // Issue order inside a step: one fragment read after each of the first
+  // MFMAs, the loads spread over the rest.
+  constexpr int NRD = NKK * ((AK ? FM : 2 * FM) + (BKM ? FN : 2 * FN));
+  constexpr int NMF = NKK * FM * FN;
+  constexpr int DMA_EVERY = (NMF - NRD) / L > 0 ? (NMF - NRD) / L : 1;
+  static_assert(NRD <= NMF, "more fragment reads than MFMAs");
+  auto interleave = [&]() {
+    int dma = 0;
+#pragma unroll
+    for (int q = 0; q < NMF; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if (q < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      else if ((q - NRD) % DMA_EVERY == 0 && dma < L) {
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // buffer load to LDS
+        ++dma;
+      }
+    }
+  };
+
+  if (n > 0) {
+    issue(st0, sbeg);
+    issue(st1, sbeg + 1);
+    FAL_WAITCNT(L, 0);
+    bar();
+    read(st0, 0);
+    // The slice count is rounded up to whole pairs: slices past the end
+    // load zeros in both operands and add nothing.
+    const int tend = sbeg + ((n + 1) / 2) * 2;
+    for (int t = sbeg; t < tend; t += 2) {
+      FAL_WAITCNT(0, 0);
+      bar();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(st0, t + 2);
+      read(st1, 1);
+      mma(0);
+      interleave();
+      __builtin_amdgcn_sched_barrier(0);
+      FAL_WAITCNT(0, 0);
+      bar();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(st1, t + 3);
+      read(st0, 0);
+      mma(1);
+      interleave();
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   // every load (including those past the end) has landed and every
@@ -1196,12 +1402,26 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     // Four LDS stages (a three-slice load lead).  Deeper rings (five stages
     // at 128 x 128, six at 256 x 128) measured no faster with operands
     // coming from HBM and slightly slower with them in cache.
-    switch (shape) {
-      case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1, 4) break;
-      case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1, 4) break;
-      case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1, 4) break;
-      default: FAL_PIPE_LAUNCH(128, 128, 2, 4) break;
+#define FAL_DBL_LAUNCH(BM, BN, OCC)                                                                           \
+  if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_dbl<1, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh); \
+  else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_dbl<1, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
+  else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_dbl<0, 1, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);      \
+  else hipLaunchKernelGGL((gemm_bf16_dbl<0, 0, BM, BN, OCC>), grid, block, 0, s, g, gelu_tanh);
+    if (FAL_GEMM_DBL && shape != PIPE_256x256) {
+      switch (shape) {
+        case PIPE_256x128: FAL_DBL_LAUNCH(256, 128, 1) break;
+        case PIPE_128x256: FAL_DBL_LAUNCH(128, 256, 1) break;
+        default: FAL_DBL_LAUNCH(128, 128, 2) break;
+      }
+    } else {
+      switch (shape) {
+        case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1, 4) break;
+        case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1, 4) break;
+        case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1, 4) break;
+        default: FAL_PIPE_LAUNCH(128, 128, 2, 4) break;
+      }
     }
+#undef FAL_DBL_LAUNCH
 #undef FAL_PIPE_LAUNCH
     return launch_reduce();
   }
