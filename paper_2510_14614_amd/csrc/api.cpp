@@ -429,11 +429,19 @@ struct Run {
     return ctx->cfg.sched == FAL_SCHED_MERGED || ctx->cfg.sched == FAL_SCHED_STREAMS_MERGED;
   }
 
+  // The block's weights were last read a whole step (or half of one) ago
+  // and have left the caches; streaming them in first lets the block's
+  // GEMMs find them in the last-level cache.
+  void warm_params(const void* bp, hipStream_t s) {
+    FAL_TRY(cache_warm(bp, ctx->Lo.block_stride * (int64_t)ctx->D.es, s));
+  }
+
   void block_fwd(int layer, const void* bp, const float* x, float* y, void* first) {
     const Dims& D = ctx->D;
     const LayerSlot& S = ctx->W.slots[layer];
     const int arch = ctx->cfg.arch;
     hipStream_t sm = ctx->sm;
+    warm_params(bp, sm);
     if (arch == FAL_ARCH_FAL && layer > 0) {
       LnFwdArgs a = lnargs(x, S.mean1, S.rstd1);
       a.g1 = P(bp, FAL_B_LN1_G); a.b1 = P(bp, FAL_B_LN1_B); a.y1 = S.h1;
@@ -617,6 +625,7 @@ struct Run {
     hipStream_t sm = ctx->sm;
     const int64_t Md = (int64_t)D.M * D.d;
     const bool last = layer == D.L - 1;
+    warm_params(bp, sm);
     // first-attention LayerNorm slot: zero unless used by this block
     const bool uses_lnF = (arch == FAL_ARCH_FAL && layer == 0 && (!block1_standard() || D.L > 1)) ||
                           (arch == FAL_ARCH_FALPLUS && layer > 0);

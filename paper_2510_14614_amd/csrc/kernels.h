@@ -209,6 +209,9 @@ int64_t dot_scratch(int64_t n);
 hipError_t add_f32(const float* a, const float* b, float* y, int64_t n, hipStream_t s);
 // Convert fp32 -> dtype.
 hipError_t cast_from_f32(DType dt, const float* x, void* y, int64_t n, hipStream_t s);
+// Read the whole 16-byte chunks of [p, p + bytes) and discard: warms the last-level
+// cache with a read-only operand before the kernels that use it.
+hipError_t cache_warm(const void* p, int64_t bytes, hipStream_t s);
 // Fill fp32 with zero (a kernel, so it can live inside captured graphs).
 hipError_t zero_f32(float* y, int64_t n, hipStream_t s);
 

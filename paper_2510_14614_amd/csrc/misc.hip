@@ -10,6 +10,8 @@
 // many workgroups.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -326,6 +328,28 @@ hipError_t cast_from_f32(DType dt, const float* x, void* y, int64_t n, hipStream
 __global__ void zero_kernel(float* y, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) y[i] = 0.f;
+}
+
+// Reads n16 16-byte chunks and discards them: brings a read-only operand
+// (a block's weights, untouched since the previous step) into the
+// last-level cache ahead of the GEMMs that read it.
+__global__ __launch_bounds__(256) void cache_warm_kernel(const uint4* p, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256) {
+    const uint4 v = p[i];
+    asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
+  }
+}
+
+hipError_t cache_warm(const void* p, int64_t bytes, hipStream_t s) {
+  if (!p || bytes <= 0) return hipSuccess;
+  // whole 16-byte chunks inside [p, p + bytes)
+  const uintptr_t a = (reinterpret_cast<uintptr_t>(p) + 15) & ~static_cast<uintptr_t>(15);
+  const int64_t n16 = ((int64_t)(reinterpret_cast<uintptr_t>(p) + bytes) - (int64_t)a) / 16;
+  if (n16 <= 0) return hipSuccess;
+  p = reinterpret_cast<const void*>(a);
+  const int blocks = (int)std::min<int64_t>(2048, cdiv(n16, 256));
+  hipLaunchKernelGGL(cache_warm_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint4*>(p), n16);
+  return hipGetLastError();
 }
 
 hipError_t zero_f32(float* y, int64_t n, hipStream_t s) {
