@@ -182,7 +182,9 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
  *   tokens  device int32 [B, T+1]; the model reads [:, :T] and predicts
  *           [:, 1:]; ids must lie in [0, V) (out-of-range ids are clamped)
  *   loss    device fp32 scalar: mean next-token cross-entropy over B*T
- *   logits  device fp32 [B*T, V] or NULL to skip writing them
+ *   logits  device fp32 [B*T, V] or NULL to skip writing them; the step
+ *           keeps the logits in the config's dtype (bf16 in bf16 mode, the
+ *           precision of the LM-head product) and widens them here
  *   grads   device fp32, full layout, overwritten */
 fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* tokens,
                             float* loss, float* logits, float* grads);

@@ -153,7 +153,7 @@ struct Work {
   float* resid;                // [L+1][M, d]
   void* hf;
   float *meanf, *rstdf;
-  float* logits;               // [M, Vp]
+  void* logits;                // dtype [M, Vp]
   void* dlogits;               // [M, Vp]
   float* row_loss;
   void* first;                 // dtype [M, d]
@@ -200,7 +200,7 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
     W.hf = cv.take<char>(M * d * es);
     W.meanf = cv.take<float>(M);
     W.rstdf = cv.take<float>(M);
-    W.logits = cv.take<float>(M * D.Vp);
+    W.logits = cv.take<char>(M * D.Vp * es);
     W.dlogits = cv.take<char>(M * D.Vp * es);
     W.row_loss = cv.take<float>(M);
     W.keys = cv.take<int32_t>(embed_bwd_scratch((int)M));
@@ -891,15 +891,15 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       r.ln(a, sm);
     }
     GemmProblem ph = Run::prob(W.hf, D.d, gparam(FAL_P_WTE), D.d, D.M, D.V, D.d);
-    ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.logits; ph.ldo = D.Vp;
+    // logits in the step's dtype (the LM-head product's precision); the
+    // cross-entropy works in fp32 from them
+    ph.epi = EPI_STORE; ph.out_f32 = r.dt == F32; ph.out = W.logits; ph.ldo = D.Vp;
     r.gemm1(1, 1, ph, sm);
     {
-      Span span(ctx, FAL_PROF_CE, sm, 0.0, (double)D.M * (4.0 * D.V + (double)D.es * D.Vp));
+      Span span(ctx, FAL_PROF_CE, sm, 0.0, (double)D.M * (double)D.es * (D.V + D.Vp));
       FAL_TRY(cross_entropy(r.dt, W.logits, D.Vp, tokens, D.B, D.T, D.V, W.dlogits, D.Vp, W.row_loss, loss, sm));
     }
-    if (logits)
-      FAL_TRY(hipMemcpy2DAsync(logits, (size_t)D.V * 4, W.logits, (size_t)D.Vp * 4, (size_t)D.V * 4, D.M,
-                               hipMemcpyDeviceToDevice, sm));
+    if (logits) FAL_TRY(rows_to_f32(r.dt, W.logits, D.Vp, logits, D.V, D.M, D.V, sm));
     // head backward: dHf = dlogits wte ; dwte = dlogits^T Hf
     GemmProblem pd = Run::prob(W.dlogits, D.Vp, gparam(FAL_P_WTE), D.d, D.M, D.d, D.V);
     pd.epi = EPI_STORE; pd.out_f32 = 1; pd.out = W.dh1; pd.ldo = D.d;

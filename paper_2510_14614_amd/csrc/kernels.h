@@ -191,13 +191,17 @@ hipError_t embed_bwd(const int32_t* tokens, int B, int T, int V, int d, const fl
                      hipStream_t s);
 int64_t embed_bwd_scratch(int M);
 
-// Cross-entropy over rows of fp32 logits [M, V] (row stride ldl) with
-// targets tokens[b, t + 1].  Writes dlogits = (softmax - onehot) / M as
-// dtype [M, ldd] (columns V..ldd-1 zeroed) and per-row loss (fp32 [M]);
-// then loss = mean(row_loss) (fp32 scalar, fixed-order reduction).
-hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32_t* tokens, int B,
+// Cross-entropy over rows of logits [M, V] (dtype: fp32 or bf16, row
+// stride ldl) with targets tokens[b, t + 1].  Writes dlogits =
+// (softmax - onehot) / M as dtype [M, ldd] (columns V..ldd-1 zeroed) and
+// per-row loss (fp32 [M]); then loss = mean(row_loss) (fp32 scalar,
+// fixed-order reduction).  Softmax, log-sum-exp and loss are fp32.
+hipError_t cross_entropy(DType dt, const void* logits, int64_t ldl, const int32_t* tokens, int B,
                          int T, int V, void* dlogits, int64_t ldd, float* row_loss, float* loss,
                          hipStream_t s);
+// dst[r, c] = src[r, c] widened to fp32, for r < rows and c < cols.
+hipError_t rows_to_f32(DType dt, const void* src, int64_t lds, float* dst, int64_t ldd, int rows, int cols,
+                       hipStream_t s);
 
 // loss = sum(a * b) over n fp32 elements (fixed-order reduction); scratch of
 // dot_scratch(n) floats.

@@ -173,14 +173,25 @@ __device__ __forceinline__ void lse_combine(float& m1, float& s1, float m2, floa
   m1 = mm;
 }
 
+// four consecutive logits as fp32 (16-byte fp32 or 8-byte bf16 load)
+__device__ __forceinline__ float4 ld4l(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4l(const bf16* p) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u), __uint_as_float(w.y << 16),
+                     __uint_as_float(w.y & 0xFFFF0000u));
+}
+
+// Logits are stored in the step's dtype (bf16 in mixed precision, as the
+// LM-head product produces them); max, log-sum-exp, loss and gradient are
+// fp32.
 template <typename S, int NPT>
-__global__ __launch_bounds__(kCeThreads) void ce_rows(const float* logits, int64_t ldl, const int32_t* tok, int T,
+__global__ __launch_bounds__(kCeThreads) void ce_rows(const S* logits, int64_t ldl, const int32_t* tok, int T,
                                                       int V, float inv_n, S* dl, int64_t ldd, float* row_loss) {
   __shared__ float rm[kCeThreads / FAL_WAVE], rs[kCeThreads / FAL_WAVE];
   const int m = blockIdx.x, b = m / T, t = m % T, tid = threadIdx.x;
   int tgt = tok[(int64_t)b * (T + 1) + t + 1];
   tgt = min(max(tgt, 0), V - 1);
-  const float* l = logits + (int64_t)m * ldl;
+  const S* l = logits + (int64_t)m * ldl;
   const int nv = (V + 3) / 4, nd = (int)(ldd / 4);
   float x[NPT][4];
   float lm = -INFINITY;
@@ -188,7 +199,7 @@ __global__ __launch_bounds__(kCeThreads) void ce_rows(const float* logits, int64
   for (int i = 0; i < NPT; ++i) {
     const int c = tid + kCeThreads * i;
     if (c < nv) {
-      const float4 v = *reinterpret_cast<const float4*>(l + 4 * c);
+      const float4 v = ld4l(l + 4 * c);
       x[i][0] = v.x; x[i][1] = 4 * c + 1 < V ? v.y : -INFINITY;
       x[i][2] = 4 * c + 2 < V ? v.z : -INFINITY; x[i][3] = 4 * c + 3 < V ? v.w : -INFINITY;
     } else {
@@ -216,7 +227,7 @@ __global__ __launch_bounds__(kCeThreads) void ce_rows(const float* logits, int64
 #pragma unroll
   for (int w = 1; w < kCeThreads / FAL_WAVE; ++w) lse_combine(gm, gs, rm[w], rs[w]);
   const float lse = gm + __logf(gs);
-  if (tid == 0) row_loss[m] = lse - l[tgt];
+  if (tid == 0) row_loss[m] = lse - to_f(l[tgt]);
   const float sc = lm == -INFINITY ? 0.f : __expf(lm - lse) * inv_n;
   S* drow = dl + (int64_t)m * ldd;
 #pragma unroll
@@ -246,7 +257,7 @@ __global__ __launch_bounds__(256) void sum_kernel(const float* x, int64_t n, flo
   if (threadIdx.x == 0) *out = red[0] * scale;
 }
 
-hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32_t* tokens, int B, int T,
+hipError_t cross_entropy(DType dt, const void* logits, int64_t ldl, const int32_t* tokens, int B, int T,
                          int V, void* dlogits, int64_t ldd, float* row_loss, float* loss, hipStream_t s) {
   const int M = B * T;
   const float inv_n = 1.f / (float)M;
@@ -257,10 +268,12 @@ hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32
   const dim3 grid(M), block(kCeThreads);
 #define FAL_CE_LAUNCH(NPT)                                                                                    \
   if (dt == BF16)                                                                                            \
-    hipLaunchKernelGGL((ce_rows<bf16, NPT>), grid, block, 0, s, logits, ldl, tokens, T, V, inv_n,              \
+    hipLaunchKernelGGL((ce_rows<bf16, NPT>), grid, block, 0, s, static_cast<const bf16*>(logits), ldl, tokens, \
+                       T, V, inv_n,                                                                          \
                        static_cast<bf16*>(dlogits), ldd, row_loss);                                          \
   else                                                                                                       \
-    hipLaunchKernelGGL((ce_rows<float, NPT>), grid, block, 0, s, logits, ldl, tokens, T, V, inv_n,             \
+    hipLaunchKernelGGL((ce_rows<float, NPT>), grid, block, 0, s, static_cast<const float*>(logits), ldl,      \
+                       tokens, T, V, inv_n,                                                                  \
                        static_cast<float*>(dlogits), ldd, row_loss);
   if (need <= 1) { FAL_CE_LAUNCH(1) }
   else if (need <= 4) { FAL_CE_LAUNCH(4) }
@@ -276,6 +289,27 @@ hipError_t cross_entropy(DType dt, const float* logits, int64_t ldl, const int32
     e = hipGetLastError();
   }
   return e;
+}
+
+// dst[r, c] = src[r, c] as fp32 for r < rows, c < cols (src in dtype).
+template <typename S>
+__global__ __launch_bounds__(256) void rows_to_f32_kernel(const S* src, int64_t lds, float* dst, int64_t ldd,
+                                                          int cols) {
+  const int r = blockIdx.y;
+  for (int c = blockIdx.x * 256 + threadIdx.x; c < cols; c += gridDim.x * 256)
+    dst[(int64_t)r * ldd + c] = to_f(src[(int64_t)r * lds + c]);
+}
+
+hipError_t rows_to_f32(DType dt, const void* src, int64_t lds, float* dst, int64_t ldd, int rows, int cols,
+                       hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const dim3 grid(std::min(cdiv(cols, 256), 64), rows), block(256);
+  if (dt == BF16)
+    hipLaunchKernelGGL(rows_to_f32_kernel<bf16>, grid, block, 0, s, static_cast<const bf16*>(src), lds, dst, ldd, cols);
+  else
+    hipLaunchKernelGGL(rows_to_f32_kernel<float>, grid, block, 0, s, static_cast<const float*>(src), lds, dst, ldd,
+                       cols);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ misc --
