@@ -254,7 +254,7 @@ struct fal_ctx {
   char* ws;
   size_t ws_bytes;
   hipStream_t sm, sa;
-  hipEvent_t ev_fork, ev_join;
+  hipEvent_t ev_fork, ev_join, ev_keys;
   int device;
   std::string err;
   // kernel timing (fal_profile_enable)
@@ -787,7 +787,8 @@ fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
   carve(*cfg, ctx->ws, ctx->W, &total);
   if (hipGetDevice(&ctx->device) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_keys, hipEventDisableTiming) != hipSuccess) {
     delete[] ctx->W.slots;
     delete ctx;
     return FAL_ERR_HIP;
@@ -801,6 +802,7 @@ fal_status_t fal_destroy(fal_ctx_t* ctx) {
   for (hipEvent_t e : ctx->prof_pool) (void)hipEventDestroy(e);
   (void)hipEventDestroy(ctx->ev_fork);
   (void)hipEventDestroy(ctx->ev_join);
+  (void)hipEventDestroy(ctx->ev_keys);
   delete[] ctx->W.slots;
   delete ctx;
   return FAL_OK;
@@ -879,6 +881,16 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
   W.first_in = W.first;
   try {
     Run r(ctx);
+    // The embedding backward's (id, position) sort depends on the tokens
+    // only: it runs on the aux stream beside the forward pass, and the
+    // scatter at the end of the step waits for it.
+    {
+      hipStream_t sk = ctx->sa;
+      if (sk != sm) r.fork();
+      Span span(ctx, FAL_PROF_EMBED, sk, 0.0, (double)D.M * 8.0);
+      FAL_TRY(embed_sort(tokens, D.B, D.T, D.V, W.keys, sk));
+    }
+    FAL_TRY(hipEventRecord(ctx->ev_keys, ctx->sa));
     {
       Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * (2.0 * D.es + 4.0));
       FAL_TRY(embed_fwd(r.dt, tokens, D.B, D.T, D.V, D.d, gparam(FAL_P_WTE), gparam(FAL_P_WPE), W.resid, sm));
@@ -922,8 +934,9 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
     {
       // dX read twice (position sums, scatter), touched wte-gradient rows read and written
       Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * 16.0);
-      FAL_TRY(embed_bwd(tokens, D.B, D.T, D.V, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE],
-                        W.keys, W.dh1, sm));
+      FAL_TRY(hipStreamWaitEvent(sm, ctx->ev_keys, 0));
+      FAL_TRY(embed_bwd(D.B, D.T, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE], W.keys, W.dh1,
+                        sm));
     }
   } catch (Fail&) {
     return FAL_ERR_HIP;

@@ -269,8 +269,9 @@ static hipError_t dispatch_hd(int hd, F&& f) {
 bool attn_mfma_supported(int hd);
 hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
                                 hipStream_t s);
-hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, const float* lse, const float* Dvec,
-                                int B, int T, int H, int hd, void* dqkv, hipStream_t s);
+hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
+                                const float* lse, float* Dvec, int B, int T, int H, int hd, void* dqkv,
+                                hipStream_t s);
 
 hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
                     float* lse, hipStream_t s) {
@@ -292,6 +293,9 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
                     int64_t lddo, const float* lse, int B, int T, int H, int hd, void* dqkv,
                     float* Dvec, float* dq_acc, hipStream_t s) {
   (void)dq_acc;
+  // the matrix-core dQ kernel computes D itself
+  if (dt == BF16 && attn_mfma_supported(hd))
+    return attn_bwd_mfma_launch(qkv, O, ldo, dO, lddo, lse, Dvec, B, T, H, hd, dqkv, s);
   const int64_t nrows = (int64_t)B * H * T;
   if (dt == BF16)
     hipLaunchKernelGGL((attn_bwd_dot<bf16>), dim3(cdiv(nrows, 256)), dim3(256), 0, s,
@@ -301,8 +305,6 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
                        static_cast<const float*>(O), ldo, static_cast<const float*>(dO), lddo, B, T, H, hd, Dvec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (dt == BF16 && attn_mfma_supported(hd))
-    return attn_bwd_mfma_launch(qkv, dO, lddo, lse, Dvec, B, T, H, hd, dqkv, s);
   const dim3 grid(H, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;

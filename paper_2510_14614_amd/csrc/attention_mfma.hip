@@ -354,9 +354,11 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
 
 // ----------------------------------------------------------- backward: dQ --
 template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* dO, int64_t lddo,
-                                                        const float* lse, const float* Dvec, int T, int H,
-                                                        bf16* dqkv) {
+// Also computes D = rowsum(dO * O) for its queries and writes it to Dvec
+// for the dK/dV kernel, which runs after it.
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* O, int64_t ldo,
+                                                        const bf16* dO, int64_t lddo, const float* lse,
+                                                        float* Dvec, int T, int H, bf16* dqkv) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
@@ -377,13 +379,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
   const float sl2 = kLog2e / sqrtf((float)HD);
 
   bf16x8v qf[KK], of[KK];
+  float dsum = 0.f;  // this lane's half of dO . O for query tq
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     qf[kk] = frag_global<HD>(Qg, ld, tq, T, kk, g);
     of[kk] = frag_global<HD>(dOg, lddo, tq, T, kk, g);
+    const bf16x8v o8 = frag_global<HD>(O + (int64_t)b * T * ldo + h * HD, ldo, tq, T, kk, g);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dsum += static_cast<float>(of[kk][j]) * static_cast<float>(o8[j]);
   }
   const float L2 = tq < T ? lse[((int64_t)b * H + h) * T + tq] * kLog2e : 0.f;
-  const float Dq = tq < T ? Dvec[((int64_t)b * H + h) * T + tq] : 0.f;
+  const float Dq = tq < T ? dsum + __shfl_xor(dsum, 32, 64) : 0.f;
+  if (g == 0 && tq < T) Dvec[((int64_t)b * H + h) * T + tq] = Dq;
   f32x16v dq[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) dq[t] = zero16();
@@ -458,18 +465,21 @@ hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, vo
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_mfma_launch(const void* qkv, const void* dO, int64_t lddo, const float* lse, const float* Dvec,
-                                int B, int T, int H, int hd, void* dqkv, hipStream_t s) {
+// dQ first (it also writes D = rowsum(dO * O) into Dvec), then dK / dV.
+hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
+                                const float* lse, float* Dvec, int B, int T, int H, int hd, void* dqkv,
+                                hipStream_t s) {
   const dim3 grid(H, B, cdiv(T, 128)), block(256);
   const bf16* q = static_cast<const bf16*>(qkv);
+  const bf16* ob = static_cast<const bf16*>(O);
   const bf16* d = static_cast<const bf16*>(dO);
   bf16* o = static_cast<bf16*>(dqkv);
   if (hd == 64) {
+    hipLaunchKernelGGL((attn_bwd_dq_mfma<64>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
     hipLaunchKernelGGL((attn_bwd_dkdv_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-    hipLaunchKernelGGL((attn_bwd_dq_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
   } else if (hd == 128) {
+    hipLaunchKernelGGL((attn_bwd_dq_mfma<128>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
     hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-    hipLaunchKernelGGL((attn_bwd_dq_mfma<128>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
   } else {
     return hipErrorInvalidValue;
   }

@@ -182,13 +182,16 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
 // X[m, :] = wte[tok[b, t]] + wpe[t]  (fp32 out), tokens [B, T+1].
 hipError_t embed_fwd(DType dt, const int32_t* tokens, int B, int T, int V, int d, const void* wte,
                      const void* wpe, float* X, hipStream_t s);
-// dwte[v] += sum over positions with input id v of dX rows (deterministic:
-// sorted by (id, position)), dwpe[t] = sum_b dX[b, t].  sort_scratch: int32
-// of embed_bwd_scratch(M) elements; partial: fp32 [M, d] scratch.
-// Requires B*T <= 16384.
-hipError_t embed_bwd(const int32_t* tokens, int B, int T, int V, int d, const float* dX,
-                     float* dwte, float* dwpe, int32_t* sort_scratch, float* partial,
-                     hipStream_t s);
+// Sorts the (input id, position) pairs of the batch into sort_scratch
+// (int32 of embed_bwd_scratch(M) elements).  Depends on the tokens only, so
+// it can run ahead of (or beside) the rest of the step.  Requires
+// B*T <= 16384.
+hipError_t embed_sort(const int32_t* tokens, int B, int T, int V, int32_t* sort_scratch, hipStream_t s);
+// dwte[v] += sum over positions with input id v of dX rows, in position
+// order (deterministic; sort_scratch as written by embed_sort), dwpe[t] =
+// sum_b dX[b, t].  partial: fp32 [M, d] scratch.
+hipError_t embed_bwd(int B, int T, int d, const float* dX, float* dwte, float* dwpe,
+                     const int32_t* sort_scratch, float* partial, hipStream_t s);
 int64_t embed_bwd_scratch(int M);
 
 // Cross-entropy over rows of logits [M, V] (dtype: fp32 or bf16, row

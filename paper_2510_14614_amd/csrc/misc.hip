@@ -127,14 +127,18 @@ __global__ __launch_bounds__(256) void wpe_grad_kernel(const float* dX, int B, i
 
 int64_t embed_bwd_scratch(int M) { return M; }
 
-hipError_t embed_bwd(const int32_t* tokens, int B, int T, int V, int d, const float* dX, float* dwte,
-                     float* dwpe, int32_t* sort_scratch, float* partial, hipStream_t s) {
+hipError_t embed_sort(const int32_t* tokens, int B, int T, int V, int32_t* sort_scratch, hipStream_t s) {
+  if (B * T > kSortMax) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(1024), 0, s, tokens, B, T, V,
+                     reinterpret_cast<uint32_t*>(sort_scratch));
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(int B, int T, int d, const float* dX, float* dwte, float* dwpe, const int32_t* sort_scratch,
+                     float* partial, hipStream_t s) {
   const int M = B * T;
   if (M > kSortMax) return hipErrorInvalidValue;
-  uint32_t* keys = reinterpret_cast<uint32_t*>(sort_scratch);
-  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(1024), 0, s, tokens, B, T, V, keys);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const uint32_t* keys = reinterpret_cast<const uint32_t*>(sort_scratch);
   const int cb = cdiv(d, 256);
   hipLaunchKernelGGL(embed_chunk_kernel, dim3(cdiv(M, kChunk), cb), dim3(256), 0, s, keys, M, d, dX, partial);
   hipLaunchKernelGGL(embed_combine_kernel, dim3(M, cb), dim3(256), 0, s, keys, M, d, partial, dwte);
