@@ -249,11 +249,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
 }
 
 // ------------------------------------------------------- backward: dK dV --
-template <int HD>
-// two wavefronts per SIMD where the registers allow it (head_dim 64; at 128
-// the dK and dV accumulators alone take 64 registers per lane)
-__global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
+// PART 0: dK and dV together (head_dim 64: two wavefronts per SIMD fit;
+// head_dim 128: the accumulators take the whole register file, one
+// wavefront per SIMD).  PART 1: dV only, PART 2: dK only (head_dim 128:
+// each pass fits two wavefronts per SIMD at the cost of recomputing S in
+// both; used when the grid has enough workgroups to put two on every CU).
+template <int HD, int PART = 0>
+__global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bwd_dkdv_mfma(
     const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, bf16* dqkv) {
+  constexpr bool DO_V = PART != 2, DO_K = PART != 1;
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sQ[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sdO[AT * (HD + 8)];
@@ -275,15 +279,18 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
   const int key = kw + c;          // this lane's key (column of S)
   const float sl2 = kLog2e / sqrtf((float)HD);
 
-  bf16x8v kf[KK], vf[KK];
+  bf16x8v kf[KK], vf[DO_K ? KK : 1];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     kf[kk] = frag_global<HD>(Kg, ld, key, T, kk, g);
-    vf[kk] = frag_global<HD>(Vg, ld, key, T, kk, g);
+    if constexpr (DO_K) vf[kk] = frag_global<HD>(Vg, ld, key, T, kk, g);
   }
-  f32x16v dk[NT], dv[NT];
+  f32x16v dk[DO_K ? NT : 1], dv[DO_V ? NT : 1];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) { dk[t] = zero16(); dv[t] = zero16(); }
+  for (int t = 0; t < NT; ++t) {
+    if constexpr (DO_K) dk[t] = zero16();
+    if constexpr (DO_V) dv[t] = zero16();
+  }
 
   RowTile<HD> rq, ro;
   if (kb0 < T) {
@@ -312,7 +319,7 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         s = mfma32(frag_rows<HD>(sQ, 32 * sub + c, kk, g), kf[kk], s);
-        dp = mfma32(frag_rows<HD>(sdO, 32 * sub + c, kk, g), vf[kk], dp);
+        if constexpr (DO_K) dp = mfma32(frag_rows<HD>(sdO, 32 * sub + c, kk, g), vf[kk], dp);
       }
       // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
       // Q and dO rows and zero L and D, so they add nothing; only the
@@ -324,16 +331,23 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
         float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -sL[qr]));
         if (diag && key > q0 + qr) p = 0.f;
         s[r] = p;
-        dp[r] = p * (dp[r] - sD[qr]);
+        if constexpr (DO_K) dp[r] = p * (dp[r] - sD[qr]);
       }
-      const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
-      const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
+      if constexpr (DO_V) {
+        const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        dv[t] = mfma32(p0, frag_tr<HD>(sdO, 32 * sub, 32 * t, lane), dv[t]);
-        dv[t] = mfma32(p1, frag_tr<HD>(sdO, 32 * sub + 16, 32 * t, lane), dv[t]);
-        dk[t] = mfma32(d0, frag_tr<HD>(sQ, 32 * sub, 32 * t, lane), dk[t]);
-        dk[t] = mfma32(d1, frag_tr<HD>(sQ, 32 * sub + 16, 32 * t, lane), dk[t]);
+        for (int t = 0; t < NT; ++t) {
+          dv[t] = mfma32(p0, frag_tr<HD>(sdO, 32 * sub, 32 * t, lane), dv[t]);
+          dv[t] = mfma32(p1, frag_tr<HD>(sdO, 32 * sub + 16, 32 * t, lane), dv[t]);
+        }
+      }
+      if constexpr (DO_K) {
+        const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          dk[t] = mfma32(d0, frag_tr<HD>(sQ, 32 * sub, 32 * t, lane), dk[t]);
+          dk[t] = mfma32(d1, frag_tr<HD>(sQ, 32 * sub + 16, 32 * t, lane), dk[t]);
+        }
       }
     }
   }
@@ -346,8 +360,8 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void attn_bwd_dkdv_mfma(
       const int kr = kw + acc_row(r, g);
       if (kr < T) {
         bf16* row = dqkv + ((int64_t)b * T + kr) * ld + h * HD + 32 * t + c;
-        row[dA] = static_cast<bf16>(dk[t][r] * scale);
-        row[2 * dA] = static_cast<bf16>(dv[t][r]);
+        if constexpr (DO_K) row[dA] = static_cast<bf16>(dk[t][r] * scale);
+        if constexpr (DO_V) row[2 * dA] = static_cast<bf16>(dv[t][r]);
       }
     }
 }
@@ -454,6 +468,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
 
 bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
 
+constexpr int kAttnCUs = 256;  // MI355X compute units
+
 hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
                                 hipStream_t s) {
   const dim3 grid(H, B, cdiv(T, 128)), block(256);
@@ -479,7 +495,12 @@ hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, con
     hipLaunchKernelGGL((attn_bwd_dkdv_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
   } else if (hd == 128) {
     hipLaunchKernelGGL((attn_bwd_dq_mfma<128>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
-    hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    if ((int64_t)grid.x * grid.y * grid.z >= 2 * kAttnCUs) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 1>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 2>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    } else {
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 0>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    }
   } else {
     return hipErrorInvalidValue;
   }

@@ -114,6 +114,20 @@ def test_long_sequence_multi_block_attention(arch, hd):
                  label=f"long a{arch} hd{hd}")
 
 
+@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL])
+def test_hd128_wide_grid_split_backward(arch):
+    # head_dim 128 with at least two attention workgroups per CU (16 heads x
+    # 7 sequences x 5 query blocks = 560): the dK and dV passes run as two
+    # kernels; T = 600 leaves the last query block ragged
+    cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, d_ff=512, vocab=512, seq_len=600,
+                 batch=7, arch=arch, dtype=1)
+    log(f"hd128 wide grid arch={arch}")
+    g, blocks = synth.make_params(cfg, seed=16)
+    tok = synth.make_tokens(cfg, seed=17, dist="zipf")
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"hd128 wide a{arch}")
+
+
 @pytest.mark.parametrize("arch", [ARCH_FAL, ARCH_FALPLUS])
 def test_large_tile_ragged_rows(arch):
     # 2000 token rows (not a multiple of 256) with launches large enough for
