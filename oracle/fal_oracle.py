@@ -36,7 +36,11 @@ Readings taken where the paper is silent (each listed in the design notes):
     misplaced parenthesis);
   - GPT-2 conventions: tanh GELU, eps 1e-5, biases on every linear layer,
     learned position embedding, final LayerNorm, LM head tied to wte,
-    no dropout; next-token cross-entropy averaged over B*T positions.
+    no dropout; next-token cross-entropy averaged over B*T positions;
+  - the optimizer of the training setups (appendix: lr 1e-4, weight decay
+    0.001, gradient clipping to norm 1; the optimizer is not named) is
+    AdamW with beta1 0.9, beta2 0.999, eps 1e-8, decay on every tensor and
+    PyTorch's clipping rule (adamw_step, train).
 
 Weights are stored [in, out] so that a linear layer is y = x @ W + b.
 Parameters are dicts of arrays (see ``paper_2510_14614_amd.synth`` for the
@@ -370,3 +374,96 @@ def forward_logits(cfg, gparams, blocks, tokens):
     xs, _, _ = stack_forward(cfg, blocks, x1)
     hf, _ = layer_norm(xs[-1], g["lnf_g"], g["lnf_b"], cfg.ln_eps)
     return hf @ g["wte"].T
+
+
+# ---------------------------------------------------------------------------
+# Optimizer and training loop
+#
+# The appendix's training setups give learning rate 1e-4, weight decay 0.001
+# and gradient clipping to global norm 1; the optimizer itself is not named.
+# Reading taken: AdamW, i.e. Adam's bias-corrected first and second moment
+# estimates (Kingma & Ba) with weight decay applied to the parameters
+# directly rather than through the gradient (Loshchilov & Hutter), with the
+# usual defaults beta1 0.9, beta2 0.999, eps 1e-8, decay on every tensor.
+# Clipping scales all gradients by min(1, clip / (norm + 1e-6)), the norm
+# being the L2 norm of every gradient entry taken together.
+# ---------------------------------------------------------------------------
+
+ADAMW_PAPER = {"lr": 1e-4, "beta1": 0.9, "beta2": 0.999, "eps": 1e-8, "weight_decay": 1e-3,
+               "max_grad_norm": 1.0}
+
+
+def global_grad_norm(grads):
+    """sqrt of the sum of squares of every entry of every gradient tensor."""
+    return math.sqrt(sum(float(np.sum(np.square(np.asarray(g, dtype=f64)))) for g in grads))
+
+
+def clip_coefficient(norm, max_grad_norm):
+    """Factor the gradients are scaled by; 1 when clipping is off (<= 0)."""
+    if max_grad_norm <= 0:
+        return 1.0
+    return min(1.0, max_grad_norm / (norm + 1e-6))
+
+
+def adamw_step(params, grads, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0,
+               max_grad_norm=0.0):
+    """One AdamW update of a list of tensors.
+
+    step is the 1-based index of this update (the bias corrections use
+    beta^step).  m and v are the moment estimates after step-1 updates
+    (zeros before the first).  Returns (params, m, v, grad_norm) as new
+    float64 arrays; grad_norm is the norm before clipping."""
+    if step < 1:
+        raise ValueError("step is 1-based")
+    norm = global_grad_norm(grads)
+    c = clip_coefficient(norm, max_grad_norm)
+    bc1 = 1.0 - beta1 ** step
+    bc2 = 1.0 - beta2 ** step
+    out_p, out_m, out_v = [], [], []
+    for p, g, m0, v0 in zip(params, grads, m, v):
+        g = c * np.asarray(g, dtype=f64)
+        m1 = beta1 * np.asarray(m0, dtype=f64) + (1.0 - beta1) * g
+        v1 = beta2 * np.asarray(v0, dtype=f64) + (1.0 - beta2) * g * g
+        p1 = np.asarray(p, dtype=f64) * (1.0 - lr * weight_decay)
+        p1 = p1 - lr * (m1 / bc1) / (np.sqrt(v1 / bc2) + eps)
+        out_p.append(p1)
+        out_m.append(m1)
+        out_v.append(v1)
+    return out_p, out_m, out_v, norm
+
+
+def _param_list(gparams, blocks):
+    names = [("g", k) for k in gparams] + [(i, k) for i, b in enumerate(blocks) for k in b]
+    vals = [gparams[k] for k in gparams] + [b[k] for b in blocks for k in b]
+    return names, vals
+
+
+def _unpack(names, vals, n_blocks):
+    g, blocks = {}, [dict() for _ in range(n_blocks)]
+    for (owner, k), x in zip(names, vals):
+        if owner == "g":
+            g[k] = x
+        else:
+            blocks[owner][k] = x
+    return g, blocks
+
+
+def train(cfg, gparams, blocks, token_batches, hp, first_step=1):
+    """Training loop: for each batch one forward + backward (train_step)
+    followed by one AdamW update of every parameter tensor.
+
+    Returns dict(losses, grad_norms, gparams, blocks, m, v) with the
+    parameters after the last update."""
+    names, p = _param_list(_as64(gparams), [_as64(b) for b in blocks])
+    m = [np.zeros_like(x) for x in p]
+    v = [np.zeros_like(x) for x in p]
+    losses, norms = [], []
+    for j, tok in enumerate(token_batches):
+        g, bl = _unpack(names, p, len(blocks))
+        r = train_step(cfg, g, bl, tok)
+        grads = [r["grads_global"][k] if owner == "g" else r["grads_blocks"][owner][k] for owner, k in names]
+        p, m, v, norm = adamw_step(p, grads, m, v, first_step + j, **hp)
+        losses.append(r["loss"])
+        norms.append(norm)
+    g, bl = _unpack(names, p, len(blocks))
+    return {"losses": losses, "grad_norms": norms, "gparams": g, "blocks": bl, "m": m, "v": v}
