@@ -19,6 +19,8 @@ Also reported, from the same process:
     no overlap between kernels, so each span times one kernel);
   * the same-kernel sequential GPT baseline and FAL+ on the same config
     (tokens/s and the ratio to it);
+  * training_with_optimizer: the same step followed by the AdamW update of
+    every parameter (tokens/s and the update's own time and bandwidth);
   * cpu_baseline: the fp64 CPU oracle timed on this host on a bounded sample
     (batch 1 of the same config).
 """
@@ -56,6 +58,8 @@ def parse():
     ap.add_argument("--sched", default="streams_merged", choices=["seq", "streams", "merged", "streams_merged"])
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-optimizer", action="store_true",
+                    help="skip the extra measurement of step + AdamW update")
     ap.add_argument("--cpu-sample-batch", type=int, default=1)
     ap.add_argument("--single-stream", action="store_true",
                     help="run the timed steps with the aux stream equal to the main stream")
@@ -78,12 +82,14 @@ def describe(cfg, arch_name, sched_name):
 
 
 class Runner:
-    def __init__(self, cfg, single_stream=False):
+    def __init__(self, cfg, single_stream=False, optimizer=False):
         import torch
 
         from paper_2510_14614_amd import fal, synth
         self.torch = torch
         self.cfg = cfg
+        self.optimizer = optimizer
+        self.hp = fal.ADAMW_PAPER
         main = torch.cuda.current_stream()
         self.F = fal.Fal(cfg, stream_main=main, stream_aux=main if single_stream else None)
         g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
@@ -96,12 +102,16 @@ class Runner:
             self.x1 = torch.from_numpy(x1).cuda()
             self.dy = torch.from_numpy(gout).cuda()
             self.dx = torch.empty_like(self.x1)
+        if optimizer:
+            self.F.init_optimizer()
 
     def step(self):
         if self.cfg.has_embed_head:
             self.F.model_step(self.tok)
         else:
             self.F.stack_step(self.x1, self.dy, self.dx)
+        if self.optimizer:
+            self.F.adamw_step(**self.hp)
 
     def time(self, steps, warmup):
         torch = self.torch
@@ -384,6 +394,26 @@ def main():
         comp["paper_context"] = ("paper: FAL single-GPU throughput up to 1.18x (1.08x average) over "
                                  "GPT-2 774M on RTX 3090/4090/A6000; context, not the target")
         out["comparison"] = comp
+
+    if not args.no_optimizer:
+        # the same step followed by the AdamW update of every parameter
+        # (fp32 master weights and moments, bf16 weight copy; the paper's
+        # lr 1e-4, weight decay 0.001, clip 1)
+        ro = Runner(cfg, single_stream=args.single_stream, optimizer=True)
+        ms_o, _ = ro.time(args.steps, args.warmup)
+        po = ro.profile(args.steps)["optimizer"]
+        n_params = ro.F.layout["total"]
+        ro.close()
+        opt_ms = po["ms"] / max(po["launches"], 1)
+        out["training_with_optimizer"] = {
+            "tokens_per_s": cfg.tokens / (ms_o / 1000.0),
+            "ms_per_step": ms_o,
+            "optimizer_ms": opt_ms,
+            "parameters": n_params,
+            "optimizer_alg_bytes": po["bytes"] / max(po["launches"], 1),
+            "optimizer_GB/s": po["bytes"] / max(po["ms"], 1e-9) / 1e6,
+            "optimizer_frac_hbm_peak": po["bytes"] / max(po["ms"], 1e-9) / 1e6 / PEAK_HBM_GBS,
+        }
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)

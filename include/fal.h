@@ -199,6 +199,46 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
 fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_in,
                             const float* dy, float* loss, float* grads, float* dx_in);
 
+/* Optimizer hyper-parameters.  The paper's training setups (appendix) use
+ * learning rate 1e-4, weight decay 0.001 and gradient clipping to global
+ * norm 1 with an Adam-type optimizer; beta1 0.9, beta2 0.999, eps 1e-8 are
+ * the usual AdamW defaults. */
+typedef struct {
+  float lr;            /* learning rate, >= 0                                 */
+  float beta1, beta2;  /* moment decay rates, in [0, 1)                       */
+  float eps;           /* added to sqrt of the second moment, >= 0            */
+  float weight_decay;  /* decoupled: p <- p (1 - lr weight_decay), >= 0       */
+  float max_grad_norm; /* clip threshold on the global L2 norm; <= 0: no clip */
+} fal_adamw_t;
+
+/* One AdamW update of a flat parameter buffer (the optimizer of the paper's
+ * training setups, appendix), after clipping the gradient to a global norm:
+ *   c = min(1, max_grad_norm / (||grads||_2 + 1e-6))   (1 without clipping)
+ *   g = c grads;  m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2
+ *   master = master (1 - lr weight_decay)
+ *            - lr / (1 - beta1^step) * m / (sqrt(v / (1 - beta2^step)) + eps)
+ * applied to every element (alignment padding included: its gradient is
+ * zero when the caller zero-filled the gradient buffer once, so it only
+ * decays).  The norm is the square root of a fixed-order fp64 sum, so the
+ * update is deterministic.
+ *   step     1-based index of this update (bias corrections use beta^step)
+ *   n        number of elements (normally `total` of fal_param_layout), >= 0
+ *   master   device fp32 [n], the fp32 weights, updated in place
+ *   params   device, config dtype [n]: receives master rounded to the dtype
+ *            (bf16: round to nearest even) for the next step.  fp32 configs:
+ *            NULL or equal to master when master is the parameter buffer.
+ *   grads    device fp32 [n], read only (e.g. from fal_model_step)
+ *   m, v     device fp32 [n] first and second moments, zero before step 1,
+ *            updated in place
+ *   grad_norm device fp32 scalar or NULL: the norm before clipping
+ * fp32 arrays must be 16-byte aligned and params 8-byte (bf16) or 16-byte
+ * (fp32) aligned; the arrays may not overlap (except params == master).
+ * Non-finite gradients are not skipped: they reach the weights.  Enqueued
+ * on the main stream; uses a few KB of the context's workspace. */
+fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step, int64_t n,
+                            float* master, void* params, const float* grads, float* m, float* v,
+                            float* grad_norm);
+
 /* Device pointer to the final block output X_L (fp32 [M, d]) held in the
  * workspace after a step; valid until the next step. */
 fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);
@@ -213,12 +253,13 @@ fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);
  * of the rows read and written; cross-entropy: logits read and dlogits
  * written; embedding: rows gathered and written forward, the position-
  * gradient and scatter traffic backward; bias gradients: the column sums'
- * input).  fal_profile_enable(ctx, 0) turns timing off; either call clears
+ * input; optimizer: the gradient read by the norm pass plus every array
+ * the update reads and writes).  fal_profile_enable(ctx, 0) turns timing off; either call clears
  * the counters.  Host memory only; no device allocation. */
 typedef enum {
   FAL_PROF_GEMM = 0, FAL_PROF_ATTN_FWD = 1, FAL_PROF_ATTN_BWD = 2, FAL_PROF_NORM = 3,
-  FAL_PROF_CE = 4, FAL_PROF_EMBED = 5, FAL_PROF_BIAS = 6,
-  FAL_PROF_NCLASS = 7
+  FAL_PROF_CE = 4, FAL_PROF_EMBED = 5, FAL_PROF_BIAS = 6, FAL_PROF_OPTIM = 7,
+  FAL_PROF_NCLASS = 8
 } fal_prof_class_t;
 fal_status_t fal_profile_enable(fal_ctx_t* ctx, int32_t enable);
 fal_status_t fal_profile_read(fal_ctx_t* ctx, int32_t cls, int64_t* launches, double* total_ms,

@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -168,6 +169,8 @@ struct Work {
   int64_t splitk_floats;
   int32_t* keys;
   float* loss_tmp;
+  double* opt_part;  // fp64 partial sums of the gradient-norm pass
+  float* opt_ctrl;   // {norm, clip factor}
 };
 
 void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
@@ -233,6 +236,8 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.splitk_main = cv.take<float>(W.splitk_floats);
   W.splitk_aux = cv.take<float>(W.splitk_floats);
   W.loss_tmp = cv.take<float>(64);
+  W.opt_part = cv.take<double>(kNormBlocks);
+  W.opt_ctrl = cv.take<float>(16);
   W.first_in = W.first;
   *total = cv.off + kAlignBytes;
 }
@@ -976,6 +981,70 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
       cur = out;
       k ^= 1;
     }
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+static bool overlaps(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + (uintptr_t)bbytes && y < x + (uintptr_t)abytes;
+}
+
+fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step, int64_t n, float* master,
+                            void* params, const float* grads, float* m, float* v, float* norm_out) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (!hp) return bad(ctx, "NULL hyper-parameters");
+  if (step < 1) return bad(ctx, "step is 1-based");
+  if (n < 0) return bad(ctx, "negative element count");
+  auto finite = [](float x) { return std::isfinite(x); };
+  if (!finite(hp->lr) || !finite(hp->beta1) || !finite(hp->beta2) || !finite(hp->eps) ||
+      !finite(hp->weight_decay) || !finite(hp->max_grad_norm))
+    return bad(ctx, "non-finite hyper-parameter");
+  if (hp->lr < 0.f || hp->eps < 0.f || hp->weight_decay < 0.f) return bad(ctx, "lr, eps and weight_decay must be >= 0");
+  if (!(hp->beta1 >= 0.f && hp->beta1 < 1.f && hp->beta2 >= 0.f && hp->beta2 < 1.f))
+    return bad(ctx, "beta1 and beta2 must lie in [0, 1)");
+  const bool bf = ctx->cfg.dtype == FAL_BF16;
+  if (n > 0 && (!master || !grads || !m || !v)) return bad(ctx, "NULL master, grads, m or v");
+  if (bf && n > 0 && !params) return bad(ctx, "params (bf16 copy) is required for a bf16 config");
+  const int lp_mode = (!params || params == master) ? 0 : (bf ? 2 : 1);
+  if (bf && lp_mode == 0 && n > 0) return bad(ctx, "params may not alias master for a bf16 config");
+  auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
+  if (!al(master, 16) || !al(grads, 16) || !al(m, 16) || !al(v, 16) ||
+      (lp_mode != 0 && !al(params, lp_mode == 2 ? 8 : 16)))
+    return bad(ctx, "fp32 arrays must be 16-byte aligned, params 8-byte (bf16) or 16-byte (fp32)");
+  if (norm_out && !al(norm_out, 4)) return bad(ctx, "grad_norm must be 4-byte aligned");
+  const int64_t b4 = n * 4;
+  const void* arr[5] = {master, grads, m, v, params};
+  const int64_t len[5] = {b4, b4, b4, b4, lp_mode == 0 ? 0 : n * (lp_mode == 2 ? 2 : 4)};
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (len[i] > 0 && len[j] > 0 && overlaps(arr[i], len[i], arr[j], len[j]))
+        return bad(ctx, "master, grads, m, v and params may not overlap");
+  if (norm_out && n > 0)
+    for (int i = 0; i < 5; ++i)
+      if (len[i] > 0 && overlaps(norm_out, 4, arr[i], len[i])) return bad(ctx, "grad_norm overlaps an array");
+  // bias corrections and step size in double on the host
+  const double bc1 = 1.0 - std::pow((double)hp->beta1, (double)step);
+  const double bc2 = 1.0 - std::pow((double)hp->beta2, (double)step);
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return bad(ctx, "bias correction underflows (beta too close to 1 for step)");
+  AdamwConsts k;
+  k.beta1 = hp->beta1;
+  k.one_minus_beta1 = (float)(1.0 - (double)hp->beta1);
+  k.beta2 = hp->beta2;
+  k.one_minus_beta2 = (float)(1.0 - (double)hp->beta2);
+  k.eps = hp->eps;
+  k.rsqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  k.step_size = (float)((double)hp->lr / bc1);
+  k.decay = (float)(1.0 - (double)hp->lr * hp->weight_decay);
+  hipStream_t sm = ctx->sm;
+  try {
+    const double bytes = 4.0 * n + (double)n * (28.0 + (lp_mode == 2 ? 2.0 : lp_mode == 1 ? 4.0 : 0.0));
+    Span span(ctx, FAL_PROF_OPTIM, sm, 0.0, bytes);
+    FAL_TRY(grad_norm(grads, n, hp->max_grad_norm, ctx->W.opt_part, ctx->W.opt_ctrl, norm_out, sm));
+    FAL_TRY(adamw_update(lp_mode, master, params, grads, m, v, n, k, ctx->W.opt_ctrl, sm));
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }

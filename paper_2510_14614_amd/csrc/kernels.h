@@ -222,4 +222,28 @@ hipError_t cache_warm(const void* p, int64_t bytes, hipStream_t s);
 // Fill fp32 with zero (a kernel, so it can live inside captured graphs).
 hipError_t zero_f32(float* y, int64_t n, hipStream_t s);
 
+// ----------------------------------------------------------- optimizer ----
+// AdamW over a flat fp32 buffer (Adam's bias-corrected moments, decoupled
+// weight decay), after scaling the gradient by a global-norm clip factor.
+constexpr int kNormBlocks = 2048;  // fp64 partial sums of the norm pass
+struct AdamwConsts {
+  float beta1, one_minus_beta1, beta2, one_minus_beta2;
+  float eps;
+  float rsqrt_bc2;  // 1 / sqrt(1 - beta2^step)
+  float step_size;  // lr / (1 - beta1^step)
+  float decay;      // 1 - lr * weight_decay
+};
+// part: kNormBlocks doubles of scratch; ctrl: 2 floats.
+// ctrl[0] = ||g||_2 over n fp32 elements (fixed-order fp64 reduction),
+// ctrl[1] = min(1, max_norm / (norm + 1e-6)) (1 when max_norm <= 0);
+// norm_out (may be NULL) receives the norm.  g 16-byte aligned.
+hipError_t grad_norm(const float* g, int64_t n, float max_norm, double* part, float* ctrl, float* norm_out,
+                     hipStream_t s);
+// One update of n elements with the gradient scaled by ctrl[1].  lp_mode 0:
+// master is the parameter buffer; 1: fp32 copy written to lp; 2: bf16 copy
+// (round to nearest even) written to lp.  fp32 arrays 16-byte aligned, lp
+// 8-byte (bf16) or 16-byte (fp32) aligned.
+hipError_t adamw_update(int lp_mode, float* master, void* lp, const float* g, float* m, float* v, int64_t n,
+                        const AdamwConsts& k, const float* ctrl, hipStream_t s);
+
 }  // namespace fal

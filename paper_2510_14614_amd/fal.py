@@ -27,11 +27,16 @@ BLOCK_TENSORS = BLOCK_NAMES
 ABI_FUNCTIONS = (
     "fal_validate_config", "fal_param_layout", "fal_workspace_bytes", "fal_init", "fal_destroy",
     "fal_block_fwd", "fal_block_bwd", "fal_model_step", "fal_stack_step", "fal_residual_out",
-    "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error",
+    "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error", "fal_adamw_step",
 )
-PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM, PROF_CE, PROF_EMBED, PROF_BIAS = range(7)
+PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM, PROF_CE, PROF_EMBED, PROF_BIAS, PROF_OPTIM = range(8)
 PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm",
-              PROF_CE: "cross_entropy", PROF_EMBED: "embedding", PROF_BIAS: "bias_grad"}
+              PROF_CE: "cross_entropy", PROF_EMBED: "embedding", PROF_BIAS: "bias_grad", PROF_OPTIM: "optimizer"}
+
+# AdamW settings of the paper's training setups (appendix: lr 1e-4, weight
+# decay 0.001, clip-grad-norm 1) with the usual beta and eps defaults.
+ADAMW_PAPER = {"lr": 1e-4, "beta1": 0.9, "beta2": 0.999, "eps": 1e-8, "weight_decay": 1e-3,
+               "max_grad_norm": 1.0}
 
 
 class fal_config_t(ctypes.Structure):
@@ -41,6 +46,17 @@ class fal_config_t(ctypes.Structure):
         ("arch", c_int32), ("dtype", c_int32), ("sched", c_int32), ("ln_eps", c_float),
         ("gelu_tanh", c_int32), ("has_embed_head", c_int32), ("fal_block1_mode", c_int32),
     ]
+
+
+class fal_adamw_t(ctypes.Structure):
+    _fields_ = [("lr", c_float), ("beta1", c_float), ("beta2", c_float), ("eps", c_float),
+                ("weight_decay", c_float), ("max_grad_norm", c_float)]
+
+
+def adamw_params(**hp) -> fal_adamw_t:
+    v = dict(ADAMW_PAPER)
+    v.update(hp)
+    return fal_adamw_t(**{k: float(v[k]) for k in ADAMW_PAPER})
 
 
 class FalError(RuntimeError):
@@ -74,6 +90,8 @@ def lib():
         L.fal_profile_enable.argtypes = [c_void_p, c_int32]
         L.fal_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_int64), POINTER(c_double),
                                        POINTER(c_double), POINTER(c_double)]
+        L.fal_adamw_step.argtypes = [c_void_p, POINTER(fal_adamw_t), c_int64, c_int64, c_void_p, c_void_p,
+                                     c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_status_string.argtypes = [c_int32]
         L.fal_status_string.restype = c_char_p
         L.fal_last_error.argtypes = [c_void_p]
@@ -244,6 +262,39 @@ class Fal:
                                    c_void_p(dx_in.data_ptr()),
                                    c_void_p(dfirst.data_ptr()) if dfirst is not None else None,
                                    c_void_p(self.block_grad_ptr(layer))), self.ctx)
+
+    # ----------------------------------------------------------- optimizer --
+    def init_optimizer(self):
+        """fp32 master weights (copied from the current parameters) and zero
+        AdamW moments, all in the flat parameter layout."""
+        torch = self.torch
+        self.master = self.params.float().clone() if self.cfg.dtype == 1 else self.params
+        self.m = torch.zeros_like(self.grads)
+        self.v = torch.zeros_like(self.grads)
+        self.grad_norm = torch.zeros(1, dtype=torch.float32, device=self.device)
+        self.opt_step = 0
+
+    def adamw_step(self, **hp):
+        """One AdamW update of every parameter from self.grads (defaults: the
+        paper's lr 1e-4, weight decay 0.001, clip 1).  Returns the pre-clip
+        gradient norm (device tensor [1])."""
+        if getattr(self, "master", None) is None:
+            self.init_optimizer()
+        self.opt_step += 1
+        p = adamw_params(**hp)
+        lp = c_void_p(self.params.data_ptr()) if self.cfg.dtype == 1 else None
+        _check(lib().fal_adamw_step(self.ctx, byref(p), self.opt_step, self.layout["total"],
+                                    c_void_p(self.master.data_ptr()), lp, c_void_p(self.grads.data_ptr()),
+                                    c_void_p(self.m.data_ptr()), c_void_p(self.v.data_ptr()),
+                                    c_void_p(self.grad_norm.data_ptr())), self.ctx)
+        return self.grad_norm
+
+    def train_step(self, tokens, **hp):
+        """Forward + backward (fal_model_step) and one AdamW update; returns
+        the loss of the batch before the update (device tensor [1])."""
+        self.model_step(tokens)
+        self.adamw_step(**hp)
+        return self.loss
 
     def profile_enable(self, on: bool = True):
         _check(lib().fal_profile_enable(self.ctx, 1 if on else 0), self.ctx)

@@ -19,6 +19,8 @@ Recipe (stated once so every caller draws the same data):
     whole vocabulary (s = 1.1), drawn by inverse CDF; ``dist="uniform"``.
   * block stack (no embedding / head): X_1 ~ N(0, 1) of shape [B*T, d] and an
     upstream gradient G ~ N(0, 1/(B*T*d)).
+  * optimizer inputs: flat float32 arrays of N(0, scale^2) draws (absolute
+    values for second moments), one seed per array.
 """
 from __future__ import annotations
 
@@ -130,3 +132,11 @@ def make_stack_inputs(cfg: Config, seed: int = 2):
     x1 = rng.normal(0.0, 1.0, size=(M, d)).astype(np.float32)
     g = rng.normal(0.0, 1.0 / np.sqrt(M * d), size=(M, d)).astype(np.float32)
     return x1, g
+
+
+def make_flat(n: int, seed: int, scale: float = 1.0, positive: bool = False) -> np.ndarray:
+    """A flat float32 array of n draws from N(0, scale^2) (its absolute value
+    when positive), e.g. weights, gradients or optimizer moments."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = rng.standard_normal(n, dtype=np.float32) * np.float32(scale)
+    return np.abs(x) if positive else x
