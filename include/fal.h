@@ -1,7 +1,7 @@
 /*
  * fal.h -- C ABI of libfal.so: one training step (forward + backward) of a
- * GPT-style Pre-LN decoder stack in three block architectures, on one
- * MI355X (gfx950):
+ * GPT-style Pre-LN decoder stack in three block architectures, and the
+ * AdamW update that follows it, on one MI355X (gfx950):
  *
  *   GPT   (Sec. 2, Eq. 1)  X_{i+1} = X_i + MHA_i(LN(X_i))
  *                                   + MLP_i(LN(X_i + MHA_i(LN(X_i))))
