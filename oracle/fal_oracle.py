@@ -21,6 +21,10 @@ the paper and 0-based here):
   output to its usual MLP input:
       X_{i+1} = X_i + MHA_i(LN(X_i))
                 + MLP_i(LN(X_i + MHA_i(LN(X_i))) + LN(MHA_1(LN(X_1))))
+* Parallel block (the configuration Sec. 5 compares against, after GPT-J and
+  PaLM): MHA and MLP read the same block input, each through its own
+  LayerNorm:
+      X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i))
 
 Readings taken where the paper is silent (each listed in the design notes):
   - the "LN(X_i)" at the MLP input is the block's own second LayerNorm
@@ -34,6 +38,8 @@ Readings taken where the paper is silent (each listed in the design notes):
     reading of Sec. 4.1);
   - FAL+ block 1 is the standard GPT block (the printed first case has a
     misplaced parenthesis);
+  - the parallel block keeps GPT-2's two LayerNorms (LN1 before MHA, LN2
+    before the MLP), both applied to X_i;
   - GPT-2 conventions: tanh GELU, eps 1e-5, biases on every linear layer,
     learned position embedding, final LayerNorm, LM head tied to wte,
     no dropout; next-token cross-entropy averaged over B*T positions;
@@ -52,7 +58,7 @@ import math
 
 import numpy as np
 
-ARCH_GPT, ARCH_FAL, ARCH_FALPLUS = 0, 1, 2
+ARCH_GPT, ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL = 0, 1, 2, 3
 
 f64 = np.float64
 
@@ -245,6 +251,11 @@ def block_forward(cfg, i, x, p, first):
         h2, c["ln2"] = layer_norm(x, p["ln2_g"], p["ln2_b"], eps)
         u = h2 + first["F"]
         xm = x + a
+    elif cfg.arch == ARCH_PARALLEL:
+        # MHA and MLP both read X_i
+        h2, c["ln2"] = layer_norm(x, p["ln2_g"], p["ln2_b"], eps)
+        u = h2
+        xm = x + a
     elif cfg.arch == ARCH_FALPLUS:
         # FAL+ (Appendix D), i >= 2 in the paper's numbering.
         xm = x + a
@@ -287,6 +298,10 @@ def block_backward(cfg, i, dy, p, c, first, dfirst):
             dA1, grads["lnF_g"], grads["lnF_b"] = layer_norm_backward(
                 dfirst["F"], first["lnF"], p["lnF_g"])
             da = da + dA1
+    elif cfg.arch == ARCH_PARALLEL:
+        dx_ln2, grads["ln2_g"], grads["ln2_b"] = layer_norm_backward(du, c["ln2"], p["ln2_g"])
+        dx = dy + dx_ln2
+        da = dy
     else:  # FAL+, i >= 1
         dxm_ln, grads["ln2_g"], grads["ln2_b"] = layer_norm_backward(du, c["ln2"], p["ln2_g"])
         grads["lnF_g"] = (du * first["xhatF"]).sum(axis=0)

@@ -1,15 +1,18 @@
 """Model configuration for the FAL / FAL+ / GPT training step.
 
-The fields mirror ``fal_config_t`` in ``include/fal.h`` one to one.  The three
+The fields mirror ``fal_config_t`` in ``include/fal.h`` one to one.  The
 architectures are the Pre-LN GPT block (Sec. 2, Eq. 1), the FAL block
-(Sec. 4.1, Eq. 2) and the FAL+ block (Sec. 5; Appendix D equations).
+(Sec. 4.1, Eq. 2), the FAL+ block (Sec. 5; Appendix D equations) and the
+parallel configuration the paper compares against in Sec. 5 (MHA and MLP
+read the same block input).
 """
 from __future__ import annotations
 
 import dataclasses
 
-ARCH_GPT, ARCH_FAL, ARCH_FALPLUS = 0, 1, 2
-ARCH_NAMES = {"gpt": ARCH_GPT, "fal": ARCH_FAL, "falplus": ARCH_FALPLUS, "fal+": ARCH_FALPLUS}
+ARCH_GPT, ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL = 0, 1, 2, 3
+ARCH_NAMES = {"gpt": ARCH_GPT, "fal": ARCH_FAL, "falplus": ARCH_FALPLUS, "fal+": ARCH_FALPLUS,
+              "parallel": ARCH_PARALLEL}
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED, SCHED_STREAMS_MERGED = 0, 1, 2, 3
 SCHED_NAMES = {"seq": SCHED_SEQ, "streams": SCHED_STREAMS, "merged": SCHED_MERGED,

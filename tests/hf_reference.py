@@ -2,16 +2,17 @@
 (the textbook Pre-LN GPT-2 implementation) in float64 on the CPU, with torch
 autograd for the gradients.
 
-GPT baseline (Eq. 1) is the unmodified library model.  FAL (Eq. 2) and FAL+
-(Appendix D) are expressed by swapping each block's second LayerNorm module
-for one that reroutes its input, everything else (attention, MLP, residual
+GPT baseline (Eq. 1) is the unmodified library model.  FAL (Eq. 2), FAL+
+(Appendix D) and the parallel block (MHA and MLP on the same input) are
+expressed by swapping each block's second LayerNorm module for one that
+reroutes its input, everything else (attention, MLP, residual
 adds, embedding, head, loss, backward) stays the library's own code.
 """
 import numpy as np
 import torch
 from transformers import GPT2Config, GPT2LMHeadModel
 
-from paper_2510_14614_amd.config import ARCH_FAL, ARCH_FALPLUS
+from paper_2510_14614_amd.config import ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL
 
 
 class _RoutedLN2(torch.nn.Module):
@@ -29,6 +30,8 @@ class _RoutedLN2(torch.nn.Module):
                 if st["block1_standard"]:
                     return self.ln2(h)                    # standard block 1 (only emits F)
             return self.ln2(st["x_in"][self.i]) + st["F"]  # LN(X_i) + LN(MHA_1(LN(X_1)))
+        if self.arch == ARCH_PARALLEL:
+            return self.ln2(st["x_in"][self.i])           # LN2(X_i): the block's own input
         if self.arch == ARCH_FALPLUS and self.i > 0:
             return self.ln2(h) + self.lnF(st["A1"])       # LN(X_i + A_i) + LN_i(MHA_1(...))
         return self.ln2(h)

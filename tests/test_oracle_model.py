@@ -18,11 +18,11 @@ import pytest
 
 import oracle
 from paper_2510_14614_amd import get_config, synth
-from paper_2510_14614_amd.config import ARCH_FAL, ARCH_FALPLUS, ARCH_GPT, Config
+from paper_2510_14614_amd.config import ARCH_FAL, ARCH_FALPLUS, ARCH_GPT, ARCH_PARALLEL, Config
 
 import hf_reference
 
-ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS]
+ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL]
 
 
 def _tiny(arch, **kw):
@@ -116,11 +116,32 @@ def test_fal_with_zero_attention_outputs_is_shifted_gpt():
     assert _rel(lf, lg) < 1e-12
 
 
+def test_fal_with_zero_first_attention_ln_is_parallel_bitwise():
+    # gamma_F = beta_F = 0 makes F = 0 exactly, so every FAL MLP reads
+    # LN2(X_i) + 0: the parallel block, bitwise (logits and gradients)
+    cfg = _tiny(ARCH_FAL, n_layer=3)
+    g, blocks = synth.make_params(cfg, seed=13, bf16=False)
+    blocks[0]["lnF_g"][:] = 0.0
+    blocks[0]["lnF_b"][:] = 0.0
+    tok = synth.make_tokens(cfg, seed=14)
+    rf = oracle.train_step(cfg, g, blocks, tok)
+    rp = oracle.train_step(cfg.replace(arch=ARCH_PARALLEL), g, blocks, tok)
+    assert rf["loss"] == rp["loss"]
+    np.testing.assert_array_equal(rf["logits"], rp["logits"])
+    for k in rf["grads_global"]:
+        np.testing.assert_array_equal(rf["grads_global"][k], rp["grads_global"][k])
+    for a, b in zip(rf["grads_blocks"], rp["grads_blocks"]):
+        for k in a:
+            if k in ("lnF_g", "lnF_b"):
+                continue  # FAL still differentiates its (zeroed) LN_F; parallel has none
+            np.testing.assert_array_equal(a[k], b[k])
+
+
 def test_fal_mlp_independent_of_own_attention():
     # Sec. 4.2: in FAL a block's MLP input does not depend on that block's
     # MHA, so changing block i's attention weights (i >= 1) leaves the MLP
     # input of block i bitwise unchanged.  In GPT it changes.
-    for arch, expect_same in ((ARCH_FAL, True), (ARCH_GPT, False), (ARCH_FALPLUS, False)):
+    for arch, expect_same in ((ARCH_FAL, True), (ARCH_GPT, False), (ARCH_FALPLUS, False), (ARCH_PARALLEL, True)):
         cfg = _tiny(arch, n_layer=3)
         g, blocks = synth.make_params(cfg, seed=11, bf16=False)
         tok = synth.make_tokens(cfg, seed=12)
