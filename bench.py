@@ -17,7 +17,8 @@ Also reported, from the same process:
     the stream each GEMM runs on, during K more steps of the same schedule
     run with the aux stream equal to the main stream (identical launches,
     no overlap between kernels, so each span times one kernel);
-  * the same-kernel sequential GPT baseline and FAL+ on the same config
+  * the same-kernel sequential GPT baseline, FAL+, and the parallel block
+    (same schedule as the measured run) on the same config
     (tokens/s and the ratio to it);
   * training_with_optimizer: the same step followed by the AdamW update of
     every parameter (tokens/s and the update's own time and bandwidth);
@@ -54,7 +55,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="gpt2-small")
-    ap.add_argument("--arch", default="fal", choices=["gpt", "fal", "falplus", "fal+"])
+    ap.add_argument("--arch", default="fal", choices=["gpt", "fal", "falplus", "fal+", "parallel"])
     ap.add_argument("--sched", default="streams_merged", choices=["seq", "streams", "merged", "streams_merged"])
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -381,7 +382,8 @@ def main():
 
     if not args.no_compare:
         comp = {}
-        for name, a, s in (("gpt_seq", "gpt", SCHED_SEQ), ("falplus_seq", "falplus", SCHED_SEQ)):
+        for name, a, s in (("gpt_seq", "gpt", SCHED_SEQ), ("falplus_seq", "falplus", SCHED_SEQ),
+                           ("parallel", "parallel", sched)):
             if ARCH_NAMES[a] == arch:
                 continue
             c2 = cfg.replace(arch=ARCH_NAMES[a], sched=s)

@@ -12,6 +12,10 @@
  *   FAL+  (Sec. 5; Appendix D) block 0 is the GPT block; every later block
  *         adds its own LayerNorm of the first attention output to the GPT
  *         MLP input: MLP_i(LN(X_i + A_i) + LN_{F,i}(MHA_1(LN(X_1)))).
+ *   PARALLEL (the configuration Sec. 5 compares against, after GPT-J and
+ *         PaLM) MHA and MLP read the same block input, each through its own
+ *         LayerNorm: X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i)).
+ *         Scheduled like the FAL blocks (two independent branches).
  *
  * MHA = QKV projection, causal scaled-dot-product attention per head,
  * concatenation, output projection; MLP = up-projection, GELU (tanh form by
@@ -57,11 +61,12 @@ typedef enum {
   FAL_ERR_STATE = 5        /* call out of order (e.g. bwd before fwd)     */
 } fal_status_t;
 
-typedef enum { FAL_ARCH_GPT = 0, FAL_ARCH_FAL = 1, FAL_ARCH_FALPLUS = 2 } fal_arch_t;
+typedef enum { FAL_ARCH_GPT = 0, FAL_ARCH_FAL = 1, FAL_ARCH_FALPLUS = 2, FAL_ARCH_PARALLEL = 3 } fal_arch_t;
 typedef enum { FAL_F32 = 0, FAL_BF16 = 1 } fal_dtype_t;
 
 /* How the two branches of a FAL block are issued (Sec. 4.2: in FAL a block's
- * MHA and MLP have no dependency and may run concurrently).
+ * MHA and MLP have no dependency and may run concurrently).  Parallel blocks
+ * are issued the same way.
  *  SEQ     : one stream, branches back to back.
  *  STREAMS : MHA branch on the main stream, MLP branch on the aux stream,
  *            joined with HIP events (same kernels as SEQ).
@@ -73,7 +78,7 @@ typedef enum { FAL_F32 = 0, FAL_BF16 = 1 } fal_dtype_t;
  *            MLP chains), and after the join the output and down
  *            projections as one GEMM over the concatenated inner dimension.
  * GPT and FAL+ blocks have no independent branches; the schedule only
- * affects FAL blocks. */
+ * affects FAL and parallel blocks. */
 typedef enum {
   FAL_SCHED_SEQ = 0, FAL_SCHED_STREAMS = 1, FAL_SCHED_MERGED = 2, FAL_SCHED_STREAMS_MERGED = 3
 } fal_sched_t;
@@ -110,7 +115,8 @@ typedef struct {
  *   LN2_G [d] LN2_B [d] W_FC [d, f] B_FC [f] W_2 [f, d] B_2 [d]
  *   LNF1_G [d] LNF1_B [d]   first-attention LayerNorm: used by block 0 in FAL
  *                           (the single LN_F) and by blocks >= 1 in FAL+
- *                           (LN_{F,i}); unused slots get zero gradients.
+ *                           (LN_{F,i}); unused slots (GPT, parallel) get
+ *                           zero gradients.
  * W_QKV's columns are [Q | K | V], each head h at columns h*head_dim. */
 enum {
   FAL_P_WTE = 0, FAL_P_WPE, FAL_P_LNF_G, FAL_P_LNF_B, FAL_P_NGLOBAL
@@ -158,8 +164,8 @@ fal_status_t fal_destroy(fal_ctx_t* ctx);
  *   x_in, x_out   device fp32 [M, d]; x_out = block output (may not alias x_in)
  *   first_attn    device dtype [M, d].  FAL: block 0 writes F = LN_F(A_1),
  *                 later blocks read it.  FAL+: block 0 writes the shared
- *                 normalisation of A_1, later blocks read it.  GPT: ignored
- *                 (may be NULL).
+ *                 normalisation of A_1, later blocks read it.  GPT and
+ *                 parallel: ignored (may be NULL).
  * Saves the activations block `layer`'s backward needs in the workspace. */
 fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
                            const float* x_in, float* x_out, void* first_attn);
@@ -171,7 +177,8 @@ fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
  *   d_first_attn  device fp32 [M, d] accumulator of the gradient w.r.t. the
  *                 first-attention tensor (FAL: F; FAL+: the normalisation).
  *                 Block n_layer-1 overwrites it, blocks below accumulate,
- *                 block 0 consumes it.  GPT: ignored (may be NULL).
+ *                 block 0 consumes it.  GPT and parallel: ignored (may be
+ *                 NULL).
  *   block_grads   device fp32, one block in the FAL_B_* layout, overwritten */
 fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
                            const float* x_in, const float* dx_out, float* dx_in,

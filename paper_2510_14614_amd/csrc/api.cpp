@@ -66,7 +66,7 @@ const char* validate(const fal_config_t* c) {
   if (c->n_head < 1) return "n_head must be >= 1";
   if (c->d_ff < 8 || c->d_ff % 8) return "d_ff must be a positive multiple of 8";
   if (c->seq_len < 1 || c->batch < 1) return "seq_len and batch must be >= 1";
-  if (c->arch < FAL_ARCH_GPT || c->arch > FAL_ARCH_FALPLUS) return "unknown arch";
+  if (c->arch < FAL_ARCH_GPT || c->arch > FAL_ARCH_PARALLEL) return "unknown arch";
   if (c->dtype != FAL_F32 && c->dtype != FAL_BF16) return "unknown dtype";
   if (c->sched < FAL_SCHED_SEQ || c->sched > FAL_SCHED_STREAMS_MERGED) return "unknown sched";
   if (!(c->ln_eps > 0.f)) return "ln_eps must be > 0";
@@ -177,7 +177,7 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   const Dims D = dims_of(c);
   Carve cv{base};
   const int64_t M = D.M, d = D.d, es = (int64_t)D.es;
-  const bool need_xm = c.arch != FAL_ARCH_FAL;
+  const bool need_xm = c.arch != FAL_ARCH_FAL && c.arch != FAL_ARCH_PARALLEL;
   for (int i = 0; i < D.L; ++i) {
     LayerSlot s{};
     s.mean1 = cv.take<float>(M);
@@ -447,10 +447,13 @@ struct Run {
     const int arch = ctx->cfg.arch;
     hipStream_t sm = ctx->sm;
     warm_params(bp, sm);
-    if (arch == FAL_ARCH_FAL && layer > 0) {
+    // FAL blocks after the first and every parallel block: two independent
+    // branches off the block input (the parallel block has no F term)
+    if ((arch == FAL_ARCH_FAL && layer > 0) || arch == FAL_ARCH_PARALLEL) {
       LnFwdArgs a = lnargs(x, S.mean1, S.rstd1);
       a.g1 = P(bp, FAL_B_LN1_G); a.b1 = P(bp, FAL_B_LN1_B); a.y1 = S.h1;
-      a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2; a.add2 = first;
+      a.g2 = P(bp, FAL_B_LN2_G); a.b2 = P(bp, FAL_B_LN2_B); a.y2 = S.h2;
+      a.add2 = arch == FAL_ARCH_FAL ? first : nullptr;
       ln(a, sm);
       if (merged()) {
         gemm2(1, 0, qkv_prob(S, bp), fc_prob(S, bp), sm);
@@ -638,7 +641,7 @@ struct Run {
       FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_G), D.d, sm));
       FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_B), D.d, sm));
     }
-    if (arch == FAL_ARCH_FAL && layer > 0) {
+    if ((arch == FAL_ARCH_FAL && layer > 0) || arch == FAL_ARCH_PARALLEL) {
       hipStream_t s2 = sm;
       float* part2 = W.part_main;
       if (streams()) { fork(); s2 = ctx->sa; part2 = W.part_aux; }
@@ -648,7 +651,7 @@ struct Run {
       LnBwdArgs a = lnb(x, S.mean1, S.rstd1);
       a.dy1 = W.dh1; a.g1 = P(bp, FAL_B_LN1_G); a.dy2 = W.dh2; a.g2 = P(bp, FAL_B_LN2_G);
       a.dres = dy; a.dx = dx; a.dx_lp = dx_lp;
-      a.dacc = dfirst; a.dacc_overwrite = last;
+      if (arch == FAL_ARCH_FAL) { a.dacc = dfirst; a.dacc_overwrite = last; }
       a.dg1 = G(gb, FAL_B_LN1_G); a.db1 = G(gb, FAL_B_LN1_B);
       a.dg2 = G(gb, FAL_B_LN2_G); a.db2 = G(gb, FAL_B_LN2_B);
       lnbwd(a, sm);
@@ -836,7 +839,8 @@ fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
   if (layer < 0 || layer >= ctx->D.L) return bad(ctx, "layer out of range");
   if (!block_params || !x_in || !x_out) return bad(ctx, "NULL block_params, x_in or x_out");
   if (x_in == x_out) return bad(ctx, "x_out may not alias x_in");
-  if (ctx->cfg.arch != FAL_ARCH_GPT && !first_attn) return bad(ctx, "first_attn is required for FAL and FAL+");
+  const bool uses_first = ctx->cfg.arch == FAL_ARCH_FAL || ctx->cfg.arch == FAL_ARCH_FALPLUS;
+  if (uses_first && !first_attn) return bad(ctx, "first_attn is required for FAL and FAL+");
   ctx->W.first_in = first_attn;
   try {
     Run r(ctx);
@@ -855,7 +859,8 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
   if (!block_params || !x_in || !dx_out || !dx_in || !block_grads)
     return bad(ctx, "NULL block_params, x_in, dx_out, dx_in or block_grads");
   if (dx_in == dx_out) return bad(ctx, "dx_in may not alias dx_out");
-  if (ctx->cfg.arch != FAL_ARCH_GPT && !d_first_attn) return bad(ctx, "d_first_attn is required for FAL and FAL+");
+  const bool uses_first = ctx->cfg.arch == FAL_ARCH_FAL || ctx->cfg.arch == FAL_ARCH_FALPLUS;
+  if (uses_first && !d_first_attn) return bad(ctx, "d_first_attn is required for FAL and FAL+");
   try {
     Run r(ctx);
     const int64_t Md = (int64_t)ctx->D.M * ctx->D.d;

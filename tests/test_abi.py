@@ -46,6 +46,8 @@ def test_named_configs_valid(name):
     (dict(fal_block1_mode=2), fal.FAL_ERR_INVALID_ARG),
     (dict(arch=0, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
     (dict(arch=2, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
+    (dict(arch=3, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
+    (dict(arch=4), fal.FAL_ERR_INVALID_ARG),
     (dict(head_dim=24), fal.FAL_ERR_UNSUPPORTED),
     (dict(vocab=70000), fal.FAL_ERR_UNSUPPORTED),
     (dict(d_model=8192), fal.FAL_ERR_UNSUPPORTED),

@@ -7,14 +7,14 @@ import pytest
 
 import oracle
 from paper_2510_14614_amd import fal, get_config, synth
-from paper_2510_14614_amd.config import (ARCH_FAL, ARCH_FALPLUS, ARCH_GPT, SCHED_MERGED, SCHED_SEQ,
+from paper_2510_14614_amd.config import (ARCH_FAL, ARCH_FALPLUS, ARCH_GPT, ARCH_PARALLEL, SCHED_MERGED, SCHED_SEQ,
                                          SCHED_STREAMS, SCHED_STREAMS_MERGED, Config)
 
 from gpu_helpers import compare_step, gpu_model_step, gpu_stack_step, log
 
 pytestmark = pytest.mark.gpu
 
-ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS]
+ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL]
 SCHEDS = [SCHED_SEQ, SCHED_STREAMS, SCHED_MERGED, SCHED_STREAMS_MERGED]
 
 
@@ -42,6 +42,18 @@ def test_tiny_fal_schedules(sched, dtype):
     tok = synth.make_tokens(cfg, seed=3)
     compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
                  label=f"tiny sched{sched} dt{dtype}")
+
+
+@pytest.mark.parametrize("sched", SCHEDS)
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_tiny_parallel_schedules(sched, dtype):
+    # the parallel block runs on the FAL two-branch schedules
+    cfg = get_config("tiny", arch=ARCH_PARALLEL, dtype=dtype, sched=sched, n_layer=3)
+    log(f"tiny parallel sched={sched} dtype={dtype}")
+    g, blocks = synth.make_params(cfg, seed=18)
+    tok = synth.make_tokens(cfg, seed=19)
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"tiny parallel sched{sched} dt{dtype}")
 
 
 @pytest.mark.parametrize("sched", [SCHED_SEQ, SCHED_STREAMS_MERGED])
@@ -101,7 +113,7 @@ def test_stack_step_shard_shapes(arch, dtype):
 
 
 @pytest.mark.parametrize("hd", [64, 128])
-@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL])
+@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL, ARCH_PARALLEL])
 def test_long_sequence_multi_block_attention(arch, hd):
     # several 128-query blocks with a ragged last block exercise the causal
     # tiling of the matrix-core attention kernels (forward and backward)
