@@ -22,6 +22,8 @@ Also reported, from the same process:
     (tokens/s and the ratio to it);
   * training_with_optimizer: the same step followed by the AdamW update of
     every parameter (tokens/s and the update's own time and bandwidth);
+  * forward_only: the forward step without gradients (fal_model_forward /
+    fal_stack_forward), this architecture and the sequential GPT;
   * cpu_baseline: the fp64 CPU oracle timed on this host on a bounded sample
     (batch 1 of the same config).
 """
@@ -61,6 +63,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-optimizer", action="store_true",
                     help="skip the extra measurement of step + AdamW update")
+    ap.add_argument("--no-forward", action="store_true",
+                    help="skip the extra forward-only measurement (FAL and GPT)")
     ap.add_argument("--cpu-sample-batch", type=int, default=1)
     ap.add_argument("--single-stream", action="store_true",
                     help="run the timed steps with the aux stream equal to the main stream")
@@ -83,13 +87,14 @@ def describe(cfg, arch_name, sched_name):
 
 
 class Runner:
-    def __init__(self, cfg, single_stream=False, optimizer=False):
+    def __init__(self, cfg, single_stream=False, optimizer=False, forward_only=False):
         import torch
 
         from paper_2510_14614_amd import fal, synth
         self.torch = torch
         self.cfg = cfg
         self.optimizer = optimizer
+        self.forward_only = forward_only
         self.hp = fal.ADAMW_PAPER
         main = torch.cuda.current_stream()
         self.F = fal.Fal(cfg, stream_main=main, stream_aux=main if single_stream else None)
@@ -107,6 +112,12 @@ class Runner:
             self.F.init_optimizer()
 
     def step(self):
+        if self.forward_only:
+            if self.cfg.has_embed_head:
+                self.F.model_forward(self.tok)
+            else:
+                self.F.stack_forward(self.x1)
+            return
         if self.cfg.has_embed_head:
             self.F.model_step(self.tok)
         else:
@@ -416,6 +427,18 @@ def main():
             "optimizer_GB/s": po["bytes"] / max(po["ms"], 1e-9) / 1e6,
             "optimizer_frac_hbm_peak": po["bytes"] / max(po["ms"], 1e-9) / 1e6 / PEAK_HBM_GBS,
         }
+
+    if not args.no_forward:
+        # forward step without gradients (the paper's inference measurement),
+        # this architecture and the same-kernel sequential GPT
+        fo = {}
+        for name, c2 in (("this", cfg), ("gpt_seq", cfg.replace(arch=ARCH_NAMES["gpt"], sched=SCHED_SEQ))):
+            rf = Runner(c2, single_stream=args.single_stream, forward_only=True)
+            ms_f, _ = rf.time(args.steps, args.warmup)
+            rf.close()
+            fo[name] = {"tokens_per_s": c2.tokens / (ms_f / 1000.0), "ms_per_forward": ms_f}
+        fo["speedup_over_gpt_same_kernels"] = fo["gpt_seq"]["ms_per_forward"] / fo["this"]["ms_per_forward"]
+        out["forward_only"] = fo
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)

@@ -246,6 +246,24 @@ fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step,
                             float* master, void* params, const float* grads, float* m, float* v,
                             float* grad_norm);
 
+/* Forward pass only, without gradients (the paper's inference measurement,
+ * Appendix D.3, times this forward step as the time to first token).
+ * Same kernels and schedule as the forward half of fal_model_step; the GELU
+ * derivative the backward would need is not written.
+ *   params  device, dtype, full layout      tokens  device int32 [B, T+1]
+ *   loss    device fp32 scalar or NULL: mean next-token cross-entropy
+ *           (targets tokens[:, 1:]), bitwise equal to fal_model_step's
+ *   logits  device fp32 [B*T, V] or NULL (widened from the dtype logits)
+ * has_embed_head must be 1. */
+fal_status_t fal_model_forward(fal_ctx_t* ctx, const void* params, const int32_t* tokens,
+                               float* loss, float* logits);
+
+/* Forward of the block stack only (has_embed_head == 0).
+ *   x_in   device fp32 [M, d]
+ *   x_out  device fp32 [M, d] or NULL; receives X_L (also readable through
+ *          fal_residual_out); may not alias x_in */
+fal_status_t fal_stack_forward(fal_ctx_t* ctx, const void* params, const float* x_in, float* x_out);
+
 /* Device pointer to the final block output X_L (fp32 [M, d]) held in the
  * workspace after a step; valid until the next step. */
 fal_status_t fal_residual_out(fal_ctx_t* ctx, const float** x_last);

@@ -314,6 +314,7 @@ struct Run {
   fal_ctx* ctx;
   DType dt;
   int tanh;
+  bool fwd_only = false;  // forward without a backward: GELU' is not kept
   explicit Run(fal_ctx* c) : ctx(c), dt(c->cfg.dtype == FAL_BF16 ? BF16 : F32), tanh(c->cfg.gelu_tanh) {}
 
   const char* P(const void* base, int k) const {
@@ -376,7 +377,7 @@ struct Run {
     GemmProblem p = prob(S.h2, D.d, P(bp, FAL_B_W_FC), D.f, D.M, D.f, D.d);
     p.epi = EPI_GELU; p.bias = P(bp, FAL_B_B_FC);
     p.out = off(S.og, D.dA); p.ldo = D.dA + D.f;
-    p.out2 = S.dgelu; p.ldo2 = D.f;
+    p.out2 = fwd_only ? nullptr : S.dgelu; p.ldo2 = D.f;
     return p;
   }
   // out-projection: A = O (first dA columns of og)
@@ -948,6 +949,76 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       FAL_TRY(embed_bwd(D.B, D.T, D.d, cur, grads + Lo.goff[FAL_P_WTE], grads + Lo.goff[FAL_P_WPE], W.keys, W.dh1,
                         sm));
     }
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_model_forward(fal_ctx_t* ctx, const void* params, const int32_t* tokens, float* loss,
+                               float* logits) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (!ctx->cfg.has_embed_head) return bad(ctx, "fal_model_forward needs has_embed_head = 1 (use fal_stack_forward)");
+  if (!params || !tokens) return bad(ctx, "NULL params or tokens");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  Work& W = ctx->W;
+  hipStream_t sm = ctx->sm;
+  const int64_t Md = (int64_t)D.M * D.d;
+  const char* pb = static_cast<const char*>(params);
+  auto gparam = [&](int k) { return pb + Lo.goff[k] * (int64_t)D.es; };
+  auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
+  W.first_in = W.first;
+  try {
+    Run r(ctx);
+    r.fwd_only = true;
+    {
+      Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * (2.0 * D.es + 4.0));
+      FAL_TRY(embed_fwd(r.dt, tokens, D.B, D.T, D.V, D.d, gparam(FAL_P_WTE), gparam(FAL_P_WPE), W.resid, sm));
+    }
+    for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), W.resid + i * Md, W.resid + (i + 1) * Md, W.first);
+    const float* xl = W.resid + (int64_t)D.L * Md;
+    {
+      LnFwdArgs a = r.lnargs(xl, W.meanf, W.rstdf);
+      a.g1 = gparam(FAL_P_LNF_G); a.b1 = gparam(FAL_P_LNF_B); a.y1 = W.hf;
+      r.ln(a, sm);
+    }
+    GemmProblem ph = Run::prob(W.hf, D.d, gparam(FAL_P_WTE), D.d, D.M, D.V, D.d);
+    ph.epi = EPI_STORE; ph.out_f32 = r.dt == F32; ph.out = W.logits; ph.ldo = D.Vp;
+    r.gemm1(1, 1, ph, sm);
+    if (loss) {
+      Span span(ctx, FAL_PROF_CE, sm, 0.0, (double)D.M * (double)D.es * D.V);
+      FAL_TRY(cross_entropy(r.dt, W.logits, D.Vp, tokens, D.B, D.T, D.V, nullptr, D.Vp, W.row_loss, loss, sm));
+    }
+    if (logits) FAL_TRY(rows_to_f32(r.dt, W.logits, D.Vp, logits, D.V, D.M, D.V, sm));
+  } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_stack_forward(fal_ctx_t* ctx, const void* params, const float* x_in, float* x_out) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
+  if (ctx->cfg.has_embed_head) return bad(ctx, "fal_stack_forward needs has_embed_head = 0");
+  if (!params || !x_in) return bad(ctx, "NULL params or x_in");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  Work& W = ctx->W;
+  const int64_t Md = (int64_t)D.M * D.d;
+  if (x_out && x_out == x_in) return bad(ctx, "x_out may not alias x_in");
+  const char* pb = static_cast<const char*>(params);
+  auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
+  auto xin = [&](int i) { return i == 0 ? x_in : W.resid + i * Md; };
+  W.first_in = W.first;
+  try {
+    Run r(ctx);
+    r.fwd_only = true;
+    for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), xin(i), W.resid + (i + 1) * Md, W.first);
+    if (x_out)
+      FAL_TRY(hipMemcpyAsync(x_out, W.resid + (int64_t)D.L * Md, Md * sizeof(float), hipMemcpyDeviceToDevice,
+                             ctx->sm));
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }

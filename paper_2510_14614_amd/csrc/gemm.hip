@@ -37,7 +37,7 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int m, int n, flo
     case EPI_GELU: {
       float gv, dg;
       gelu_and_grad(v, gelu_tanh, gv, dg);
-      static_cast<S*>(P.out2)[(int64_t)m * P.ldo2 + n] = from_f<S>(dg);
+      if (P.out2) static_cast<S*>(P.out2)[(int64_t)m * P.ldo2 + n] = from_f<S>(dg);
       static_cast<S*>(P.out)[(int64_t)m * P.ldo + n] = from_f<S>(gv);
       break;
     }
@@ -317,7 +317,7 @@ __device__ __forceinline__ void apply4(const GemmProblem& P, int m, int n, float
       float g[4], dg[4];
 #pragma unroll
       for (int c = 0; c < 4; ++c) gelu_and_grad(v[c], gelu_tanh, g[c], dg[c]);
-      st4(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n, dg);
+      if (P.out2) st4(static_cast<bf16*>(P.out2) + (int64_t)m * P.ldo2 + n, dg);
       st4(static_cast<bf16*>(P.out) + o, g);
     } else if (EPI == EPI_RESID) {
       const float4 r = *reinterpret_cast<const float4*>(P.resid + (int64_t)m * P.ldr + n);
@@ -341,7 +341,7 @@ __device__ __forceinline__ void apply4(const GemmProblem& P, int m, int n, float
       } else if (EPI == EPI_GELU) {
         float g, dg;
         gelu_and_grad(v[c], gelu_tanh, g, dg);
-        static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + c] = from_f<bf16>(dg);
+        if (P.out2) static_cast<bf16*>(P.out2)[(int64_t)m * P.ldo2 + n + c] = from_f<bf16>(dg);
         static_cast<bf16*>(P.out)[oc] = from_f<bf16>(g);
       } else if (EPI == EPI_RESID) {
         static_cast<float*>(P.out)[oc] = P.resid[(int64_t)m * P.ldr + n + c] + v[c];
@@ -1355,7 +1355,7 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       if (P.bias) ok = ok && al(P.bias, 8);
       if (P.bias2) ok = ok && al(P.bias2, 8);
       if (P.epi == EPI_RESID) ok = ok && al(P.resid, 16) && P.ldr % 4 == 0;
-      if (P.epi == EPI_GELU) ok = ok && P.out2 && al(P.out2, 8) && P.ldo2 % 4 == 0;
+      if (P.epi == EPI_GELU && P.out2) ok = ok && al(P.out2, 8) && P.ldo2 % 4 == 0;
       if (P.epi == EPI_MUL_AUX) ok = ok && P.aux && al(P.aux, 8) && P.ldaux % 4 == 0;
       P.vec_out = ok ? 1 : 0;
     }

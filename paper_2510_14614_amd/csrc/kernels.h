@@ -19,7 +19,7 @@ enum DType : int { F32 = 0, BF16 = 1 };
 // A and B hold the storage dtype of the launch; accumulation is fp32.
 enum Epi : int {
   EPI_STORE = 0,     // out = acc + bias (+ bias2)          (out: f32 or dtype)
-  EPI_GELU = 1,      // v = acc + bias: out = GELU(v), out2 = GELU'(v)   (dtype)
+  EPI_GELU = 1,      // v = acc + bias: out = GELU(v), out2 = GELU'(v) if out2   (dtype)
   EPI_RESID = 2,     // out(f32) = resid(f32) + acc + bias   (resid may equal out)
   EPI_MUL_AUX = 3,   // out = acc * aux (aux = GELU' saved by EPI_GELU)  (aux, out: dtype)
 };
@@ -196,7 +196,8 @@ int64_t embed_bwd_scratch(int M);
 
 // Cross-entropy over rows of logits [M, V] (dtype: fp32 or bf16, row
 // stride ldl) with targets tokens[b, t + 1].  Writes dlogits =
-// (softmax - onehot) / M as dtype [M, ldd] (columns V..ldd-1 zeroed) and
+// (softmax - onehot) / M as dtype [M, ldd] (columns V..ldd-1 zeroed;
+// skipped when dlogits is NULL, ldd still a multiple of 4 >= V) and
 // per-row loss (fp32 [M]); then loss = mean(row_loss) (fp32 scalar,
 // fixed-order reduction).  Softmax, log-sum-exp and loss are fp32.
 hipError_t cross_entropy(DType dt, const void* logits, int64_t ldl, const int32_t* tokens, int B,

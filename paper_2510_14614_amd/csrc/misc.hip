@@ -232,6 +232,7 @@ __global__ __launch_bounds__(kCeThreads) void ce_rows(const S* logits, int64_t l
   for (int w = 1; w < kCeThreads / FAL_WAVE; ++w) lse_combine(gm, gs, rm[w], rs[w]);
   const float lse = gm + __logf(gs);
   if (tid == 0) row_loss[m] = lse - to_f(l[tgt]);
+  if (!dl) return;  // loss only
   const float sc = lm == -INFINITY ? 0.f : __expf(lm - lse) * inv_n;
   S* drow = dl + (int64_t)m * ldd;
 #pragma unroll

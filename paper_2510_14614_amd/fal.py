@@ -28,6 +28,7 @@ ABI_FUNCTIONS = (
     "fal_validate_config", "fal_param_layout", "fal_workspace_bytes", "fal_init", "fal_destroy",
     "fal_block_fwd", "fal_block_bwd", "fal_model_step", "fal_stack_step", "fal_residual_out",
     "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error", "fal_adamw_step",
+    "fal_model_forward", "fal_stack_forward",
 )
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM, PROF_CE, PROF_EMBED, PROF_BIAS, PROF_OPTIM = range(8)
 PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm",
@@ -86,6 +87,8 @@ def lib():
                                     c_void_p, c_void_p]
         L.fal_model_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_stack_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fal_model_forward.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fal_stack_forward.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_residual_out.argtypes = [c_void_p, POINTER(c_void_p)]
         L.fal_profile_enable.argtypes = [c_void_p, c_int32]
         L.fal_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_int64), POINTER(c_double),
@@ -243,6 +246,19 @@ class Fal:
                                     c_void_p(self.loss.data_ptr()), lp, c_void_p(self.grads.data_ptr())),
                self.ctx)
         return self.loss
+
+    def model_forward(self, tokens, logits=None, loss=True):
+        """Forward only (no gradients).  Returns the loss tensor (device [1])
+        when loss is True, else None."""
+        assert tokens.dtype == self.torch.int32 and tokens.is_cuda and tokens.is_contiguous()
+        lp = c_void_p(logits.data_ptr()) if logits is not None else None
+        _check(lib().fal_model_forward(self.ctx, c_void_p(self.params.data_ptr()), c_void_p(tokens.data_ptr()),
+                                       c_void_p(self.loss.data_ptr()) if loss else None, lp), self.ctx)
+        return self.loss if loss else None
+
+    def stack_forward(self, x_in, x_out=None):
+        _check(lib().fal_stack_forward(self.ctx, c_void_p(self.params.data_ptr()), c_void_p(x_in.data_ptr()),
+                                       c_void_p(x_out.data_ptr()) if x_out is not None else None), self.ctx)
 
     def stack_step(self, x_in, dy, dx_in=None):
         _check(lib().fal_stack_step(self.ctx, c_void_p(self.params.data_ptr()), c_void_p(x_in.data_ptr()),
