@@ -12,8 +12,8 @@
  *   FAL+  (Sec. 5; Appendix D) block 0 is the GPT block; every later block
  *         adds its own LayerNorm of the first attention output to the GPT
  *         MLP input: MLP_i(LN(X_i + A_i) + LN_{F,i}(MHA_1(LN(X_1)))).
- *   PARALLEL (the configuration Sec. 5 compares against, after GPT-J and
- *         PaLM) MHA and MLP read the same block input, each through its own
+ *   PARALLEL (the configuration Sec. 6.1 and 6.4 compare against, after
+ *         GPT-J and PaLM) MHA and MLP read the same block input, each through its own
  *         LayerNorm: X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i)).
  *         Scheduled like the FAL blocks (two independent branches).
  *

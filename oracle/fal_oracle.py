@@ -21,8 +21,8 @@ the paper and 0-based here):
   output to its usual MLP input:
       X_{i+1} = X_i + MHA_i(LN(X_i))
                 + MLP_i(LN(X_i + MHA_i(LN(X_i))) + LN(MHA_1(LN(X_1))))
-* Parallel block (the configuration Sec. 5 compares against, after GPT-J and
-  PaLM): MHA and MLP read the same block input, each through its own
+* Parallel block (the configuration Sec. 6.1 and Sec. 6.4 compare against,
+  after GPT-J and PaLM): MHA and MLP read the same block input, each through its own
   LayerNorm:
       X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i))
 

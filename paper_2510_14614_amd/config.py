@@ -3,8 +3,8 @@
 The fields mirror ``fal_config_t`` in ``include/fal.h`` one to one.  The
 architectures are the Pre-LN GPT block (Sec. 2, Eq. 1), the FAL block
 (Sec. 4.1, Eq. 2), the FAL+ block (Sec. 5; Appendix D equations) and the
-parallel configuration the paper compares against in Sec. 5 (MHA and MLP
-read the same block input).
+parallel configuration the paper compares against in Sec. 6.1 and 6.4
+(MHA and MLP read the same block input).
 """
 from __future__ import annotations
 
