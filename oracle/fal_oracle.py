@@ -40,6 +40,10 @@ Readings taken where the paper is silent (each listed in the design notes):
     misplaced parenthesis);
   - the parallel block keeps GPT-2's two LayerNorms (LN1 before MHA, LN2
     before the MLP), both applied to X_i;
+  - the bidirectional mask (config bidirectional = 1) is only the attention
+    mask of the masked-language-model study's encoder blocks (Sec. 6.4,
+    after Cramming); it applies to the block stack, whose MLM head and
+    loss are outside this path;
   - GPT-2 conventions: tanh GELU, eps 1e-5, biases on every linear layer,
     learned position embedding, final LayerNorm, LM head tied to wte,
     no dropout; next-token cross-entropy averaged over B*T positions;
@@ -122,21 +126,30 @@ def gelu_grad(x, tanh_form=True):
     return cdf + x * pdf
 
 
-def causal_attention(q, k, v):
-    """Scaled dot-product attention of each head with a causal mask
-    (query t sees keys 0..t).  q, k, v: [B, H, T, hd]."""
+def attention(q, k, v, causal=True):
+    """Scaled dot-product attention of each head; with the causal mask
+    query t sees keys 0..t, without it (the bidirectional encoder of the
+    masked-language-model study) every key of its sequence.
+    q, k, v: [B, H, T, hd]."""
     hd = q.shape[-1]
     T = q.shape[-2]
     s = q @ np.swapaxes(k, -1, -2) / math.sqrt(hd)
-    future = np.triu(np.ones((T, T), dtype=bool), k=1)
-    s = np.where(future, -np.inf, s)
+    if causal:
+        future = np.triu(np.ones((T, T), dtype=bool), k=1)
+        s = np.where(future, -np.inf, s)
     s = s - s.max(axis=-1, keepdims=True)
     p = np.exp(s)
     p = p / p.sum(axis=-1, keepdims=True)
     return p @ v, p
 
 
+def causal_attention(q, k, v):
+    return attention(q, k, v, causal=True)
+
+
 def causal_attention_backward(do, q, k, v, p):
+    """Backward of attention given its probabilities p (any mask: masked
+    entries of p are zero)."""
     hd = q.shape[-1]
     scale = 1.0 / math.sqrt(hd)
     dv = np.swapaxes(p, -1, -2) @ do
@@ -180,7 +193,7 @@ def mha_forward(h, p, cfg):
     q = _split_heads(qkv[:, :dA], B, T, H)
     k = _split_heads(qkv[:, dA:2 * dA], B, T, H)
     v = _split_heads(qkv[:, 2 * dA:], B, T, H)
-    o4, prob = causal_attention(q, k, v)
+    o4, prob = attention(q, k, v, causal=not getattr(cfg, "bidirectional", 0))
     o = _merge_heads(o4)
     a = o @ p["w_o"] + p["b_o"]
     return a, (h, q, k, v, prob, o)

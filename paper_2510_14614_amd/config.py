@@ -36,6 +36,7 @@ class Config:
     gelu_tanh: int = 1        # 1: tanh approximation, 0: erf form
     has_embed_head: int = 1   # 0: block stack only (no embedding, no LM head)
     fal_block1_mode: int = 0  # FAL only: 0 Eq. 2 in block 1 too, 1 standard block 1 emitting F
+    bidirectional: int = 0    # 1: no attention mask (encoder blocks; block stack only)
 
     @property
     def d_attn(self) -> int:
@@ -50,9 +51,13 @@ class Config:
 
     def train_flops_per_token(self) -> float:
         """Algorithmic training FLOPs per token: forward+backward counted as
-        three forwards, causal attention at (T+1)/2 keys per query, tied head."""
+        three forwards, causal attention at (T+1)/2 keys per query (T keys
+        when bidirectional), tied head."""
         d, dA, f, T, V = self.d_model, self.d_attn, self.d_ff, self.seq_len, self.vocab
-        per_layer = 2 * d * 3 * dA + 2 * dA * d + 4 * d * f + 2 * dA * (T + 1)
+        # QK^T and PV: 4 dA FLOPs per (query, key); (T+1)/2 keys per query
+        # under the causal mask, T without it
+        keys = 2 * T if self.bidirectional else T + 1
+        per_layer = 2 * d * 3 * dA + 2 * dA * d + 4 * d * f + 2 * dA * keys
         head = 2 * d * V if self.has_embed_head else 0
         return 3.0 * (self.n_layer * per_layer + head)
 

@@ -244,6 +244,44 @@ def test_finite_differences_block_stack(arch):
 
 
 @pytest.mark.parametrize("arch", ARCHS)
+def test_finite_differences_bidirectional_block_stack(arch):
+    cfg = _micro(arch, has_embed_head=0, bidirectional=1)
+    _, blocks = _scaled_micro_params(cfg.replace(has_embed_head=1), seed=26)
+    rng = np.random.default_rng(27)
+    x1 = rng.normal(size=(cfg.tokens, cfg.d_model))
+    gout = rng.normal(size=(cfg.tokens, cfg.d_model))
+    r = oracle.stack_step(cfg, blocks, x1, gout)
+    loss_fn = lambda: oracle.stack_step(cfg, blocks, x1, gout)["loss"]
+    for i, b in enumerate(blocks):
+        _fd_check(loss_fn, b, r["grads_blocks"][i], rtol=1e-5, atol=1e-8)
+    _fd_check(loss_fn, {"x1": x1}, {"x1": r["dx1"]}, rtol=1e-5, atol=1e-8)
+
+
+@pytest.mark.parametrize("arch", ARCHS)
+def test_bidirectional_stack_is_position_equivariant(arch):
+    # the block stack carries no position information, so without the
+    # causal mask permuting the positions of every sequence permutes its
+    # outputs and leaves the parameter gradients unchanged; with the mask
+    # it does not
+    cfg = _tiny(arch, has_embed_head=0, bidirectional=1, n_layer=3)
+    _, blocks = synth.make_params(cfg.replace(has_embed_head=1), seed=28, bf16=False)
+    x1, gout = synth.make_stack_inputs(cfg, seed=29)
+    B, T, d = cfg.batch, cfg.seq_len, cfg.d_model
+    perm = np.random.default_rng(30).permutation(T)
+    pm = lambda a: np.asarray(a, dtype=np.float64).reshape(B, T, d)[:, perm].reshape(B * T, d)
+    for c, equivariant in ((cfg, True), (cfg.replace(bidirectional=0), False)):
+        a = oracle.stack_step(c, blocks, x1, gout)
+        b = oracle.stack_step(c, blocks, pm(x1), pm(gout))
+        same_y = np.allclose(pm(a["y"]), b["y"], rtol=1e-12, atol=1e-13)
+        assert same_y == equivariant
+        if equivariant:
+            np.testing.assert_allclose(pm(a["dx1"]), b["dx1"], rtol=1e-10, atol=1e-12)
+            for ga, gb in zip(a["grads_blocks"], b["grads_blocks"]):
+                for k in ga:
+                    np.testing.assert_allclose(ga[k], gb[k], rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("arch", ARCHS)
 def test_finite_differences_sampled_tiny(arch):
     cfg = _tiny(arch)
     g, blocks = synth.make_params(cfg, seed=25, bf16=False)

@@ -78,20 +78,22 @@ def test_gelu_matches_torch_and_fd(tanh_form):
     np.testing.assert_allclose(oracle.gelu_grad(x, tanh_form), fd, rtol=1e-7, atol=1e-9)
 
 
-def _brute_force_attention(q, k, v):
-    """Explicit loops: o[t] = sum_{s<=t} exp(q.k_s/sqrt(hd)) v_s / sum exp."""
+def _brute_force_attention(q, k, v, causal=True):
+    """Explicit loops: o[t] = sum_s exp(q.k_s/sqrt(hd)) v_s / sum exp over
+    s <= t (causal) or every s."""
     B, H, T, hd = q.shape
     o = np.zeros_like(q)
     for b in range(B):
         for h in range(H):
             for t in range(T):
+                n = t + 1 if causal else T
                 scores = [sum(q[b, h, t, c] * k[b, h, s, c] for c in range(hd)) / math.sqrt(hd)
-                          for s in range(t + 1)]
+                          for s in range(n)]
                 mx = max(scores)
                 w = [math.exp(sc - mx) for sc in scores]
                 z = sum(w)
                 for c in range(hd):
-                    o[b, h, t, c] = sum(w[s] * v[b, h, s, c] for s in range(t + 1)) / z
+                    o[b, h, t, c] = sum(w[s] * v[b, h, s, c] for s in range(n)) / z
     return o
 
 
@@ -100,6 +102,34 @@ def test_attention_brute_force():
     q, k, v = (rng.normal(size=(2, 2, 6, 3)) for _ in range(3))
     o, _ = oracle.causal_attention(q, k, v)
     np.testing.assert_allclose(o, _brute_force_attention(q, k, v), rtol=1e-12, atol=1e-14)
+
+
+def test_bidirectional_attention_brute_force():
+    rng = np.random.default_rng(5)
+    q, k, v = (rng.normal(size=(2, 2, 6, 3)) for _ in range(3))
+    o, _ = oracle.attention(q, k, v, causal=False)
+    np.testing.assert_allclose(o, _brute_force_attention(q, k, v, causal=False), rtol=1e-12, atol=1e-14)
+    # the last query sees every key under either mask
+    oc, _ = oracle.attention(q, k, v, causal=True)
+    np.testing.assert_allclose(o[:, :, -1], oc[:, :, -1], rtol=1e-13, atol=1e-15)
+    # identical keys: every query gets the mean of all values
+    k = np.repeat(rng.normal(size=(1, 1, 1, 3)), 6, axis=2)
+    o, _ = oracle.attention(q[:1, :1], k, v[:1, :1], causal=False)
+    np.testing.assert_allclose(o, np.broadcast_to(v[:1, :1].mean(axis=2, keepdims=True), o.shape),
+                               rtol=1e-13, atol=1e-15)
+
+
+def test_bidirectional_attention_matches_torch_sdpa_and_grads():
+    rng = np.random.default_rng(6)
+    q, k, v, do = (rng.normal(size=(2, 3, 7, 4)) for _ in range(4))
+    o, p = oracle.attention(q, k, v, causal=False)
+    dq, dk, dv = oracle.causal_attention_backward(do, q, k, v, p)
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    to = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=False)
+    to.backward(torch.tensor(do))
+    np.testing.assert_allclose(o, to.detach().numpy(), rtol=1e-11, atol=1e-13)
+    for mine, ref in ((dq, tq), (dk, tk), (dv, tv)):
+        np.testing.assert_allclose(mine, ref.grad.numpy(), rtol=1e-10, atol=1e-12)
 
 
 def test_attention_special_cases():
