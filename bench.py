@@ -81,8 +81,9 @@ def parse():
 
 
 def describe(cfg, arch_name, sched_name):
+    mask = "bidirectional attention" if cfg.bidirectional else "causal attention"
     return (f"{arch_name} training step, L{cfg.n_layer} d{cfg.d_model} H{cfg.n_head}x{cfg.head_dim} "
-            f"f{cfg.d_ff} V{cfg.vocab} T{cfg.seq_len} B{cfg.batch}, bf16 storage / fp32 accumulate, "
+            f"f{cfg.d_ff} V{cfg.vocab} T{cfg.seq_len} B{cfg.batch}, {mask}, bf16 storage / fp32 accumulate, "
             f"{sched_name} schedule")
 
 

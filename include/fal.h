@@ -106,6 +106,13 @@ typedef struct {
                              "preparation stage" reading of Sec. 4.1).  Any
                              other value, or 1 with another arch, is
                              FAL_ERR_INVALID_ARG.                             */
+  int32_t bidirectional;  /* 0: causal attention (query t sees keys 0..t);
+                             1: no mask, every query sees every key of its
+                             sequence: the encoder blocks of the paper's
+                             masked-language-model depth study (Sec. 6.4,
+                             after Cramming).  1 requires has_embed_head = 0
+                             (the MLM head and loss are not part of this
+                             library).                                       */
 } fal_config_t;
 
 /* Parameter tensors.  Global tensors (present only when has_embed_head):

@@ -62,9 +62,11 @@ class Config:
         return 3.0 * (self.n_layer * per_layer + head)
 
 
-# The five workload shapes: a tiny fp32 model, GPT-2-small and GPT-2-medium
-# shaped models, a ~1.3B GPT shape and one GPU's tensor-parallel share of a
-# ~7B block stack (8 of 32 heads, FFN 11008/4).
+# The workload shapes: a tiny fp32 model, GPT-2-small and GPT-2-medium
+# shaped models, a ~1.3B GPT shape, one GPU's tensor-parallel share of a
+# ~7B block stack (8 of 32 heads, FFN 11008/4), and the 48-block encoder
+# stack of the masked-language-model depth study (BERT-Large blocks, no
+# attention mask, sequence 128; one micro-batch of 128 sequences).
 CONFIGS = {
     "tiny": Config(n_layer=2, d_model=64, n_head=4, head_dim=16, d_ff=256, vocab=256,
                    seq_len=32, batch=2, arch=ARCH_FAL, dtype=DTYPE_F32),
@@ -77,6 +79,8 @@ CONFIGS = {
     "7b-tp-shard": Config(n_layer=32, d_model=4096, n_head=8, head_dim=128, d_ff=2752,
                           vocab=0, seq_len=2048, batch=2, arch=ARCH_FAL, dtype=DTYPE_BF16,
                           has_embed_head=0),
+    "mlm-48": Config(n_layer=48, d_model=1024, n_head=16, head_dim=64, d_ff=4096, vocab=0, seq_len=128,
+                     batch=128, arch=ARCH_FAL, dtype=DTYPE_BF16, has_embed_head=0, bidirectional=1),
 }
 
 

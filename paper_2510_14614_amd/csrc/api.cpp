@@ -74,6 +74,9 @@ const char* validate(const fal_config_t* c) {
   if (c->has_embed_head != 0 && c->has_embed_head != 1) return "has_embed_head must be 0 or 1";
   if (c->fal_block1_mode != 0 && c->fal_block1_mode != 1) return "fal_block1_mode must be 0 or 1";
   if (c->fal_block1_mode == 1 && c->arch != FAL_ARCH_FAL) return "fal_block1_mode 1 applies to FAL only";
+  if (c->bidirectional != 0 && c->bidirectional != 1) return "bidirectional must be 0 or 1";
+  if (c->bidirectional && c->has_embed_head)
+    return "bidirectional attention is for the block stack (has_embed_head = 0): the next-token loss needs the causal mask";
   if (c->has_embed_head) {
     if (c->vocab < 1) return "vocab must be >= 1";
     if (c->vocab > 65535) return "vocab above 65535 is not supported";
@@ -393,11 +396,14 @@ struct Run {
     p.bias = P(bp, FAL_B_B_2);
     return p;
   }
+  int causal() const { return ctx->cfg.bidirectional ? 0 : 1; }
+  // twice the keys each query sees on average: T + 1 causal, 2T unmasked
+  double attn_keys2() const { return ctx->cfg.bidirectional ? 2.0 * ctx->D.T : ctx->D.T + 1.0; }
   void attention_fwd(const LayerSlot& S, hipStream_t s) {
     const Dims& D = ctx->D;
-    const double fl = 2.0 * D.B * D.H * (double)D.hd * D.T * (D.T + 1.0);
+    const double fl = 2.0 * D.B * D.H * (double)D.hd * D.T * attn_keys2();
     Span span(ctx, FAL_PROF_ATTN_FWD, s, fl, (double)D.es * D.M * 4.0 * D.dA);
-    FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.hd, S.og, D.dA + D.f, S.lse, s));
+    FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.hd, causal(), S.og, D.dA + D.f, S.lse, s));
   }
   void ln(const LnFwdArgs& a, hipStream_t s) {
     const double row = 4.0 + (double)ctx->D.es * (!!a.y1 + !!a.y2 + !!a.add2 + !!a.xhatF + !!a.xhat_out);
@@ -599,10 +605,10 @@ struct Run {
     gemm1(0, 0, wgrad(S.og, D.dA + D.f, da_lp, D.d, D.dA, D.d, D.M, G(gb, FAL_B_W_O)), s);
     colsum(da, 1, D.d, D.d, G(gb, FAL_B_B_O), part, s);
     {
-      const double fl = 4.0 * D.B * D.H * (double)D.hd * D.T * (D.T + 1.0);
+      const double fl = 4.0 * D.B * D.H * (double)D.hd * D.T * attn_keys2();
       Span span(ctx, FAL_PROF_ATTN_BWD, s, fl, (double)D.es * D.M * 8.0 * D.dA);
-      FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, W.dqkv,
-                       W.Dvec, nullptr, s));
+      FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, causal(),
+                       W.dqkv, W.Dvec, nullptr, s));
     }
     GemmProblem ph = dgrad(W.dqkv, 3 * D.dA, P(bp, FAL_B_W_QKV), D.d, 3 * D.dA, D.M);
     ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.dh1; ph.ldo = D.d;

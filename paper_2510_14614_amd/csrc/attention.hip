@@ -1,6 +1,7 @@
-// Causal scaled-dot-product attention per head (the MHA of Sec. 2), in the
-// blockwise form with an online softmax so that the T x T score matrix is
-// never stored (FlashAttention, which the paper uses on its GPUs).
+// Scaled-dot-product attention per head (the MHA of Sec. 2), causal or (for
+// the bidirectional encoder blocks) unmasked, in the blockwise form with an
+// online softmax so that the T x T score matrix is never stored
+// (FlashAttention, which the paper uses on its GPUs).
 //
 // This file holds the SIMT kernels: fp32 arithmetic on fp32 or bf16
 // storage, any head_dim in {16, 32, 64, 128}.  A workgroup holds 64 query
@@ -8,8 +9,9 @@
 // row; K/V (or Q/dO) tiles of 64 rows are staged in LDS.
 //
 // Backward is deterministic without atomics: one kernel accumulates dK, dV
-// per key block over the query blocks at or after it; a second kernel
-// accumulates dQ per query block over the key blocks at or before it.
+// per key block over the query blocks that see it (at or after it when
+// causal); a second kernel accumulates dQ per query block over the key
+// blocks it sees.
 #include <math.h>
 
 #include "common.h"
@@ -20,8 +22,8 @@ namespace fal {
 constexpr int ABR = 64;  // rows per tile
 
 template <typename S, int HD>
-__global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H, S* O, int64_t ldo,
-                                                     float* lse) {
+__global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H, int causal, S* O,
+                                                     int64_t ldo, float* lse) {
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
   __shared__ float Vs[ABR][HD + 1];
@@ -43,7 +45,7 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
     o[c] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  const int kend = min(T, qb * ABR + ABR);
+  const int kend = causal ? min(T, qb * ABR + ABR) : T;
   for (int k0 = 0; k0 < kend; k0 += ABR) {
     for (int e = tid; e < ABR * HD; e += 256) {
       const int kr = e / HD, c = e % HD, key = k0 + kr;
@@ -62,7 +64,7 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
       p += __shfl_xor(p, 1, FAL_WAVE);
       p += __shfl_xor(p, 2, FAL_WAVE);
       const int key = k0 + j;
-      sc[j] = (key <= t && key < T) ? p : -INFINITY;
+      sc[j] = ((!causal || key <= t) && key < T) ? p : -INFINITY;
       mt = fmaxf(mt, sc[j]);
     }
     if (mt > -INFINITY) {
@@ -121,7 +123,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dot(const S* O, int64_t ldo, con
 template <typename S, int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S* dO, int64_t lddo,
                                                           const float* lse, const float* Dvec, int T,
-                                                          int H, S* dqkv) {
+                                                          int H, int causal, S* dqkv) {
   constexpr int P = HD / 4;
   __shared__ float Qs[ABR][HD + 1];
   __shared__ float dOs[ABR][HD + 1];
@@ -145,7 +147,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S*
     dk[c] = 0.f;
     dv[c] = 0.f;
   }
-  for (int q0 = kb * ABR; q0 < T; q0 += ABR) {
+  for (int q0 = causal ? kb * ABR : 0; q0 < T; q0 += ABR) {
     for (int e = tid; e < ABR * HD; e += 256) {
       const int qr = e / HD, c = e % HD, tq = q0 + qr;
       const bool ok = tq < T;
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S*
       s += __shfl_xor(s, 2, FAL_WAVE);
       dp += __shfl_xor(dp, 1, FAL_WAVE);
       dp += __shfl_xor(dp, 2, FAL_WAVE);
-      const float p = (valid && tq < T && tq >= key) ? expf(s * scale - Ls[j]) : 0.f;
+      const float p = (valid && tq < T && (!causal || tq >= key)) ? expf(s * scale - Ls[j]) : 0.f;
       const float ds = p * (dp - Ds[j]) * scale;
 #pragma unroll
       for (int c = 0; c < P; ++c) {
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S*
 template <typename S, int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* dO, int64_t lddo,
                                                         const float* lse, const float* Dvec, int T,
-                                                        int H, S* dqkv) {
+                                                        int H, int causal, S* dqkv) {
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
   __shared__ float Vs[ABR][HD + 1];
@@ -219,7 +221,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* d
   }
   const float L = valid ? lse[((int64_t)b * H + h) * T + t] : 0.f;
   const float Dt = valid ? Dvec[((int64_t)b * H + h) * T + t] : 0.f;
-  const int kend = min(T, qb * ABR + ABR);
+  const int kend = causal ? min(T, qb * ABR + ABR) : T;
   for (int k0 = 0; k0 < kend; k0 += ABR) {
     for (int e = tid; e < ABR * HD; e += 256) {
       const int kr = e / HD, c = e % HD, key = k0 + kr;
@@ -241,7 +243,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* d
       s += __shfl_xor(s, 2, FAL_WAVE);
       dp += __shfl_xor(dp, 1, FAL_WAVE);
       dp += __shfl_xor(dp, 2, FAL_WAVE);
-      const float p = (valid && key <= t && key < T) ? expf(s * scale - L) : 0.f;
+      const float p = (valid && (!causal || key <= t) && key < T) ? expf(s * scale - L) : 0.f;
       const float ds = p * (dp - Dt) * scale;
 #pragma unroll
       for (int c = 0; c < P; ++c) dq[c] = fmaf(ds, Ks[j][part * P + c], dq[c]);
@@ -267,35 +269,35 @@ static hipError_t dispatch_hd(int hd, F&& f) {
 }
 
 bool attn_mfma_supported(int hd);
-hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
-                                hipStream_t s);
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
+                                float* lse, hipStream_t s);
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
-                                const float* lse, float* Dvec, int B, int T, int H, int hd, void* dqkv,
+                                const float* lse, float* Dvec, int B, int T, int H, int hd, int causal, void* dqkv,
                                 hipStream_t s);
 
-hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo,
+hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
                     float* lse, hipStream_t s) {
-  if (dt == BF16 && attn_mfma_supported(hd)) return attn_fwd_mfma_launch(qkv, B, T, H, hd, O, ldo, lse, s);
+  if (dt == BF16 && attn_mfma_supported(hd)) return attn_fwd_mfma_launch(qkv, B, T, H, hd, causal, O, ldo, lse, s);
   const dim3 grid(H, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
     if (dt == BF16)
       hipLaunchKernelGGL((attn_fwd_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv), T, H,
-                         static_cast<bf16*>(O), ldo, lse);
+                         causal, static_cast<bf16*>(O), ldo, lse);
     else
       hipLaunchKernelGGL((attn_fwd_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv), T,
-                         H, static_cast<float*>(O), ldo, lse);
+                         H, causal, static_cast<float*>(O), ldo, lse);
     return hipGetLastError();
   });
 }
 
 hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const void* dO,
-                    int64_t lddo, const float* lse, int B, int T, int H, int hd, void* dqkv,
+                    int64_t lddo, const float* lse, int B, int T, int H, int hd, int causal, void* dqkv,
                     float* Dvec, float* dq_acc, hipStream_t s) {
   (void)dq_acc;
   // the matrix-core dQ kernel computes D itself
   if (dt == BF16 && attn_mfma_supported(hd))
-    return attn_bwd_mfma_launch(qkv, O, ldo, dO, lddo, lse, Dvec, B, T, H, hd, dqkv, s);
+    return attn_bwd_mfma_launch(qkv, O, ldo, dO, lddo, lse, Dvec, B, T, H, hd, causal, dqkv, s);
   const int64_t nrows = (int64_t)B * H * T;
   if (dt == BF16)
     hipLaunchKernelGGL((attn_bwd_dot<bf16>), dim3(cdiv(nrows, 256)), dim3(256), 0, s,
@@ -310,14 +312,14 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
     constexpr int HD = decltype(c)::value;
     if (dt == BF16) {
       hipLaunchKernelGGL((attn_bwd_dkdv_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
-                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, static_cast<bf16*>(dqkv));
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<bf16*>(dqkv));
       hipLaunchKernelGGL((attn_bwd_dq_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
-                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, static_cast<bf16*>(dqkv));
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<bf16*>(dqkv));
     } else {
       hipLaunchKernelGGL((attn_bwd_dkdv_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
-                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, static_cast<float*>(dqkv));
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<float*>(dqkv));
       hipLaunchKernelGGL((attn_bwd_dq_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
-                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, static_cast<float*>(dqkv));
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<float*>(dqkv));
     }
     return hipGetLastError();
   });

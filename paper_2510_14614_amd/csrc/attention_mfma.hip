@@ -1,5 +1,6 @@
-// Causal attention on the gfx950 matrix cores (bf16 in, fp32 accumulate),
-// head_dim 64 or 128.  Same mathematics as the SIMT kernels in
+// Attention on the gfx950 matrix cores (bf16 in, fp32 accumulate), head_dim
+// 64 or 128, with the causal mask (CAUSAL = true) or without it (the
+// bidirectional encoder blocks: every query sees every key of its sequence).  Same mathematics as the SIMT kernels in
 // attention.hip (blockwise, online softmax, deterministic backward), laid
 // out for v_mfma_f32_32x32x16_bf16:
 //
@@ -138,7 +139,7 @@ __device__ __forceinline__ bf16x8v frag_global(const bf16* src, int64_t ld, int 
 }
 
 // ------------------------------------------------------------- forward --
-template <int HD>
+template <int HD, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, int H, bf16* O, int64_t ldo,
                                                      float* lse) {
   constexpr int KK = HD / 16, NT = HD / 32;
@@ -172,8 +173,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
   constexpr float kSlack = 8.f;
   float mref = -INFINITY, lsum = 0.f;
 
-  const int kend = min(T, qb * 128 + 128);
-  const int wave_kend = min(T, q0 + 32);
+  const int kend = CAUSAL ? min(T, qb * 128 + 128) : T;
+  const int wave_kend = CAUSAL ? min(T, q0 + 32) : T;
   RowTile<HD> rk, rv;
   rk.load(Kg, ld, 0, T, tid);
   rv.load(Vg, ld, 0, T, tid);
@@ -193,13 +194,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
       f32x16v s = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
-      // Only the sub-tile on the diagonal (kb == q0) holds keys after a
-      // query or past T; every earlier one is fully visible.
-      if (kb + 31 > q0) {
+      // Causal: only the sub-tile on the diagonal (kb == q0) holds keys
+      // after a query or past T; every earlier one is fully visible.
+      // Without the mask only the last sub-tile can hold keys past T.
+      if (CAUSAL ? kb + 31 > q0 : kb + 31 >= T) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kb + acc_row(r, g);
-          if (key > tq || key >= T) s[r] = -INFINITY;
+          if ((CAUSAL && key > tq) || key >= T) s[r] = -INFINITY;
         }
       }
       float mx = s[0];
@@ -254,7 +256,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
 // wavefront per SIMD).  PART 1: dV only, PART 2: dK only (head_dim 128:
 // each pass fits two wavefronts per SIMD at the cost of recomputing S in
 // both; used when the grid has enough workgroups to put two on every CU).
-template <int HD, int PART = 0>
+template <int HD, int PART, bool CAUSAL>
 __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bwd_dkdv_mfma(
     const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, bf16* dqkv) {
   constexpr bool DO_V = PART != 2, DO_K = PART != 1;
@@ -292,12 +294,14 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     if constexpr (DO_V) dv[t] = zero16();
   }
 
+  // causal: only the queries at or after this block's keys see them
+  const int qbeg = CAUSAL ? kb0 : 0;
   RowTile<HD> rq, ro;
-  if (kb0 < T) {
-    rq.load(Qg, ld, kb0, T, tid);
-    ro.load(dOg, lddo, kb0, T, tid);
+  if (qbeg < T) {
+    rq.load(Qg, ld, qbeg, T, tid);
+    ro.load(dOg, lddo, qbeg, T, tid);
   }
-  for (int q0 = kb0; q0 < T; q0 += AT) {
+  for (int q0 = qbeg; q0 < T; q0 += AT) {
     __syncthreads();
     rq.store(sQ, q0, T, tid);
     ro.store(sdO, q0, T, tid);
@@ -314,7 +318,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
       const int qs = q0 + 32 * sub;
-      if (qs + 31 < kw || qs >= T) continue;  // whole sub-tile before this wave's keys
+      if ((CAUSAL && qs + 31 < kw) || qs >= T) continue;  // whole sub-tile before this wave's keys
       f32x16v s = zero16(), dp = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
@@ -324,7 +328,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
       // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
       // Q and dO rows and zero L and D, so they add nothing; only the
       // diagonal sub-tile (qs == kw) has queries before this wave's keys.
-      const bool diag = qs < kw + 32;
+      const bool diag = CAUSAL && qs < kw + 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qr = 32 * sub + acc_row(r, g);
@@ -367,7 +371,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
 }
 
 // ----------------------------------------------------------- backward: dQ --
-template <int HD>
+template <int HD, bool CAUSAL>
 // Also computes D = rowsum(dO * O) for its queries and writes it to Dvec
 // for the dK/dV kernel, which runs after it.
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* O, int64_t ldo,
@@ -409,8 +413,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
 #pragma unroll
   for (int t = 0; t < NT; ++t) dq[t] = zero16();
 
-  const int kend = min(T, qb * 128 + 128);
-  const int wave_kend = min(T, q0 + 32);
+  const int kend = CAUSAL ? min(T, qb * 128 + 128) : T;
+  const int wave_kend = CAUSAL ? min(T, q0 + 32) : T;
   RowTile<HD> rk, rv;
   rk.load(Kg, ld, 0, T, tid);
   rv.load(Vg, ld, 0, T, tid);
@@ -436,7 +440,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
       // s[r] = S^T[key kb + acc_row(r, g)][query tq].  Keys past T have
       // zero K and V rows (dS there multiplies a zero K row); only the
       // diagonal sub-tile (kb == q0) has keys after a query.
-      const bool diag = kb + 31 > q0;
+      const bool diag = CAUSAL && kb + 31 > q0;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -L2));
@@ -470,37 +474,54 @@ bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
 
 constexpr int kAttnCUs = 256;  // MI355X compute units
 
-hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, void* O, int64_t ldo, float* lse,
-                                hipStream_t s) {
-  const dim3 grid(H, B, cdiv(T, 128)), block(256);
+template <int HD, bool CAUSAL>
+static void fwd_launch(dim3 grid, hipStream_t s, const bf16* q, int T, int H, bf16* o, int64_t ldo, float* lse) {
+  hipLaunchKernelGGL((attn_fwd_mfma<HD, CAUSAL>), grid, dim3(256), 0, s, q, T, H, o, ldo, lse);
+}
+
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
+                                float* lse, hipStream_t s) {
+  const dim3 grid(H, B, cdiv(T, 128));
   const bf16* q = static_cast<const bf16*>(qkv);
   bf16* o = static_cast<bf16*>(O);
-  if (hd == 64) hipLaunchKernelGGL((attn_fwd_mfma<64>), grid, block, 0, s, q, T, H, o, ldo, lse);
-  else if (hd == 128) hipLaunchKernelGGL((attn_fwd_mfma<128>), grid, block, 0, s, q, T, H, o, ldo, lse);
+  if (hd == 64) causal ? fwd_launch<64, true>(grid, s, q, T, H, o, ldo, lse) : fwd_launch<64, false>(grid, s, q, T, H, o, ldo, lse);
+  else if (hd == 128) causal ? fwd_launch<128, true>(grid, s, q, T, H, o, ldo, lse) : fwd_launch<128, false>(grid, s, q, T, H, o, ldo, lse);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
+template <int HD, bool CAUSAL>
+static void bwd_launch(dim3 grid, hipStream_t s, const bf16* q, const bf16* ob, int64_t ldo, const bf16* d,
+                       int64_t lddo, const float* lse, float* Dvec, int T, int H, bf16* o) {
+  const dim3 block(256);
+  hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, CAUSAL>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+  if constexpr (HD == 128) {
+    if ((int64_t)grid.x * grid.y * grid.z >= 2 * kAttnCUs) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+}
+
 // dQ first (it also writes D = rowsum(dO * O) into Dvec), then dK / dV.
+// head_dim 128 with at least two workgroups per CU: separate dV and dK
+// passes (each fits two wavefronts per SIMD).
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
-                                const float* lse, float* Dvec, int B, int T, int H, int hd, void* dqkv,
+                                const float* lse, float* Dvec, int B, int T, int H, int hd, int causal, void* dqkv,
                                 hipStream_t s) {
-  const dim3 grid(H, B, cdiv(T, 128)), block(256);
+  const dim3 grid(H, B, cdiv(T, 128));
   const bf16* q = static_cast<const bf16*>(qkv);
   const bf16* ob = static_cast<const bf16*>(O);
   const bf16* d = static_cast<const bf16*>(dO);
   bf16* o = static_cast<bf16*>(dqkv);
   if (hd == 64) {
-    hipLaunchKernelGGL((attn_bwd_dq_mfma<64>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
-    hipLaunchKernelGGL((attn_bwd_dkdv_mfma<64>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    if (causal) bwd_launch<64, true>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+    else bwd_launch<64, false>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
   } else if (hd == 128) {
-    hipLaunchKernelGGL((attn_bwd_dq_mfma<128>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
-    if ((int64_t)grid.x * grid.y * grid.z >= 2 * kAttnCUs) {
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 1>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 2>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-    } else {
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<128, 0>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-    }
+    if (causal) bwd_launch<128, true>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+    else bwd_launch<128, false>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
   } else {
     return hipErrorInvalidValue;
   }

@@ -48,6 +48,8 @@ def test_named_configs_valid(name):
     (dict(arch=2, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
     (dict(arch=3, fal_block1_mode=1), fal.FAL_ERR_INVALID_ARG),
     (dict(arch=4), fal.FAL_ERR_INVALID_ARG),
+    (dict(bidirectional=2, has_embed_head=0), fal.FAL_ERR_INVALID_ARG),
+    (dict(bidirectional=1), fal.FAL_ERR_INVALID_ARG),  # needs the block stack
     (dict(head_dim=24), fal.FAL_ERR_UNSUPPORTED),
     (dict(vocab=70000), fal.FAL_ERR_UNSUPPORTED),
     (dict(d_model=8192), fal.FAL_ERR_UNSUPPORTED),

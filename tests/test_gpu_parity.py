@@ -112,6 +112,36 @@ def test_stack_step_shard_shapes(arch, dtype):
     compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"stack a{arch} dt{dtype}")
 
 
+@pytest.mark.parametrize("hd,dtype", [(16, 0), (32, 1), (64, 0), (64, 1), (128, 1)])
+@pytest.mark.parametrize("arch", ARCHS)
+def test_bidirectional_stack_step(arch, hd, dtype):
+    # encoder blocks without the causal mask: every query block sees every
+    # key block; T = 300 leaves ragged last blocks of 32, 64 and 128 rows
+    # (matrix-core kernels at head_dim 64 / 128 in bf16, SIMT otherwise)
+    cfg = Config(n_layer=2, d_model=2 * hd, n_head=2, head_dim=hd, d_ff=264, vocab=0, seq_len=300,
+                 batch=2, arch=arch, dtype=dtype, has_embed_head=0, bidirectional=1,
+                 sched=SCHED_STREAMS_MERGED)
+    log(f"bidirectional stack arch={arch} hd={hd} dtype={dtype}")
+    _, blocks = synth.make_params(cfg, seed=44)
+    x1, gout = synth.make_stack_inputs(cfg, seed=45)
+    ref = oracle.stack_step(cfg, blocks, x1, gout)
+    ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
+    compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"bidir a{arch} hd{hd} dt{dtype}")
+
+
+def test_bidirectional_hd128_wide_grid_split_backward():
+    # 16 heads x 7 sequences x 5 blocks = 560 workgroups: the unmasked dV and
+    # dK passes run as two kernels
+    cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, d_ff=512, vocab=0, seq_len=600,
+                 batch=7, arch=ARCH_FAL, dtype=1, has_embed_head=0, bidirectional=1)
+    log("bidirectional hd128 wide grid")
+    _, blocks = synth.make_params(cfg, seed=46)
+    x1, gout = synth.make_stack_inputs(cfg, seed=47)
+    ref = oracle.stack_step(cfg, blocks, x1, gout)
+    ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
+    compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label="bidir hd128 wide")
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 @pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL, ARCH_PARALLEL])
 def test_long_sequence_multi_block_attention(arch, hd):
