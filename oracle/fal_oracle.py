@@ -40,6 +40,10 @@ Readings taken where the paper is silent (each listed in the design notes):
     misplaced parenthesis);
   - the parallel block keeps GPT-2's two LayerNorms (LN1 before MHA, LN2
     before the MLP), both applied to X_i;
+  - grouped-query attention (config n_kv_head, Appendix E.1 uses two
+    groups): W_QKV's columns are [Q (n_head heads) | K (n_kv_head heads) |
+    V (n_kv_head heads)], query head h reads key/value head
+    h // (n_head / n_kv_head);
   - the bidirectional mask (config bidirectional = 1) is only the attention
     mask of the masked-language-model study's encoder blocks (Sec. 6.4,
     after Cramming); it applies to the block stack, whose MLM head and
@@ -186,13 +190,22 @@ def _merge_heads(x):
     return x.transpose(0, 2, 1, 3).reshape(B * T, H * hd)
 
 
+def kv_heads(cfg):
+    """Number of key/value heads: n_head for MHA, fewer for grouped-query
+    attention (Appendix E.1 uses two groups)."""
+    return getattr(cfg, "n_kv_head", 0) or cfg.n_head
+
+
 def mha_forward(h, p, cfg):
+    """MHA; with grouped-query attention the Hkv key/value heads are each
+    shared by n_head / Hkv consecutive query heads (Ainslie et al.)."""
     B, T, H = cfg.batch, cfg.seq_len, cfg.n_head
-    dA = H * cfg.head_dim
+    Hkv = kv_heads(cfg)
+    dA, dKV = H * cfg.head_dim, Hkv * cfg.head_dim
     qkv = h @ p["w_qkv"] + p["b_qkv"]
     q = _split_heads(qkv[:, :dA], B, T, H)
-    k = _split_heads(qkv[:, dA:2 * dA], B, T, H)
-    v = _split_heads(qkv[:, 2 * dA:], B, T, H)
+    k = np.repeat(_split_heads(qkv[:, dA:dA + dKV], B, T, Hkv), H // Hkv, axis=1)
+    v = np.repeat(_split_heads(qkv[:, dA + dKV:], B, T, Hkv), H // Hkv, axis=1)
     o4, prob = attention(q, k, v, causal=not getattr(cfg, "bidirectional", 0))
     o = _merge_heads(o4)
     a = o @ p["w_o"] + p["b_o"]
@@ -205,6 +218,11 @@ def mha_backward(da, p, cache, cfg):
     grads = {"w_o": o.T @ da, "b_o": da.sum(axis=0)}
     do = _split_heads(da @ p["w_o"].T, B, T, H)
     dq, dk, dv = causal_attention_backward(do, q, k, v, prob)
+    # a shared key/value head collects the gradients of every query head of its group
+    Hkv = kv_heads(cfg)
+    grp = H // Hkv
+    dk = dk.reshape(B, Hkv, grp, T, -1).sum(axis=2)
+    dv = dv.reshape(B, Hkv, grp, T, -1).sum(axis=2)
     dqkv = np.concatenate([_merge_heads(dq), _merge_heads(dk), _merge_heads(dv)], axis=1)
     grads["w_qkv"] = h.T @ dqkv
     grads["b_qkv"] = dqkv.sum(axis=0)

@@ -37,6 +37,19 @@ class Config:
     has_embed_head: int = 1   # 0: block stack only (no embedding, no LM head)
     fal_block1_mode: int = 0  # FAL only: 0 Eq. 2 in block 1 too, 1 standard block 1 emitting F
     bidirectional: int = 0    # 1: no attention mask (encoder blocks; block stack only)
+    n_kv_head: int = 0        # key/value heads (grouped-query attention); 0: n_head
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_kv_head or self.n_head
+
+    @property
+    def d_kv(self) -> int:
+        return self.kv_heads * self.head_dim
+
+    @property
+    def d_qkv(self) -> int:
+        return self.d_attn + 2 * self.d_kv
 
     @property
     def d_attn(self) -> int:
@@ -57,7 +70,7 @@ class Config:
         # QK^T and PV: 4 dA FLOPs per (query, key); (T+1)/2 keys per query
         # under the causal mask, T without it
         keys = 2 * T if self.bidirectional else T + 1
-        per_layer = 2 * d * 3 * dA + 2 * dA * d + 4 * d * f + 2 * dA * keys
+        per_layer = 2 * d * self.d_qkv + 2 * dA * d + 4 * d * f + 2 * dA * keys
         head = 2 * d * V if self.has_embed_head else 0
         return 3.0 * (self.n_layer * per_layer + head)
 

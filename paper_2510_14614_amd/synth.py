@@ -44,7 +44,7 @@ def block_shapes(cfg: Config) -> dict:
     d, dA, f = cfg.d_model, cfg.d_attn, cfg.d_ff
     return {
         "ln1_g": (d,), "ln1_b": (d,),
-        "w_qkv": (d, 3 * dA), "b_qkv": (3 * dA,),
+        "w_qkv": (d, cfg.d_qkv), "b_qkv": (cfg.d_qkv,),
         "w_o": (dA, d), "b_o": (d,),
         "ln2_g": (d,), "ln2_b": (d,),
         "w_fc": (d, f), "b_fc": (f,),

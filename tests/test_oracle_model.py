@@ -365,3 +365,80 @@ def test_finite_differences_fal_block1_standard():
     _fd_check(loss_fn, g, r["grads_global"])
     for i, b in enumerate(blocks):
         _fd_check(loss_fn, b, r["grads_blocks"][i])
+
+
+# ---------------------------------------------------------------------------
+# Grouped-query attention (Appendix E.1: two key/value groups)
+# ---------------------------------------------------------------------------
+
+def _tile_kv(cfg_g, blocks):
+    """MHA parameters whose per-head key/value projections repeat the shared
+    GQA head of each group."""
+    H, Hkv, hd, dA = cfg_g.n_head, cfg_g.kv_heads, cfg_g.head_dim, cfg_g.d_attn
+    grp = H // Hkv
+    cols = [h // grp for h in range(H)]
+    out = []
+    for b in blocks:
+        b = {k: np.asarray(v, dtype=np.float64) for k, v in b.items()}
+        w, bias = b["w_qkv"], b["b_qkv"]
+        kw = np.concatenate([w[:, dA + g * hd:dA + (g + 1) * hd] for g in cols], axis=1)
+        vw = np.concatenate([w[:, dA + Hkv * hd + g * hd:dA + Hkv * hd + (g + 1) * hd] for g in cols], axis=1)
+        kb = np.concatenate([bias[dA + g * hd:dA + (g + 1) * hd] for g in cols])
+        vb = np.concatenate([bias[dA + Hkv * hd + g * hd:dA + Hkv * hd + (g + 1) * hd] for g in cols])
+        b = dict(b)
+        b["w_qkv"] = np.concatenate([w[:, :dA], kw, vw], axis=1)
+        b["b_qkv"] = np.concatenate([bias[:dA], kb, vb])
+        out.append(b)
+    return out
+
+
+def _fold_kv_grad(cfg_g, g_mha):
+    """Gradient of the shared GQA key/value columns: the sum over the query
+    heads of each group of the tiled MHA gradient."""
+    H, Hkv, hd, dA = cfg_g.n_head, cfg_g.kv_heads, cfg_g.head_dim, cfg_g.d_attn
+    grp = H // Hkv
+    parts = [g_mha[..., :dA]]
+    for base in (dA, dA + H * hd):  # K block, then V block of the MHA layout
+        for g in range(Hkv):
+            parts.append(sum(g_mha[..., base + h * hd:base + (h + 1) * hd] for h in range(g * grp, (g + 1) * grp)))
+    return np.concatenate(parts, axis=-1)
+
+
+@pytest.mark.parametrize("arch", ARCHS)
+def test_gqa_is_mha_with_shared_kv_heads(arch):
+    cfg = _tiny(arch, n_kv_head=2)
+    g, blocks = synth.make_params(cfg, seed=50, bf16=False)
+    tok = synth.make_tokens(cfg, seed=51)
+    rg = oracle.train_step(cfg, g, blocks, tok)
+    rm = oracle.train_step(cfg.replace(n_kv_head=0), g, _tile_kv(cfg, blocks), tok)
+    assert abs(rg["loss"] - rm["loss"]) <= 1e-13 * rm["loss"]
+    np.testing.assert_allclose(rg["logits"], rm["logits"], rtol=1e-12, atol=1e-13)
+    for k in rg["grads_global"]:
+        np.testing.assert_allclose(rg["grads_global"][k], rm["grads_global"][k], rtol=1e-10, atol=1e-13)
+    for a, b in zip(rg["grads_blocks"], rm["grads_blocks"]):
+        for k in a:
+            ref = _fold_kv_grad(cfg, b[k]) if k in ("w_qkv", "b_qkv") else b[k]
+            np.testing.assert_allclose(a[k], ref, rtol=1e-10, atol=1e-13, err_msg=k)
+
+
+def test_gqa_with_one_head_per_group_is_mha_bitwise():
+    cfg = _tiny(ARCH_FAL)
+    g, blocks = synth.make_params(cfg, seed=52, bf16=False)
+    tok = synth.make_tokens(cfg, seed=53)
+    a = oracle.train_step(cfg, g, blocks, tok)
+    b = oracle.train_step(cfg.replace(n_kv_head=cfg.n_head), g, blocks, tok)
+    assert a["loss"] == b["loss"]
+    for x, y in zip(a["grads_blocks"], b["grads_blocks"]):
+        for k in x:
+            np.testing.assert_array_equal(x[k], y[k])
+
+
+@pytest.mark.parametrize("arch", ARCHS)
+def test_finite_differences_gqa(arch):
+    cfg = _micro(arch, n_head=4, head_dim=2, n_kv_head=2)
+    g, blocks = _scaled_micro_params(cfg, seed=54)
+    tok = synth.make_tokens(cfg, seed=55, dist="uniform")
+    r = oracle.train_step(cfg, g, blocks, tok)
+    loss_fn = lambda: oracle.train_step(cfg, g, blocks, tok)["loss"]
+    for i, b in enumerate(blocks):
+        _fd_check(loss_fn, b, r["grads_blocks"][i])
