@@ -113,18 +113,25 @@ typedef struct {
                              after Cramming).  1 requires has_embed_head = 0
                              (the MLM head and loss are not part of this
                              library).                                       */
+  int32_t n_kv_head;      /* key/value heads: 0 (or n_head) is multi-head
+                             attention; a divisor of n_head gives grouped-
+                             query attention, query head h reading key/value
+                             head h / (n_head / n_kv_head) (Appendix E.1
+                             evaluates two groups).                          */
 } fal_config_t;
 
 /* Parameter tensors.  Global tensors (present only when has_embed_head):
  *   WTE [V, d], WPE [T, d], LNF_G [d], LNF_B [d].
- * Per-block tensors, identical layout in every block (dA = n_head*head_dim):
- *   LN1_G [d] LN1_B [d] W_QKV [d, 3dA] B_QKV [3dA] W_O [dA, d] B_O [d]
+ * Per-block tensors, identical layout in every block (dA = n_head*head_dim,
+ * dKV = n_kv_head*head_dim, dKV = dA without grouped-query attention):
+ *   LN1_G [d] LN1_B [d] W_QKV [d, dA+2dKV] B_QKV [dA+2dKV] W_O [dA, d] B_O [d]
  *   LN2_G [d] LN2_B [d] W_FC [d, f] B_FC [f] W_2 [f, d] B_2 [d]
  *   LNF1_G [d] LNF1_B [d]   first-attention LayerNorm: used by block 0 in FAL
  *                           (the single LN_F) and by blocks >= 1 in FAL+
  *                           (LN_{F,i}); unused slots (GPT, parallel) get
  *                           zero gradients.
- * W_QKV's columns are [Q | K | V], each head h at columns h*head_dim. */
+ * W_QKV's columns are [Q | K | V], each head h at columns h*head_dim of its
+ * part (Q: n_head heads, K and V: n_kv_head heads each). */
 enum {
   FAL_P_WTE = 0, FAL_P_WPE, FAL_P_LNF_G, FAL_P_LNF_B, FAL_P_NGLOBAL
 };

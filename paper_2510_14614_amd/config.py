@@ -79,7 +79,8 @@ class Config:
 # shaped models, a ~1.3B GPT shape, one GPU's tensor-parallel share of a
 # ~7B block stack (8 of 32 heads, FFN 11008/4), and the 48-block encoder
 # stack of the masked-language-model depth study (BERT-Large blocks, no
-# attention mask, sequence 128; one micro-batch of 128 sequences).
+# attention mask, sequence 128; one micro-batch of 128 sequences), also with
+# grouped-query attention in two groups as in the transformer-variant study.
 CONFIGS = {
     "tiny": Config(n_layer=2, d_model=64, n_head=4, head_dim=16, d_ff=256, vocab=256,
                    seq_len=32, batch=2, arch=ARCH_FAL, dtype=DTYPE_F32),
@@ -94,6 +95,9 @@ CONFIGS = {
                           has_embed_head=0),
     "mlm-48": Config(n_layer=48, d_model=1024, n_head=16, head_dim=64, d_ff=4096, vocab=0, seq_len=128,
                      batch=128, arch=ARCH_FAL, dtype=DTYPE_BF16, has_embed_head=0, bidirectional=1),
+    "mlm-48-gqa2": Config(n_layer=48, d_model=1024, n_head=16, head_dim=64, d_ff=4096, vocab=0, seq_len=128,
+                          batch=128, arch=ARCH_FAL, dtype=DTYPE_BF16, has_embed_head=0, bidirectional=1,
+                          n_kv_head=2),
 }
 
 

@@ -44,6 +44,7 @@ int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
 struct Dims {
   int L, d, H, hd, dA, f, V, Vp, T, B, M;
+  int Hkv, dqkv;  // key/value heads; QKV width dA + 2 * Hkv * hd
   size_t es;  // bytes per stored element
 };
 
@@ -51,6 +52,8 @@ Dims dims_of(const fal_config_t& c) {
   Dims D;
   D.L = c.n_layer; D.d = c.d_model; D.H = c.n_head; D.hd = c.head_dim;
   D.dA = c.n_head * c.head_dim; D.f = c.d_ff;
+  D.Hkv = c.n_kv_head > 0 ? c.n_kv_head : c.n_head;
+  D.dqkv = D.dA + 2 * D.Hkv * c.head_dim;
   D.V = c.has_embed_head ? c.vocab : 0;
   D.Vp = (int)align_up(D.V, 64);
   D.T = c.seq_len; D.B = c.batch; D.M = c.batch * c.seq_len;
@@ -75,6 +78,8 @@ const char* validate(const fal_config_t* c) {
   if (c->fal_block1_mode != 0 && c->fal_block1_mode != 1) return "fal_block1_mode must be 0 or 1";
   if (c->fal_block1_mode == 1 && c->arch != FAL_ARCH_FAL) return "fal_block1_mode 1 applies to FAL only";
   if (c->bidirectional != 0 && c->bidirectional != 1) return "bidirectional must be 0 or 1";
+  if (c->n_kv_head < 0 || (c->n_kv_head > 0 && c->n_head % c->n_kv_head))
+    return "n_kv_head must be 0 or divide n_head";
   if (c->bidirectional && c->has_embed_head)
     return "bidirectional attention is for the block stack (has_embed_head = 0): the next-token loss needs the causal mask";
   if (c->has_embed_head) {
@@ -120,8 +125,8 @@ Layout layout_of(const fal_config_t& c) {
     }
   }
   Lo.block_base = off;
-  const int64_t d = D.d, dA = D.dA, f = D.f;
-  const int64_t bs[FAL_B_NTENSOR] = {d, d, d * 3 * dA, 3 * dA, dA * d, d, d, d, d * f, f, f * d, d, d, d};
+  const int64_t d = D.d, dA = D.dA, f = D.f, q3 = D.dqkv;
+  const int64_t bs[FAL_B_NTENSOR] = {d, d, d * q3, q3, dA * d, d, d, d, d * f, f, f * d, d, d, d};
   int64_t b = 0;
   for (int i = 0; i < FAL_B_NTENSOR; ++i) {
     Lo.boff[i] = b;
@@ -187,7 +192,7 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
     s.rstd1 = cv.take<float>(M);
     s.h1 = cv.take<char>(M * d * es);
     s.h2 = cv.take<char>(M * d * es);
-    s.qkv = cv.take<char>(M * 3 * D.dA * es);
+    s.qkv = cv.take<char>(M * D.dqkv * es);
     s.og = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
     s.dgelu = cv.take<char>(M * D.f * es);
     s.lse = cv.take<float>((int64_t)D.B * D.H * D.T);
@@ -227,12 +232,12 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.dxm_lp = cv.take<char>(M * d * es);
   W.da_lp = cv.take<char>(M * d * es);
   W.dog = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
-  W.dqkv = cv.take<char>(M * 3 * D.dA * es);
+  W.dqkv = cv.take<char>(M * D.dqkv * es);
   W.Dvec = cv.take<float>((int64_t)D.B * D.H * D.T);
   const int64_t part = std::max<int64_t>({ln_bwd_scratch((int)M, (int)d), dot_scratch(M * d)});
   W.part_main = cv.take<float>(part);
   W.part_aux = cv.take<float>(part);
-  W.bias_part = cv.take<float>(col_sum_batch_scratch((int)M, (int)(2 * d + D.f + 3 * D.dA)));
+  W.bias_part = cv.take<float>(col_sum_batch_scratch((int)M, (int)(2 * d + D.f + D.dqkv)));
   // a split is only chosen while fewer than 512 output tiles of 128x128
   // exist, so (512 + 512) tiles of partials bound every split decision
   W.splitk_floats = (int64_t)1024 * 128 * 128;
@@ -371,8 +376,8 @@ struct Run {
   // ----- forward pieces ----------------------------------------------------
   GemmProblem qkv_prob(const LayerSlot& S, const void* bp) {
     const Dims& D = ctx->D;
-    GemmProblem p = prob(S.h1, D.d, P(bp, FAL_B_W_QKV), 3 * D.dA, D.M, 3 * D.dA, D.d);
-    p.epi = EPI_STORE; p.bias = P(bp, FAL_B_B_QKV); p.out = S.qkv; p.ldo = 3 * D.dA;
+    GemmProblem p = prob(S.h1, D.d, P(bp, FAL_B_W_QKV), D.dqkv, D.M, D.dqkv, D.d);
+    p.epi = EPI_STORE; p.bias = P(bp, FAL_B_B_QKV); p.out = S.qkv; p.ldo = D.dqkv;
     return p;
   }
   GemmProblem fc_prob(const LayerSlot& S, const void* bp) {
@@ -402,8 +407,8 @@ struct Run {
   void attention_fwd(const LayerSlot& S, hipStream_t s) {
     const Dims& D = ctx->D;
     const double fl = 2.0 * D.B * D.H * (double)D.hd * D.T * attn_keys2();
-    Span span(ctx, FAL_PROF_ATTN_FWD, s, fl, (double)D.es * D.M * 4.0 * D.dA);
-    FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.hd, causal(), S.og, D.dA + D.f, S.lse, s));
+    Span span(ctx, FAL_PROF_ATTN_FWD, s, fl, (double)D.es * D.M * ((double)D.dqkv + D.dA));
+    FAL_TRY(attn_fwd(dt, S.qkv, D.B, D.T, D.H, D.Hkv, D.hd, causal(), S.og, D.dA + D.f, S.lse, s));
   }
   void ln(const LnFwdArgs& a, hipStream_t s) {
     const double row = 4.0 + (double)ctx->D.es * (!!a.y1 + !!a.y2 + !!a.add2 + !!a.xhatF + !!a.xhat_out);
@@ -606,15 +611,15 @@ struct Run {
     colsum(da, 1, D.d, D.d, G(gb, FAL_B_B_O), part, s);
     {
       const double fl = 4.0 * D.B * D.H * (double)D.hd * D.T * attn_keys2();
-      Span span(ctx, FAL_PROF_ATTN_BWD, s, fl, (double)D.es * D.M * 8.0 * D.dA);
-      FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.hd, causal(),
-                       W.dqkv, W.Dvec, nullptr, s));
+      Span span(ctx, FAL_PROF_ATTN_BWD, s, fl, (double)D.es * D.M * (2.0 * D.dqkv + 2.0 * D.dA));
+      FAL_TRY(attn_bwd(dt, S.qkv, S.og, D.dA + D.f, W.dog, D.dA + D.f, S.lse, D.B, D.T, D.H, D.Hkv, D.hd,
+                       causal(), W.dqkv, W.Dvec, nullptr, s));
     }
-    GemmProblem ph = dgrad(W.dqkv, 3 * D.dA, P(bp, FAL_B_W_QKV), D.d, 3 * D.dA, D.M);
+    GemmProblem ph = dgrad(W.dqkv, D.dqkv, P(bp, FAL_B_W_QKV), D.d, D.dqkv, D.M);
     ph.epi = EPI_STORE; ph.out_f32 = 1; ph.out = W.dh1; ph.ldo = D.d;
     gemm1(1, 1, ph, s);
-    gemm1(0, 0, wgrad(S.h1, D.d, W.dqkv, 3 * D.dA, D.d, 3 * D.dA, D.M, G(gb, FAL_B_W_QKV)), s);
-    colsum(W.dqkv, 0, 3 * D.dA, 3 * D.dA, G(gb, FAL_B_B_QKV), part, s);
+    gemm1(0, 0, wgrad(S.h1, D.d, W.dqkv, D.dqkv, D.d, D.dqkv, D.M, G(gb, FAL_B_W_QKV)), s);
+    colsum(W.dqkv, 0, D.dqkv, D.dqkv, G(gb, FAL_B_B_QKV), part, s);
   }
 
   LnBwdArgs lnb(const float* x, const float* mean, const float* rstd) {

@@ -22,7 +22,7 @@ namespace fal {
 constexpr int ABR = 64;  // rows per tile
 
 template <typename S, int HD>
-__global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H, int causal, S* O,
+__global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H, int Hkv, int causal, S* O,
                                                      int64_t ldo, float* lse) {
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
@@ -31,8 +31,9 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
   // longest (latest) query blocks first
   const int qb = gridDim.z - 1 - blockIdx.z;
   const int h = blockIdx.x, b = blockIdx.y;
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
+  const int dA = H * HD, dKV = Hkv * HD;
+  const int64_t ld = dA + 2 * (int64_t)dKV;
+  const int kcol = dA + (h / (H / Hkv)) * HD, vcol = kcol + dKV;  // the group's key/value head
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
   const int t = qb * ABR + r;
   const bool valid = t < T;
@@ -50,8 +51,8 @@ __global__ __launch_bounds__(256) void attn_fwd_simt(const S* qkv, int T, int H,
     for (int e = tid; e < ABR * HD; e += 256) {
       const int kr = e / HD, c = e % HD, key = k0 + kr;
       const bool ok = key < T;
-      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + dA + h * HD + c]) : 0.f;
-      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + c]) : 0.f;
+      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + kcol + c]) : 0.f;
+      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + vcol + c]) : 0.f;
     }
     __syncthreads();
     float sc[ABR];
@@ -123,72 +124,77 @@ __global__ __launch_bounds__(256) void attn_bwd_dot(const S* O, int64_t ldo, con
 template <typename S, int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S* dO, int64_t lddo,
                                                           const float* lse, const float* Dvec, int T,
-                                                          int H, int causal, S* dqkv) {
+                                                          int H, int Hkv, int causal, S* dqkv) {
   constexpr int P = HD / 4;
   __shared__ float Qs[ABR][HD + 1];
   __shared__ float dOs[ABR][HD + 1];
   __shared__ float Ls[ABR], Ds[ABR];
-  const int kb = blockIdx.z, h = blockIdx.x, b = blockIdx.y;  // causal block index slowest
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
+  // grid (Hkv, B, blocks), causal block index slowest; a key/value head
+  // accumulates over the query heads of its group in order
+  const int kb = blockIdx.z, kvh = blockIdx.x, b = blockIdx.y, grp = H / Hkv;
+  const int dA = H * HD, dKV = Hkv * HD;
+  const int64_t ld = dA + 2 * (int64_t)dKV;
+  const int kcol = dA + kvh * HD, vcol = kcol + dKV;
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
   const int key = kb * ABR + r;
   const bool valid = key < T;
   const float scale = 1.f / sqrtf((float)HD);
   const S* base = qkv + (int64_t)b * T * ld;
   const S* dObase = dO + (int64_t)b * T * lddo;
-  const float* lrow = lse + ((int64_t)b * H + h) * T;
-  const float* drow = Dvec + ((int64_t)b * H + h) * T;
   float k[P], v[P], dk[P], dv[P];
 #pragma unroll
   for (int c = 0; c < P; ++c) {
-    k[c] = valid ? to_f(base[(int64_t)key * ld + dA + h * HD + part * P + c]) : 0.f;
-    v[c] = valid ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + part * P + c]) : 0.f;
+    k[c] = valid ? to_f(base[(int64_t)key * ld + kcol + part * P + c]) : 0.f;
+    v[c] = valid ? to_f(base[(int64_t)key * ld + vcol + part * P + c]) : 0.f;
     dk[c] = 0.f;
     dv[c] = 0.f;
   }
-  for (int q0 = causal ? kb * ABR : 0; q0 < T; q0 += ABR) {
-    for (int e = tid; e < ABR * HD; e += 256) {
-      const int qr = e / HD, c = e % HD, tq = q0 + qr;
-      const bool ok = tq < T;
-      Qs[qr][c] = ok ? to_f(base[(int64_t)tq * ld + h * HD + c]) : 0.f;
-      dOs[qr][c] = ok ? to_f(dObase[(int64_t)tq * lddo + h * HD + c]) : 0.f;
-    }
-    if (tid < ABR) {
-      const int tq = q0 + tid;
-      Ls[tid] = tq < T ? lrow[tq] : 0.f;
-      Ds[tid] = tq < T ? drow[tq] : 0.f;
-    }
-    __syncthreads();
+  for (int h = kvh * grp; h < (kvh + 1) * grp; ++h) {
+    const float* lrow = lse + ((int64_t)b * H + h) * T;
+    const float* drow = Dvec + ((int64_t)b * H + h) * T;
+    for (int q0 = causal ? kb * ABR : 0; q0 < T; q0 += ABR) {
+      for (int e = tid; e < ABR * HD; e += 256) {
+        const int qr = e / HD, c = e % HD, tq = q0 + qr;
+        const bool ok = tq < T;
+        Qs[qr][c] = ok ? to_f(base[(int64_t)tq * ld + h * HD + c]) : 0.f;
+        dOs[qr][c] = ok ? to_f(dObase[(int64_t)tq * lddo + h * HD + c]) : 0.f;
+      }
+      if (tid < ABR) {
+        const int tq = q0 + tid;
+        Ls[tid] = tq < T ? lrow[tq] : 0.f;
+        Ds[tid] = tq < T ? drow[tq] : 0.f;
+      }
+      __syncthreads();
 #pragma unroll 4
-    for (int j = 0; j < ABR; ++j) {
-      const int tq = q0 + j;
-      float s = 0.f, dp = 0.f;
+      for (int j = 0; j < ABR; ++j) {
+        const int tq = q0 + j;
+        float s = 0.f, dp = 0.f;
 #pragma unroll
-      for (int c = 0; c < P; ++c) {
-        s = fmaf(Qs[j][part * P + c], k[c], s);
-        dp = fmaf(dOs[j][part * P + c], v[c], dp);
-      }
-      s += __shfl_xor(s, 1, FAL_WAVE);
-      s += __shfl_xor(s, 2, FAL_WAVE);
-      dp += __shfl_xor(dp, 1, FAL_WAVE);
-      dp += __shfl_xor(dp, 2, FAL_WAVE);
-      const float p = (valid && tq < T && (!causal || tq >= key)) ? expf(s * scale - Ls[j]) : 0.f;
-      const float ds = p * (dp - Ds[j]) * scale;
+        for (int c = 0; c < P; ++c) {
+          s = fmaf(Qs[j][part * P + c], k[c], s);
+          dp = fmaf(dOs[j][part * P + c], v[c], dp);
+        }
+        s += __shfl_xor(s, 1, FAL_WAVE);
+        s += __shfl_xor(s, 2, FAL_WAVE);
+        dp += __shfl_xor(dp, 1, FAL_WAVE);
+        dp += __shfl_xor(dp, 2, FAL_WAVE);
+        const float p = (valid && tq < T && (!causal || tq >= key)) ? expf(s * scale - Ls[j]) : 0.f;
+        const float ds = p * (dp - Ds[j]) * scale;
 #pragma unroll
-      for (int c = 0; c < P; ++c) {
-        dv[c] = fmaf(p, dOs[j][part * P + c], dv[c]);
-        dk[c] = fmaf(ds, Qs[j][part * P + c], dk[c]);
+        for (int c = 0; c < P; ++c) {
+          dv[c] = fmaf(p, dOs[j][part * P + c], dv[c]);
+          dk[c] = fmaf(ds, Qs[j][part * P + c], dk[c]);
+        }
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
   if (valid) {
-    S* row = dqkv + ((int64_t)b * T + key) * ld + h * HD + part * P;
+    S* row = dqkv + ((int64_t)b * T + key) * ld;
 #pragma unroll
     for (int c = 0; c < P; ++c) {
-      row[dA + c] = from_f<S>(dk[c]);
-      row[2 * dA + c] = from_f<S>(dv[c]);
+      row[kcol + part * P + c] = from_f<S>(dk[c]);
+      row[vcol + part * P + c] = from_f<S>(dv[c]);
     }
   }
 }
@@ -196,7 +202,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_simt(const S* qkv, const S*
 template <typename S, int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* dO, int64_t lddo,
                                                         const float* lse, const float* Dvec, int T,
-                                                        int H, int causal, S* dqkv) {
+                                                        int H, int Hkv, int causal, S* dqkv) {
   constexpr int P = HD / 4;
   __shared__ float Ks[ABR][HD + 1];
   __shared__ float Vs[ABR][HD + 1];
@@ -205,8 +211,9 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* d
   // short blocks; the longest (latest) query blocks are dispatched first.
   const int qb = gridDim.z - 1 - blockIdx.z;
   const int h = blockIdx.x, b = blockIdx.y;
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
+  const int dA = H * HD, dKV = Hkv * HD;
+  const int64_t ld = dA + 2 * (int64_t)dKV;
+  const int kcol = dA + (h / (H / Hkv)) * HD, vcol = kcol + dKV;
   const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
   const int t = qb * ABR + r;
   const bool valid = t < T;
@@ -226,8 +233,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_simt(const S* qkv, const S* d
     for (int e = tid; e < ABR * HD; e += 256) {
       const int kr = e / HD, c = e % HD, key = k0 + kr;
       const bool ok = key < T;
-      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + dA + h * HD + c]) : 0.f;
-      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + 2 * dA + h * HD + c]) : 0.f;
+      Ks[kr][c] = ok ? to_f(base[(int64_t)key * ld + kcol + c]) : 0.f;
+      Vs[kr][c] = ok ? to_f(base[(int64_t)key * ld + vcol + c]) : 0.f;
     }
     __syncthreads();
 #pragma unroll 4
@@ -269,35 +276,38 @@ static hipError_t dispatch_hd(int hd, F&& f) {
 }
 
 bool attn_mfma_supported(int hd);
-hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
-                                float* lse, hipStream_t s);
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int Hkv, int hd, int causal, void* O,
+                                int64_t ldo, float* lse, hipStream_t s);
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
-                                const float* lse, float* Dvec, int B, int T, int H, int hd, int causal, void* dqkv,
-                                hipStream_t s);
+                                const float* lse, float* Dvec, int B, int T, int H, int Hkv, int hd, int causal,
+                                void* dqkv, hipStream_t s);
 
-hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
-                    float* lse, hipStream_t s) {
-  if (dt == BF16 && attn_mfma_supported(hd)) return attn_fwd_mfma_launch(qkv, B, T, H, hd, causal, O, ldo, lse, s);
+hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int Hkv, int hd, int causal, void* O,
+                    int64_t ldo, float* lse, hipStream_t s) {
+  if (Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
+  if (dt == BF16 && attn_mfma_supported(hd))
+    return attn_fwd_mfma_launch(qkv, B, T, H, Hkv, hd, causal, O, ldo, lse, s);
   const dim3 grid(H, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
     if (dt == BF16)
       hipLaunchKernelGGL((attn_fwd_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv), T, H,
-                         causal, static_cast<bf16*>(O), ldo, lse);
+                         Hkv, causal, static_cast<bf16*>(O), ldo, lse);
     else
       hipLaunchKernelGGL((attn_fwd_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv), T,
-                         H, causal, static_cast<float*>(O), ldo, lse);
+                         H, Hkv, causal, static_cast<float*>(O), ldo, lse);
     return hipGetLastError();
   });
 }
 
 hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const void* dO,
-                    int64_t lddo, const float* lse, int B, int T, int H, int hd, int causal, void* dqkv,
+                    int64_t lddo, const float* lse, int B, int T, int H, int Hkv, int hd, int causal, void* dqkv,
                     float* Dvec, float* dq_acc, hipStream_t s) {
   (void)dq_acc;
+  if (Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
   // the matrix-core dQ kernel computes D itself
   if (dt == BF16 && attn_mfma_supported(hd))
-    return attn_bwd_mfma_launch(qkv, O, ldo, dO, lddo, lse, Dvec, B, T, H, hd, causal, dqkv, s);
+    return attn_bwd_mfma_launch(qkv, O, ldo, dO, lddo, lse, Dvec, B, T, H, Hkv, hd, causal, dqkv, s);
   const int64_t nrows = (int64_t)B * H * T;
   if (dt == BF16)
     hipLaunchKernelGGL((attn_bwd_dot<bf16>), dim3(cdiv(nrows, 256)), dim3(256), 0, s,
@@ -307,19 +317,19 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const
                        static_cast<const float*>(O), ldo, static_cast<const float*>(dO), lddo, B, T, H, hd, Dvec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 grid(H, B, cdiv(T, ABR)), block(256);
+  const dim3 grid(H, B, cdiv(T, ABR)), gkv(Hkv, B, cdiv(T, ABR)), block(256);
   return dispatch_hd(hd, [&](auto c) {
     constexpr int HD = decltype(c)::value;
     if (dt == BF16) {
-      hipLaunchKernelGGL((attn_bwd_dkdv_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
-                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<bf16*>(dqkv));
+      hipLaunchKernelGGL((attn_bwd_dkdv_simt<bf16, HD>), gkv, block, 0, s, static_cast<const bf16*>(qkv),
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, Hkv, causal, static_cast<bf16*>(dqkv));
       hipLaunchKernelGGL((attn_bwd_dq_simt<bf16, HD>), grid, block, 0, s, static_cast<const bf16*>(qkv),
-                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<bf16*>(dqkv));
+                         static_cast<const bf16*>(dO), lddo, lse, Dvec, T, H, Hkv, causal, static_cast<bf16*>(dqkv));
     } else {
-      hipLaunchKernelGGL((attn_bwd_dkdv_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
-                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<float*>(dqkv));
+      hipLaunchKernelGGL((attn_bwd_dkdv_simt<float, HD>), gkv, block, 0, s, static_cast<const float*>(qkv),
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, Hkv, causal, static_cast<float*>(dqkv));
       hipLaunchKernelGGL((attn_bwd_dq_simt<float, HD>), grid, block, 0, s, static_cast<const float*>(qkv),
-                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, causal, static_cast<float*>(dqkv));
+                         static_cast<const float*>(dO), lddo, lse, Dvec, T, H, Hkv, causal, static_cast<float*>(dqkv));
     }
     return hipGetLastError();
   });

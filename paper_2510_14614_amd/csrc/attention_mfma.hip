@@ -140,8 +140,8 @@ __device__ __forceinline__ bf16x8v frag_global(const bf16* src, int64_t ld, int 
 
 // ------------------------------------------------------------- forward --
 template <int HD, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, int H, bf16* O, int64_t ldo,
-                                                     float* lse) {
+__global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, int H, int Hkv, bf16* O,
+                                                     int64_t ldo, float* lse) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
@@ -150,11 +150,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
   // short blocks; the longest (latest) query blocks are dispatched first.
   const int qb = gridDim.z - 1 - blockIdx.z;
   const int h = blockIdx.x, b = blockIdx.y;
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
+  const int dA = H * HD, dKV = Hkv * HD, kvh = h / (H / Hkv);
+  const int64_t ld = dA + 2 * (int64_t)dKV;
   const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
-  const bf16* Kg = Qg + dA;
-  const bf16* Vg = Qg + 2 * dA;
+  const bf16* Kg = qkv + (int64_t)b * T * ld + dA + kvh * HD;  // shared by the heads of a group
+  const bf16* Vg = Kg + dKV;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
   const int q0 = qb * 128 + wave * 32;
   const int tq = q0 + c;
@@ -258,24 +258,24 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
 // both; used when the grid has enough workgroups to put two on every CU).
 template <int HD, int PART, bool CAUSAL>
 __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bwd_dkdv_mfma(
-    const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, bf16* dqkv) {
+    const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, int Hkv,
+    bf16* dqkv) {
   constexpr bool DO_V = PART != 2, DO_K = PART != 1;
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sQ[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sdO[AT * (HD + 8)];
   __shared__ float sL[AT], sD[AT];
-  // grid (H, B, blocks): causal block index slowest (even XCD mix); the
-  // earliest key blocks see the most queries and are dispatched first
+  // grid (Hkv, B, blocks): causal block index slowest (even XCD mix); the
+  // earliest key blocks see the most queries and are dispatched first.  A
+  // key/value head accumulates over every query head of its group, in order.
   const int kb0 = blockIdx.z * 128;
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
-  const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
-  const bf16* Kg = Qg + dA;
-  const bf16* Vg = Qg + 2 * dA;
-  const bf16* dOg = dO + (int64_t)b * T * lddo + h * HD;
-  const float* Lg = lse + ((int64_t)b * H + h) * T;
-  const float* Dg = Dvec + ((int64_t)b * H + h) * T;
+  const int kvh = blockIdx.x, b = blockIdx.y, grp = H / Hkv;
+  const int dA = H * HD, dKV = Hkv * HD;
+  const int64_t ld = dA + 2 * (int64_t)dKV;
+  const bf16* Qb = qkv + (int64_t)b * T * ld;
+  const bf16* Kg = Qb + dA + kvh * HD;
+  const bf16* Vg = Kg + dKV;
+  const bf16* dOb = dO + (int64_t)b * T * lddo;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
   const int kw = kb0 + wave * 32;  // this wave's first key
   const int key = kw + c;          // this lane's key (column of S)
@@ -294,14 +294,21 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     if constexpr (DO_V) dv[t] = zero16();
   }
 
-  // causal: only the queries at or after this block's keys see them
+  // causal: only the queries at or after this block's keys see them.
+  // Iteration it covers query tile it % nq of group head it / nq.
   const int qbeg = CAUSAL ? kb0 : 0;
+  const int nq = qbeg < T ? (T - qbeg + AT - 1) / AT : 0;
+  const int nit = grp * nq;
   RowTile<HD> rq, ro;
-  if (qbeg < T) {
-    rq.load(Qg, ld, qbeg, T, tid);
-    ro.load(dOg, lddo, qbeg, T, tid);
+  if (nit > 0) {
+    rq.load(Qb + kvh * grp * HD, ld, qbeg, T, tid);
+    ro.load(dOb + kvh * grp * HD, lddo, qbeg, T, tid);
   }
-  for (int q0 = qbeg; q0 < T; q0 += AT) {
+  for (int it = 0; it < nit; ++it) {
+    const int h = kvh * grp + it / nq;
+    const int q0 = qbeg + (it % nq) * AT;
+    const float* Lg = lse + ((int64_t)b * H + h) * T;
+    const float* Dg = Dvec + ((int64_t)b * H + h) * T;
     __syncthreads();
     rq.store(sQ, q0, T, tid);
     ro.store(sdO, q0, T, tid);
@@ -311,9 +318,11 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
       sD[tid] = tq < T ? Dg[tq] : 0.f;
     }
     __syncthreads();
-    if (q0 + AT < T) {
-      rq.load(Qg, ld, q0 + AT, T, tid);
-      ro.load(dOg, lddo, q0 + AT, T, tid);
+    if (it + 1 < nit) {
+      const int hn = kvh * grp + (it + 1) / nq;
+      const int qn = qbeg + ((it + 1) % nq) * AT;
+      rq.load(Qb + hn * HD, ld, qn, T, tid);
+      ro.load(dOb + hn * HD, lddo, qn, T, tid);
     }
 #pragma unroll
     for (int sub = 0; sub < AT / 32; ++sub) {
@@ -363,9 +372,9 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     for (int r = 0; r < 16; ++r) {
       const int kr = kw + acc_row(r, g);
       if (kr < T) {
-        bf16* row = dqkv + ((int64_t)b * T + kr) * ld + h * HD + 32 * t + c;
-        if constexpr (DO_K) row[dA] = static_cast<bf16>(dk[t][r] * scale);
-        if constexpr (DO_V) row[2 * dA] = static_cast<bf16>(dv[t][r]);
+        bf16* row = dqkv + ((int64_t)b * T + kr) * ld + dA + kvh * HD + 32 * t + c;
+        if constexpr (DO_K) row[0] = static_cast<bf16>(dk[t][r] * scale);
+        if constexpr (DO_V) row[dKV] = static_cast<bf16>(dv[t][r]);
       }
     }
 }
@@ -376,7 +385,7 @@ template <int HD, bool CAUSAL>
 // for the dK/dV kernel, which runs after it.
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, const bf16* O, int64_t ldo,
                                                         const bf16* dO, int64_t lddo, const float* lse,
-                                                        float* Dvec, int T, int H, bf16* dqkv) {
+                                                        float* Dvec, int T, int H, int Hkv, bf16* dqkv) {
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
@@ -385,11 +394,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
   // short blocks; the longest (latest) query blocks are dispatched first.
   const int qb = gridDim.z - 1 - blockIdx.z;
   const int h = blockIdx.x, b = blockIdx.y;
-  const int dA = H * HD;
-  const int64_t ld = 3 * (int64_t)dA;
+  const int dA = H * HD, dKV = Hkv * HD, kvh = h / (H / Hkv);
+  const int64_t ld = dA + 2 * (int64_t)dKV;
   const bf16* Qg = qkv + (int64_t)b * T * ld + h * HD;
-  const bf16* Kg = Qg + dA;
-  const bf16* Vg = Qg + 2 * dA;
+  const bf16* Kg = qkv + (int64_t)b * T * ld + dA + kvh * HD;
+  const bf16* Vg = Kg + dKV;
   const bf16* dOg = dO + (int64_t)b * T * lddo + h * HD;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, c = lane & 31;
   const int q0 = qb * 128 + wave * 32;
@@ -475,53 +484,61 @@ bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
 constexpr int kAttnCUs = 256;  // MI355X compute units
 
 template <int HD, bool CAUSAL>
-static void fwd_launch(dim3 grid, hipStream_t s, const bf16* q, int T, int H, bf16* o, int64_t ldo, float* lse) {
-  hipLaunchKernelGGL((attn_fwd_mfma<HD, CAUSAL>), grid, dim3(256), 0, s, q, T, H, o, ldo, lse);
+static void fwd_launch(dim3 grid, hipStream_t s, const bf16* q, int T, int H, int Hkv, bf16* o, int64_t ldo,
+                       float* lse) {
+  hipLaunchKernelGGL((attn_fwd_mfma<HD, CAUSAL>), grid, dim3(256), 0, s, q, T, H, Hkv, o, ldo, lse);
 }
 
-hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
-                                float* lse, hipStream_t s) {
+hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int Hkv, int hd, int causal, void* O,
+                                int64_t ldo, float* lse, hipStream_t s) {
   const dim3 grid(H, B, cdiv(T, 128));
   const bf16* q = static_cast<const bf16*>(qkv);
   bf16* o = static_cast<bf16*>(O);
-  if (hd == 64) causal ? fwd_launch<64, true>(grid, s, q, T, H, o, ldo, lse) : fwd_launch<64, false>(grid, s, q, T, H, o, ldo, lse);
-  else if (hd == 128) causal ? fwd_launch<128, true>(grid, s, q, T, H, o, ldo, lse) : fwd_launch<128, false>(grid, s, q, T, H, o, ldo, lse);
-  else return hipErrorInvalidValue;
+  if (hd == 64) {
+    if (causal) fwd_launch<64, true>(grid, s, q, T, H, Hkv, o, ldo, lse);
+    else fwd_launch<64, false>(grid, s, q, T, H, Hkv, o, ldo, lse);
+  } else if (hd == 128) {
+    if (causal) fwd_launch<128, true>(grid, s, q, T, H, Hkv, o, ldo, lse);
+    else fwd_launch<128, false>(grid, s, q, T, H, Hkv, o, ldo, lse);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
+// dQ over (query head, sequence, query block); dK / dV over (key/value
+// head, sequence, key block).
 template <int HD, bool CAUSAL>
-static void bwd_launch(dim3 grid, hipStream_t s, const bf16* q, const bf16* ob, int64_t ldo, const bf16* d,
-                       int64_t lddo, const float* lse, float* Dvec, int T, int H, bf16* o) {
-  const dim3 block(256);
-  hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, CAUSAL>), grid, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+static void bwd_launch(int B, int T, int H, int Hkv, hipStream_t s, const bf16* q, const bf16* ob, int64_t ldo,
+                       const bf16* d, int64_t lddo, const float* lse, float* Dvec, bf16* o) {
+  const dim3 block(256), gq(H, B, cdiv(T, 128)), gk(Hkv, B, cdiv(T, 128));
+  hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, CAUSAL>), gq, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, Hkv, o);
   if constexpr (HD == 128) {
-    if ((int64_t)grid.x * grid.y * grid.z >= 2 * kAttnCUs) {
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+    if ((int64_t)gk.x * gk.y * gk.z >= 2 * kAttnCUs) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
       return;
     }
   }
-  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL>), grid, block, 0, s, q, d, lddo, lse, Dvec, T, H, o);
+  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
 }
 
 // dQ first (it also writes D = rowsum(dO * O) into Dvec), then dK / dV.
 // head_dim 128 with at least two workgroups per CU: separate dV and dK
 // passes (each fits two wavefronts per SIMD).
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
-                                const float* lse, float* Dvec, int B, int T, int H, int hd, int causal, void* dqkv,
-                                hipStream_t s) {
-  const dim3 grid(H, B, cdiv(T, 128));
+                                const float* lse, float* Dvec, int B, int T, int H, int Hkv, int hd, int causal,
+                                void* dqkv, hipStream_t s) {
   const bf16* q = static_cast<const bf16*>(qkv);
   const bf16* ob = static_cast<const bf16*>(O);
   const bf16* d = static_cast<const bf16*>(dO);
   bf16* o = static_cast<bf16*>(dqkv);
   if (hd == 64) {
-    if (causal) bwd_launch<64, true>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
-    else bwd_launch<64, false>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+    if (causal) bwd_launch<64, true>(B, T, H, Hkv, s, q, ob, ldo, d, lddo, lse, Dvec, o);
+    else bwd_launch<64, false>(B, T, H, Hkv, s, q, ob, ldo, d, lddo, lse, Dvec, o);
   } else if (hd == 128) {
-    if (causal) bwd_launch<128, true>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
-    else bwd_launch<128, false>(grid, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, o);
+    if (causal) bwd_launch<128, true>(B, T, H, Hkv, s, q, ob, ldo, d, lddo, lse, Dvec, o);
+    else bwd_launch<128, false>(B, T, H, Hkv, s, q, ob, ldo, d, lddo, lse, Dvec, o);
   } else {
     return hipErrorInvalidValue;
   }

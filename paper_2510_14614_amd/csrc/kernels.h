@@ -166,17 +166,19 @@ hipError_t col_sum_batch(DType dt, const ColSumBatch& b, float* scratch, hipStre
 int64_t col_sum_batch_scratch(int M, int W);
 
 // ------------------------------------------------------------ attention ----
-// Multi-head attention on the packed QKV activations [M, 3*dA] (Q | K | V,
-// head h at h*hd), M = B*T; causal = 1: query t sees keys 0..t, 0: every key
-// of its sequence.  O: dtype [M, ldo] (head h at column h*hd), LSE: fp32
+// Multi-head attention on the packed QKV activations [M, dA + 2*dKV]
+// (Q | K | V, dA = H*hd, dKV = Hkv*hd, head h at h*hd of its part; query
+// head h reads key/value head h / (H / Hkv)), M = B*T; causal = 1: query t
+// sees keys 0..t, 0: every key of its sequence.  O: dtype [M, ldo] (head h at column h*hd), LSE: fp32
 // [B, H, T] (natural log of the softmax denominators including the
 // 1/sqrt(hd) scale).
-hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int hd, int causal, void* O, int64_t ldo,
-                    float* lse, hipStream_t s);
-// Backward: from dO (dtype [M, ldo]) produce dQKV (dtype [M, 3dA]).
+hipError_t attn_fwd(DType dt, const void* qkv, int B, int T, int H, int Hkv, int hd, int causal, void* O,
+                    int64_t ldo, float* lse, hipStream_t s);
+// Backward: from dO (dtype [M, ldo]) produce dQKV (dtype [M, dA + 2dKV]); a
+// key/value head's gradient sums its group's query heads in head order.
 // Dvec: fp32 [B, H, T] scratch (rowsum(dO * O)); dq_acc: fp32 [M, dA] scratch.
 hipError_t attn_bwd(DType dt, const void* qkv, const void* O, int64_t ldo, const void* dO,
-                    int64_t lddo, const float* lse, int B, int T, int H, int hd, int causal, void* dqkv,
+                    int64_t lddo, const float* lse, int B, int T, int H, int Hkv, int hd, int causal, void* dqkv,
                     float* Dvec, float* dq_acc, hipStream_t s);
 
 // ------------------------------------------------ embedding / loss / misc ----

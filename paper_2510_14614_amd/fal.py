@@ -46,7 +46,7 @@ class fal_config_t(ctypes.Structure):
         ("d_ff", c_int32), ("vocab", c_int32), ("seq_len", c_int32), ("batch", c_int32),
         ("arch", c_int32), ("dtype", c_int32), ("sched", c_int32), ("ln_eps", c_float),
         ("gelu_tanh", c_int32), ("has_embed_head", c_int32), ("fal_block1_mode", c_int32),
-        ("bidirectional", c_int32),
+        ("bidirectional", c_int32), ("n_kv_head", c_int32),
     ]
 
 
@@ -110,7 +110,8 @@ def lib():
 def to_c(cfg: Config) -> fal_config_t:
     return fal_config_t(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.head_dim, cfg.d_ff, cfg.vocab,
                         cfg.seq_len, cfg.batch, cfg.arch, cfg.dtype, cfg.sched, cfg.ln_eps,
-                        cfg.gelu_tanh, cfg.has_embed_head, cfg.fal_block1_mode, cfg.bidirectional)
+                        cfg.gelu_tanh, cfg.has_embed_head, cfg.fal_block1_mode, cfg.bidirectional,
+                        cfg.n_kv_head)
 
 
 def _check(status, ctx=None):

@@ -50,6 +50,8 @@ def test_named_configs_valid(name):
     (dict(arch=4), fal.FAL_ERR_INVALID_ARG),
     (dict(bidirectional=2, has_embed_head=0), fal.FAL_ERR_INVALID_ARG),
     (dict(bidirectional=1), fal.FAL_ERR_INVALID_ARG),  # needs the block stack
+    (dict(n_kv_head=3), fal.FAL_ERR_INVALID_ARG),      # must divide n_head (4)
+    (dict(n_kv_head=-1), fal.FAL_ERR_INVALID_ARG),
     (dict(head_dim=24), fal.FAL_ERR_UNSUPPORTED),
     (dict(vocab=70000), fal.FAL_ERR_UNSUPPORTED),
     (dict(d_model=8192), fal.FAL_ERR_UNSUPPORTED),

@@ -129,6 +129,46 @@ def test_bidirectional_stack_step(arch, hd, dtype):
     compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"bidir a{arch} hd{hd} dt{dtype}")
 
 
+@pytest.mark.parametrize("dtype", [0, 1])
+@pytest.mark.parametrize("arch", ARCHS)
+def test_gqa_model_step(arch, dtype):
+    # grouped-query attention, two key/value heads for four query heads
+    # (matrix-core kernels in bf16, SIMT in fp32); ragged T
+    cfg = Config(n_layer=2, d_model=256, n_head=4, head_dim=64, n_kv_head=2, d_ff=328, vocab=1000,
+                 seq_len=100, batch=3, arch=arch, dtype=dtype, sched=SCHED_STREAMS_MERGED)
+    log(f"gqa model step arch={arch} dtype={dtype}")
+    g, blocks = synth.make_params(cfg, seed=60)
+    tok = synth.make_tokens(cfg, seed=61, dist="zipf")
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok), label=f"gqa a{arch} dt{dtype}")
+
+
+@pytest.mark.parametrize("hd,dtype,kv", [(16, 1, 1), (32, 0, 2), (64, 1, 2), (128, 1, 1)])
+def test_gqa_bidirectional_stack_step(hd, dtype, kv):
+    # the transformer-variant study's setting: encoder blocks with two (or
+    # one) key/value groups
+    cfg = Config(n_layer=2, d_model=4 * hd, n_head=4, head_dim=hd, n_kv_head=kv, d_ff=264, vocab=0, seq_len=300,
+                 batch=2, arch=ARCH_FALPLUS, dtype=dtype, has_embed_head=0, bidirectional=1)
+    log(f"gqa bidirectional stack hd={hd} dtype={dtype} kv={kv}")
+    _, blocks = synth.make_params(cfg, seed=62)
+    x1, gout = synth.make_stack_inputs(cfg, seed=63)
+    ref = oracle.stack_step(cfg, blocks, x1, gout)
+    ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
+    compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"gqa bidir hd{hd} kv{kv}")
+
+
+def test_gqa_hd128_wide_grid_split_backward():
+    # 8 key/value heads x 14 sequences x 5 blocks = 560 dK/dV workgroups:
+    # separate dV and dK passes, each summing two query heads
+    cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, n_kv_head=8, d_ff=512, vocab=0, seq_len=600,
+                 batch=14, arch=ARCH_GPT, dtype=1, has_embed_head=0)
+    log("gqa hd128 wide grid")
+    _, blocks = synth.make_params(cfg, seed=64)
+    x1, gout = synth.make_stack_inputs(cfg, seed=65)
+    ref = oracle.stack_step(cfg, blocks, x1, gout)
+    ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
+    compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label="gqa hd128 wide")
+
+
 def test_bidirectional_hd128_wide_grid_split_backward():
     # 16 heads x 7 sequences x 5 blocks = 560 workgroups: the unmasked dV and
     # dK passes run as two kernels
