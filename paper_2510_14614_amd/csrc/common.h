@@ -45,24 +45,23 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 
 // GELU (MLP non-linearity).  tanh form 0.5 x (1 + tanh(u)) with
 // u = sqrt(2/pi) (x + 0.044715 x^3), evaluated through the identity
-// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)) (one exp2 and one reciprocal);
-// derivative s + 2 x s (1 - s) u' with s = 1 / (1 + exp(-2u)).
-// erf form x * Phi(x) uses the library erff.
-__device__ __forceinline__ float gelu_sig_arg(float x) {
-  // -2u * log2(e)
-  const float c2 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
-  return c2 * (x + 0.044715f * x * x * x);
-}
-
-// GELU and its derivative at x, sharing the exponential: tanh form
-// x * s with s = sigmoid(2u), u = sqrt(2/pi) (x + 0.044715 x^3), so
-// GELU' = s + 2 x s (1 - s) du/dx; erf form x Phi(x), GELU' = Phi + x phi.
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)) = s, one exp2 and one reciprocal
+// (the hardware's: exp2 of a large argument gives inf and s = 0, of a very
+// negative one 0 and s = 1, the limits GELU needs); derivative
+// s + 2 x s (1 - s) u'.  erf form x * Phi(x) uses the library erff.
+// GELU and its derivative at x share the exponential; erf form:
+// GELU' = Phi + x phi.
 __device__ __forceinline__ void gelu_and_grad(float x, int tanh_form, float& g, float& dg) {
   if (tanh_form) {
-    const float s = __builtin_amdgcn_rcpf(1.f + exp2f(gelu_sig_arg(x)));
-    const float du = 0.7978845608028654f * (1.f + 3.f * 0.044715f * x * x);
+    constexpr float kC = 0.7978845608028654f;                 // sqrt(2/pi)
+    constexpr float kA = -2.0f * kC * 1.4426950408889634f;    // -2 sqrt(2/pi) log2(e)
+    const float x2 = x * x;
+    const float arg = x * fmaf(x2, kA * 0.044715f, kA);        // -2u log2(e)
+    const float s = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(arg));
     g = x * s;
-    dg = s + 2.f * x * s * (1.f - s) * du;
+    // 2 u' = 2 sqrt(2/pi) (1 + 3 * 0.044715 x^2)
+    const float du2 = fmaf(x2, 2.f * kC * 3.f * 0.044715f, 2.f * kC);
+    dg = fmaf(g * (1.f - s), du2, s);
     return;
   }
   const float cdf = 0.5f * (1.f + erff(x * 0.7071067811865476f));
