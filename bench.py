@@ -46,7 +46,8 @@ METRIC = "training tokens/s on 1 MI355X (FAL vs GPT baseline); MFMA util % of bf
 # FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy); valid only while the
 # sources it was measured on are unchanged.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_gpt2-small_traffic.md")
-TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h")
+TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h",
+                   "paper_2510_14614_amd/csrc/common.h")
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
