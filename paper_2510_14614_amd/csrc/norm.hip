@@ -147,6 +147,8 @@ __global__ __launch_bounds__(256) void ln_param_partials(LnBwdArgs a) {
   if (j < d) {
     const int r0 = rb * kPartRows + rg * (kPartRows / 4);
     const int r1 = min(a.M, r0 + kPartRows / 4);
+    // unrolled so that several rows' loads are in flight at once
+#pragma unroll 4
     for (int r = r0; r < r1; ++r) {
       const int64_t o = (int64_t)r * d + j;
       const float mu = a.mean[r], rs = a.rstd[r];
@@ -212,6 +214,7 @@ __global__ __launch_bounds__(256) void col_reduce_multi(ColReduceArgs a) {
   float s = 0.f;
   if (col < a.d) {
     const float* p = a.part + (int64_t)a.src[k] * a.d + col;
+#pragma unroll 8
     for (int b = part; b < a.nblk; b += 4) s += p[(int64_t)b * a.stride];
   }
   red[part][threadIdx.x & 63] = s;
