@@ -579,18 +579,20 @@ __global__ __launch_bounds__(256) void col_sum_batch_partials(ColSumPacked b) {
   float s[4] = {0.f, 0.f, 0.f, 0.f};
   if (j < in.N) {
     const int r0 = blockIdx.y * kColRows + rg * (kColRows / 4), r1 = min(b.M, r0 + kColRows / 4);
+    // 4-column vector loads, several rows in flight
     if (in.f32) {
       const float* x = static_cast<const float*>(in.x);
+#pragma unroll 4
       for (int r = r0; r < r1; ++r) {
         const float4 v = *reinterpret_cast<const float4*>(x + (int64_t)r * in.ld + j);
         s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
       }
     } else {
       const S* x = static_cast<const S*>(in.x);
+#pragma unroll 4
       for (int r = r0; r < r1; ++r) {
-        const S* p = x + (int64_t)r * in.ld + j;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) s[c] += to_f(p[c]);
+        const float4 v = ld4s<S>(x + (int64_t)r * in.ld + j);
+        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
       }
     }
   }
@@ -613,8 +615,10 @@ __global__ __launch_bounds__(256) void col_reduce_batch(ColSumPacked b, int nblk
   const int col = blockIdx.x * 64 + (threadIdx.x & 63);
   const int q = threadIdx.x >> 6;
   float s = 0.f;
-  if (col < W)
+  if (col < W) {
+#pragma unroll 8
     for (int blk = q; blk < nblk; blk += 4) s += b.part[(int64_t)blk * W + col];
+  }
   red[q][threadIdx.x & 63] = s;
   __syncthreads();
   if (q == 0 && col < W) {
@@ -644,6 +648,8 @@ hipError_t col_sum_batch(DType dt, const ColSumBatch& b, float* scratch, hipStre
   for (int k = 0; k < b.n; ++k) {
     const ColSumInput& in = b.in[k];
     if (!in.x || !in.out || in.N % 4 || in.ld % 4 || in.N < 1) return hipErrorInvalidValue;
+    // rows are read 4 columns at a time
+    if (reinterpret_cast<uintptr_t>(in.x) % ((in.f32 || dt == F32) ? 16 : 8)) return hipErrorInvalidValue;
     p.in[k] = in;
     p.off[k] = w;
     w += in.N;
