@@ -1172,6 +1172,25 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* part, int spli
   out[(int64_t)m * ldo + n] = v;
 }
 
+// The same four columns at a time (N and ldo multiples of 4, out 16-byte
+// aligned): one 16-byte load per slice, the slices summed in order.
+__global__ __launch_bounds__(256) void splitk_reduce4(const float* part, int splits, int M, int N, const bf16* bias,
+                                                      const bf16* bias2, float* out, int64_t ldo) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= (int64_t)M * N) return;
+  const int m = i / N, n = i % N;
+  const int64_t MN = (int64_t)M * N;
+  float4 v = *reinterpret_cast<const float4*>(part + i);
+#pragma unroll 4
+  for (int s = 1; s < splits; ++s) {
+    const float4 p = *reinterpret_cast<const float4*>(part + s * MN + i);
+    v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+  }
+  if (bias) { v.x += to_f(bias[n]); v.y += to_f(bias[n + 1]); v.z += to_f(bias[n + 2]); v.w += to_f(bias[n + 3]); }
+  if (bias2) { v.x += to_f(bias2[n]); v.y += to_f(bias2[n + 1]); v.z += to_f(bias2[n + 2]); v.w += to_f(bias2[n + 3]); }
+  *reinterpret_cast<float4*>(out + (int64_t)m * ldo + n) = v;
+}
+
 // ------------------------------------------------------------- launcher --
 // Block shapes.  128x128 (2x2 wavefronts of 64x64) and 128x96 (2x2 of 64x48)
 // run two workgroups per CU; 256x256 (4x2 wavefronts of 64x128) runs one and
@@ -1376,9 +1395,15 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     if (g.n == 1 && P.splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(splitk_reduce, dim3(cdiv((int64_t)P.M * P.N, 256)), dim3(256), 0, s, P.part, P.splits,
-                         P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
-                         static_cast<float*>(P.out), P.ldo);
+      const bool v4 = P.N % 4 == 0 && P.ldo % 4 == 0 && reinterpret_cast<uintptr_t>(P.out) % 16 == 0;
+      if (v4)
+        hipLaunchKernelGGL(splitk_reduce4, dim3(cdiv((int64_t)P.M * P.N / 4, 256)), dim3(256), 0, s, P.part,
+                           P.splits, P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
+                           static_cast<float*>(P.out), P.ldo);
+      else
+        hipLaunchKernelGGL(splitk_reduce, dim3(cdiv((int64_t)P.M * P.N, 256)), dim3(256), 0, s, P.part, P.splits,
+                           P.M, P.N, static_cast<const bf16*>(P.bias), static_cast<const bf16*>(P.bias2),
+                           static_cast<float*>(P.out), P.ldo);
     }
     return hipGetLastError();
   };
