@@ -650,8 +650,9 @@ struct Run {
     const bool uses_lnF = (arch == FAL_ARCH_FAL && layer == 0 && (!block1_standard() || D.L > 1)) ||
                           (arch == FAL_ARCH_FALPLUS && layer > 0);
     if (!uses_lnF) {
-      FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_G), D.d, sm));
-      FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_B), D.d, sm));
+      // both slots in one launch (the alignment padding between them is zero too)
+      const int64_t n = ctx->Lo.boff[FAL_B_LNF1_B] + D.d - ctx->Lo.boff[FAL_B_LNF1_G];
+      FAL_TRY(zero_f32(G(gb, FAL_B_LNF1_G), n, sm));
     }
     if ((arch == FAL_ARCH_FAL && layer > 0) || arch == FAL_ARCH_PARALLEL) {
       hipStream_t s2 = sm;
