@@ -383,7 +383,10 @@ __device__ __forceinline__ void wave_lds_order() {
 // with consecutive lanes on consecutive columns, so every
 // global access (output, residual, pre-activation) covers whole row segments
 // of the wavefront tile (128 B of bf16 for a 64-column tile).
-template <int EPI, int F32OUT, int FM, int FN>
+// TR = 1: the accumulators are transposed blocks (the MFMA ran as B^T A^T):
+// lane 16g+c of block (i, j) holds row 16i + c, columns 16j + 4g .. +3,
+// written to the strip as one 16-byte store.
+template <int EPI, int F32OUT, int FM, int FN, int TR = 0>
 __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], float* stage,
                                              int mw, int nw, int lane, int gelu_tanh) {
   constexpr int WTN = FN * 16, PITCH = WTN + 4;
@@ -398,10 +401,17 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
   for (int i = 0; i < FM; ++i) {
     // straight from the MFMA layout: lane 16g+c holds rows 4g..4g+3 of
     // column c (with the 4-float pad, 64 different banks per store)
+    if (TR) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j)
+        *reinterpret_cast<float4*>(stage + (lane & 15) * PITCH + 16 * j + 4 * (lane >> 4)) =
+            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    } else {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) stage[((lane >> 4) * 4 + r) * PITCH + 16 * j + (lane & 15)] = acc[i][j][r];
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) stage[((lane >> 4) * 4 + r) * PITCH + 16 * j + (lane & 15)] = acc[i][j][r];
+    }
     wave_lds_order();
     // kept rolled: unrolling it multiplies the epilogue code (one copy per
     // output kind) several-fold, and the once-per-tile epilogue then runs
@@ -880,7 +890,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[cur][i], rb[cur][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rb[cur][j], ra[cur][i], acc[i][j], 0, 0, 0);
       ra[nxt][i] = fa.read(stage, i);
     }
   };
@@ -957,17 +967,17 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
     Q.ldo = P.N;
     Q.bias = Q.bias2 = nullptr;
     Q.vec_out = (P.N & 3) == 0;
-    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    store_staged<EPI_STORE, 1, FM, FN, 1>(Q, acc, stage, mw, nw, lane, gelu_tanh);
     return;
   }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
-      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
       break;
-    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
@@ -1081,7 +1091,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dbl(GemmGroup g, int gelu_
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[buf][kk][i], rb[buf][kk][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rb[buf][kk][j], ra[buf][kk][i], acc[i][j], 0, 0, 0);
   };
   // Issue order inside a step: one fragment read after each of the first
   // MFMAs, the loads spread over the rest.
@@ -1144,17 +1154,17 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dbl(GemmGroup g, int gelu_
     Q.ldo = P.N;
     Q.bias = Q.bias2 = nullptr;
     Q.vec_out = (P.N & 3) == 0;
-    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    store_staged<EPI_STORE, 1, FM, FN, 1>(Q, acc, stage, mw, nw, lane, gelu_tanh);
     return;
   }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
-      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
       break;
-    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
