@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
 // wavefront per SIMD).  PART 1: dV only, PART 2: dK only (head_dim 128:
 // each pass fits two wavefronts per SIMD at the cost of recomputing S in
 // both; used when the grid has enough workgroups to put two on every CU).
-template <int HD, int PART, bool CAUSAL>
+template <int HD, int PART, bool CAUSAL, bool GQA>
 __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bwd_dkdv_mfma(
     const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, int Hkv,
     bf16* dqkv) {
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
   // earliest key blocks see the most queries and are dispatched first.  A
   // key/value head accumulates over every query head of its group, in order.
   const int kb0 = blockIdx.z * 128;
-  const int kvh = blockIdx.x, b = blockIdx.y, grp = H / Hkv;
+  const int kvh = blockIdx.x, b = blockIdx.y, grp = GQA ? H / Hkv : 1;
   const int dA = H * HD, dKV = Hkv * HD;
   const int64_t ld = dA + 2 * (int64_t)dKV;
   const bf16* Qb = qkv + (int64_t)b * T * ld;
@@ -305,8 +305,9 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     ro.load(dOb + kvh * grp * HD, lddo, qbeg, T, tid);
   }
   for (int it = 0; it < nit; ++it) {
-    const int h = kvh * grp + it / nq;
-    const int q0 = qbeg + (it % nq) * AT;
+    // without grouping the iteration is the query tile itself
+    const int h = kvh * grp + (GQA ? it / nq : 0);
+    const int q0 = qbeg + (GQA ? it % nq : it) * AT;
     const float* Lg = lse + ((int64_t)b * H + h) * T;
     const float* Dg = Dvec + ((int64_t)b * H + h) * T;
     __syncthreads();
@@ -319,8 +320,8 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     }
     __syncthreads();
     if (it + 1 < nit) {
-      const int hn = kvh * grp + (it + 1) / nq;
-      const int qn = qbeg + ((it + 1) % nq) * AT;
+      const int hn = kvh * grp + (GQA ? (it + 1) / nq : 0);
+      const int qn = qbeg + (GQA ? (it + 1) % nq : it + 1) * AT;
       rq.load(Qb + hn * HD, ld, qn, T, tid);
       ro.load(dOb + hn * HD, lddo, qn, T, tid);
     }
@@ -508,19 +509,27 @@ hipError_t attn_fwd_mfma_launch(const void* qkv, int B, int T, int H, int Hkv, i
 
 // dQ over (query head, sequence, query block); dK / dV over (key/value
 // head, sequence, key block).
+template <int HD, bool CAUSAL, bool GQA>
+static void dkdv_launch(dim3 gk, hipStream_t s, const bf16* q, const bf16* d, int64_t lddo, const float* lse,
+                        const float* Dvec, int T, int H, int Hkv, bf16* o) {
+  const dim3 block(256);
+  if constexpr (HD == 128) {
+    if ((int64_t)gk.x * gk.y * gk.z >= 2 * kAttnCUs) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+}
+
 template <int HD, bool CAUSAL>
 static void bwd_launch(int B, int T, int H, int Hkv, hipStream_t s, const bf16* q, const bf16* ob, int64_t ldo,
                        const bf16* d, int64_t lddo, const float* lse, float* Dvec, bf16* o) {
   const dim3 block(256), gq(H, B, cdiv(T, 128)), gk(Hkv, B, cdiv(T, 128));
   hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, CAUSAL>), gq, block, 0, s, q, ob, ldo, d, lddo, lse, Dvec, T, H, Hkv, o);
-  if constexpr (HD == 128) {
-    if ((int64_t)gk.x * gk.y * gk.z >= 2 * kAttnCUs) {
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
-      return;
-    }
-  }
-  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+  if (Hkv == H) dkdv_launch<HD, CAUSAL, false>(gk, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+  else dkdv_launch<HD, CAUSAL, true>(gk, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
 }
 
 // dQ first (it also writes D = rowsum(dO * O) into Dvec), then dK / dV.
