@@ -1,7 +1,8 @@
 /*
  * fal.h -- C ABI of libfal.so: one training step (forward + backward) of a
- * GPT-style Pre-LN decoder stack in three block architectures, and the
- * AdamW update that follows it, on one MI355X (gfx950):
+ * GPT-style Pre-LN decoder stack in four block architectures, the forward
+ * pass alone, and the AdamW update that follows a step, on one MI355X
+ * (gfx950):
  *
  *   GPT   (Sec. 2, Eq. 1)  X_{i+1} = X_i + MHA_i(LN(X_i))
  *                                   + MLP_i(LN(X_i + MHA_i(LN(X_i))))
@@ -13,13 +14,15 @@
  *         adds its own LayerNorm of the first attention output to the GPT
  *         MLP input: MLP_i(LN(X_i + A_i) + LN_{F,i}(MHA_1(LN(X_1)))).
  *   PARALLEL (the configuration Sec. 6.1 and 6.4 compare against, after
- *         GPT-J and PaLM) MHA and MLP read the same block input, each through its own
- *         LayerNorm: X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i)).
+ *         GPT-J and PaLM) MHA and MLP read the same block input, each
+ *         through its own LayerNorm:
+ *         X_{i+1} = X_i + MHA_i(LN1(X_i)) + MLP_i(LN2(X_i)).
  *         Scheduled like the FAL blocks (two independent branches).
  *
- * MHA = QKV projection, causal scaled-dot-product attention per head,
- * concatenation, output projection; MLP = up-projection, GELU (tanh form by
- * default), down-projection (Sec. 2).  Biases on every linear layer, learned
+ * MHA = QKV projection, scaled-dot-product attention per head (causal; no
+ * mask for encoder stacks; optionally grouped-query with shared key/value
+ * heads), concatenation, output projection; MLP = up-projection, GELU (tanh
+ * form by default), down-projection (Sec. 2).  Biases on every linear layer, learned
  * position embedding, final LayerNorm and an LM head tied to the token
  * embedding (GPT-2 conventions).
  *
