@@ -443,7 +443,7 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
 #define FAL_GEMM_REMAP 1
 #endif
 #ifndef FAL_GEMM_GROUP_M
-#define FAL_GEMM_GROUP_M 8
+#define FAL_GEMM_GROUP_M 4
 #endif
 constexpr int kXcds = 8, kGroupM = FAL_GEMM_GROUP_M;
 __device__ __forceinline__ int xcd_remap(int bid, int total) {
