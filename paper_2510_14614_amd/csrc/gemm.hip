@@ -442,6 +442,9 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
 #ifndef FAL_GEMM_REMAP
 #define FAL_GEMM_REMAP 1
 #endif
+#ifndef FAL_OCC3_KMAX
+#define FAL_OCC3_KMAX 1024  // longest K (both segments) sent to the three-workgroup kernel
+#endif
 #ifndef FAL_GEMM_GROUP_M
 #define FAL_GEMM_GROUP_M 4
 #endif
@@ -1449,7 +1452,7 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
     // orientations and long K keep the double buffer.
     int kmax = 0;
     for (int i = 0; i < g.n; ++i) kmax = std::max(kmax, g.p[i].K + g.p[i].K2);
-    const bool occ3 = shape == PIPE_128x128 && a_kmaj && !b_kmaj && sp == 1 && kmax <= 1024;
+    const bool occ3 = shape == PIPE_128x128 && a_kmaj && !b_kmaj && sp == 1 && kmax <= FAL_OCC3_KMAX;
     if (occ3) {
       hipLaunchKernelGGL((gemm_bf16_pipe<1, 0, 128, 128, 3, 3>), grid, block, 0, s, g, gelu_tanh);
     } else if (FAL_GEMM_DBL && shape != PIPE_256x256) {
