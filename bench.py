@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-optimizer", action="store_true",
                     help="skip the extra measurement of step + AdamW update")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured as a HIP graph instead of eager launches")
     ap.add_argument("--no-forward", action="store_true",
                     help="skip the extra forward-only measurement (FAL and GPT)")
     ap.add_argument("--cpu-sample-batch", type=int, default=1)
@@ -89,7 +91,7 @@ def describe(cfg, arch_name, sched_name):
 
 
 class Runner:
-    def __init__(self, cfg, single_stream=False, optimizer=False, forward_only=False):
+    def __init__(self, cfg, single_stream=False, optimizer=False, forward_only=False, graph=False):
         import torch
 
         from paper_2510_14614_amd import fal, synth
@@ -98,8 +100,10 @@ class Runner:
         self.optimizer = optimizer
         self.forward_only = forward_only
         self.hp = fal.ADAMW_PAPER
-        main = torch.cuda.current_stream()
+        # a graph is captured on a stream of its own, which the context must use
+        main = torch.cuda.Stream() if graph else torch.cuda.current_stream()
         self.F = fal.Fal(cfg, stream_main=main, stream_aux=main if single_stream else None)
+        self.graph = None
         g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
         self.F.load_params(g, blocks)
         if cfg.has_embed_head:
@@ -112,8 +116,31 @@ class Runner:
             self.dx = torch.empty_like(self.x1)
         if optimizer:
             self.F.init_optimizer()
+        if graph:
+            self.capture()
+
+    def capture(self):
+        """Records one whole step (every launch of both streams) as a HIP graph
+        and replays it from then on: the same kernels, without the per-launch
+        host work and dispatch gaps."""
+        torch = self.torch
+        with torch.cuda.stream(self.F.stream_main):
+            for _ in range(2):
+                self.launch()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=self.F.stream_main):
+            self.launch()
+        torch.cuda.synchronize()
+        self.graph = g
 
     def step(self):
+        if self.graph is not None:
+            self.graph.replay()
+            return
+        self.launch()
+
+    def launch(self):
         if self.forward_only:
             if self.cfg.has_embed_head:
                 self.F.model_forward(self.tok)
@@ -132,7 +159,7 @@ class Runner:
         for _ in range(warmup):
             self.step()
         torch.cuda.synchronize()
-        s = self.F.stream_main
+        s = self.F.stream_main if self.graph is None else torch.cuda.current_stream()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(s)
@@ -328,7 +355,7 @@ def main():
     sched = SCHED_NAMES[args.sched]
     cfg = get_config(args.config, arch=arch, sched=sched, dtype=1)
 
-    r = Runner(cfg, single_stream=args.single_stream)
+    r = Runner(cfg, single_stream=args.single_stream, graph=args.graph)
     ms, wall = r.time(args.steps, args.warmup)
     r.close()
     # Kernel roofline from a serialized pass (aux stream = main stream: the

@@ -672,7 +672,7 @@ struct Run {
     }
     if (arch == FAL_ARCH_FAL && !block1_standard()) {  // block 0, Eq. 2
       mlp_bwd(S, bp, dy_lp, dy, gb, sm, W.part_main);
-      if (last) FAL_TRY(hipMemcpyAsync(dfirst, W.dh2, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
+      if (last) FAL_TRY(copy_f32(dfirst, W.dh2, Md, sm));
       else FAL_TRY(add_f32(dfirst, W.dh2, dfirst, Md, sm));
       // dA_1 = dY + LN_F backward of the accumulated dF
       LnBwdArgs f = lnb(W.a1, W.meanF, W.rstdF);
@@ -708,7 +708,7 @@ struct Run {
     const float* da = W.dxm;
     if (arch == FAL_ARCH_FALPLUS && layer == 0 && D.L > 1) {
       // dA_1 = dXm + backward of norm(A_1) applied to the accumulated dxhatF
-      FAL_TRY(hipMemcpyAsync(W.da, W.dxm, Md * sizeof(float), hipMemcpyDeviceToDevice, sm));
+      FAL_TRY(copy_f32(W.da, W.dxm, Md, sm));
       FAL_TRY(norm_bwd(W.a1, W.meanF, W.rstdF, dfirst, D.M, D.d, W.da, 1, sm));
       FAL_TRY(cast_from_f32(dt, W.da, W.da_lp, Md, sm));
       da_lp = W.da_lp;
@@ -1029,8 +1029,7 @@ fal_status_t fal_stack_forward(fal_ctx_t* ctx, const void* params, const float* 
     r.fwd_only = true;
     for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), xin(i), W.resid + (i + 1) * Md, W.first);
     if (x_out)
-      FAL_TRY(hipMemcpyAsync(x_out, W.resid + (int64_t)D.L * Md, Md * sizeof(float), hipMemcpyDeviceToDevice,
-                             ctx->sm));
+      FAL_TRY(copy_f32(x_out, W.resid + (int64_t)D.L * Md, Md, ctx->sm));
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }

@@ -225,6 +225,9 @@ hipError_t cast_from_f32(DType dt, const float* x, void* y, int64_t n, hipStream
 hipError_t cache_warm(const void* p, int64_t bytes, hipStream_t s);
 // Fill fp32 with zero (a kernel, so it can live inside captured graphs).
 hipError_t zero_f32(float* y, int64_t n, hipStream_t s);
+// y = x over n fp32 elements (a kernel rather than a runtime copy, so every
+// node of a captured step is a kernel).
+hipError_t copy_f32(float* y, const float* x, int64_t n, hipStream_t s);
 
 // ----------------------------------------------------------- optimizer ----
 // AdamW over a flat fp32 buffer (Adam's bias-corrected moments, decoupled

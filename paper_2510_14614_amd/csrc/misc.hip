@@ -391,6 +391,26 @@ hipError_t cache_warm(const void* p, int64_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void copy4_kernel(float4* y, const float4* x, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) y[i] = x[i];
+}
+__global__ __launch_bounds__(256) void copy_kernel(float* y, const float* x, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) y[i] = x[i];
+}
+
+hipError_t copy_f32(float* y, const float* x, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const bool v4 = n % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0;
+  const int64_t units = v4 ? n / 4 : n;
+  const int blocks = (int)std::min<int64_t>(4096, (units + 255) / 256);
+  if (v4)
+    hipLaunchKernelGGL(copy4_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<float4*>(y),
+                       reinterpret_cast<const float4*>(x), units);
+  else
+    hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(256), 0, s, y, x, units);
+  return hipGetLastError();
+}
+
 hipError_t zero_f32(float* y, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(zero_kernel, dim3(cdiv(n, 256)), dim3(256), 0, s, y, n);
   return hipGetLastError();
