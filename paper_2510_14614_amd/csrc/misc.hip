@@ -248,6 +248,87 @@ __global__ __launch_bounds__(kCeThreads) void ce_rows(const S* logits, int64_t l
   }
 }
 
+// bf16 rows with 16-byte accesses: lane c of the workgroup holds groups of
+// eight raw logits (packed, four registers per group) rather than their
+// exponentials, and recomputes exp(x - lse) for the gradient.  Packed raw
+// values keep the kernel under 64 registers, so two 1024-thread workgroups
+// share a compute unit and one row's reduction overlaps another's loads.
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf_at(const uint4& u, int e) {
+  const uint32_t w = e < 2 ? u.x : e < 4 ? u.y : e < 6 ? u.z : u.w;
+  return (e & 1) ? bf_hi(w) : bf_lo(w);
+}
+__device__ __forceinline__ uint32_t bf_pack2(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, from_f<bf16>(a)) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, from_f<bf16>(b)) << 16);
+}
+
+template <int NPT>
+__global__ __launch_bounds__(kCeThreads) void ce_rows_x8(const bf16* logits, int64_t ldl, const int32_t* tok, int T,
+                                                         int V, float inv_n, bf16* dl, int64_t ldd,
+                                                         float* row_loss) {
+  __shared__ float rm[kCeThreads / FAL_WAVE], rs[kCeThreads / FAL_WAVE];
+  const int m = blockIdx.x, b = m / T, t = m % T, tid = threadIdx.x;
+  int tgt = tok[(int64_t)b * (T + 1) + t + 1];
+  tgt = min(max(tgt, 0), V - 1);
+  const bf16* l = logits + (int64_t)m * ldl;
+  const int nv = (V + 7) / 8, nd = (int)(ldd / 8);
+  uint4 raw[NPT];
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c = tid + kCeThreads * i;
+    raw[i] = c < nv ? *reinterpret_cast<const uint4*>(l + 8 * c) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  float lm = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c = tid + kCeThreads * i;
+    if (c < nv) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * c + e < V) lm = fmaxf(lm, bf_at(raw[i], e));
+    }
+  }
+  float ls = 0.f;
+  if (lm != -INFINITY) {
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+      const int c = tid + kCeThreads * i;
+      if (c < nv) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * c + e < V) ls += __expf(bf_at(raw[i], e) - lm);
+      }
+    }
+  }
+  float gm = lm, gs = ls;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) lse_combine(gm, gs, __shfl_xor(gm, o, FAL_WAVE), __shfl_xor(gs, o, FAL_WAVE));
+  if ((tid & (FAL_WAVE - 1)) == 0) { rm[tid / FAL_WAVE] = gm; rs[tid / FAL_WAVE] = gs; }
+  __syncthreads();
+  gm = rm[0]; gs = rs[0];
+#pragma unroll
+  for (int w = 1; w < kCeThreads / FAL_WAVE; ++w) lse_combine(gm, gs, rm[w], rs[w]);
+  const float lse = gm + __logf(gs);
+  if (tid == 0) row_loss[m] = lse - to_f(l[tgt]);
+  if (!dl) return;  // loss only
+  bf16* drow = dl + (int64_t)m * ldd;
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c = tid + kCeThreads * i;
+    if (c >= nd) continue;
+    float g[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int col = 8 * c + e;
+      g[e] = col < V ? __expf(bf_at(raw[i], e) - lse) * inv_n - (col == tgt ? inv_n : 0.f) : 0.f;
+    }
+    *reinterpret_cast<uint4*>(drow + 8 * c) =
+        make_uint4(bf_pack2(g[0], g[1]), bf_pack2(g[2], g[3]), bf_pack2(g[4], g[5]), bf_pack2(g[6], g[7]));
+  }
+}
+
 // out = scale * sum(x[0..n)), fixed order (single workgroup).
 __global__ __launch_bounds__(256) void sum_kernel(const float* x, int64_t n, float scale, float* out) {
   __shared__ float red[256];
@@ -280,13 +361,27 @@ hipError_t cross_entropy(DType dt, const void* logits, int64_t ldl, const int32_
     hipLaunchKernelGGL((ce_rows<float, NPT>), grid, block, 0, s, static_cast<const float*>(logits), ldl,      \
                        tokens, T, V, inv_n,                                                                  \
                        static_cast<float*>(dlogits), ldd, row_loss);
-  if (need <= 1) { FAL_CE_LAUNCH(1) }
+  // bf16 rows in 16-byte groups when both row pitches allow it
+  const int need8 = (int)((ldd / 8 + kCeThreads - 1) / kCeThreads);
+  const bool x8 = dt == BF16 && ldl % 8 == 0 && ldd % 8 == 0 && need8 <= 8 &&
+                  reinterpret_cast<uintptr_t>(logits) % 16 == 0 && reinterpret_cast<uintptr_t>(dlogits) % 16 == 0;
+#define FAL_CE_X8_LAUNCH(NPT)                                                                              \
+  hipLaunchKernelGGL((ce_rows_x8<NPT>), grid, block, 0, s, static_cast<const bf16*>(logits), ldl, tokens, T, V, \
+                     inv_n, static_cast<bf16*>(dlogits), ldd, row_loss);
+  if (x8) {
+    if (need8 <= 1) { FAL_CE_X8_LAUNCH(1) }
+    else if (need8 <= 2) { FAL_CE_X8_LAUNCH(2) }
+    else if (need8 <= 4) { FAL_CE_X8_LAUNCH(4) }
+    else if (need8 <= 7) { FAL_CE_X8_LAUNCH(7) }  // GPT-2 vocabulary (50257 padded to 50304)
+    else { FAL_CE_X8_LAUNCH(8) }
+  } else if (need <= 1) { FAL_CE_LAUNCH(1) }
   else if (need <= 4) { FAL_CE_LAUNCH(4) }
   else if (need <= 8) { FAL_CE_LAUNCH(8) }
   else if (need <= 13) { FAL_CE_LAUNCH(13) }  // GPT-2 vocabulary (50257 padded to 50304)
   else if (need <= 16) { FAL_CE_LAUNCH(16) }
   else return hipErrorInvalidValue;
 #undef FAL_CE_LAUNCH
+#undef FAL_CE_X8_LAUNCH
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (loss) {

@@ -16,7 +16,7 @@ ARCHS = [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS, ARCH_PARALLEL]
 
 
 def _ragged(arch, dtype, **kw):
-    base = dict(n_layer=2, d_model=192, n_head=3, head_dim=64, d_ff=328, vocab=1000, seq_len=100,
+    base = dict(n_layer=2, d_model=192, n_head=3, head_dim=64, d_ff=328, vocab=1003, seq_len=100,
                 batch=3, arch=arch, dtype=dtype, sched=SCHED_STREAMS_MERGED)
     base.update(kw)
     return Config(**base)
