@@ -73,6 +73,10 @@ def parse():
                     help="run the timed steps with the aux stream equal to the main stream")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "OUT_MD"),
                     help="offline: write a kernel summary from a rocprofv3 --stats kernel_stats.csv")
+    ap.add_argument("--summarize-mfma", nargs=3, metavar=("PMC_CSV", "TRACE_CSV", "OUT_MD"),
+                    help="offline: write the MFMA-utilisation summary from a rocprofv3 --pmc "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES "
+                         "counter_collection.csv and the kernel_trace.csv of the same run")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "PROBE_MIB", "OUT_MD"),
                     help="offline: write the GEMM traffic summary from two rocprofv3 --pmc counter_collection.csv "
                          "of runs made with --copy-probe PROBE_MIB")
@@ -332,6 +336,53 @@ def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
     print("\n".join(lines))
 
 
+N_SIMD = 256 * 4  # MI355X: 256 compute units of 4 SIMDs
+CLOCK_GHZ = 2.4   # MI355X peak engine clock
+
+
+def summarize_mfma(pmc_csv, trace_csv, out_md, cmds):
+    """MFMA work and busy time per kernel class from per-dispatch counters.
+
+    Executed bf16 MFMA FLOPs = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512; busy
+    fraction = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x duration x 2.4 GHz),
+    the duration taken from the kernel trace of the same run.  At 1024 bf16
+    FLOPs per SIMD per cycle the two agree when every busy cycle does dense
+    bf16 work.
+    """
+    dur = {}
+    for r in csv.DictReader(open(trace_csv)):
+        dur[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    per = {}
+    for r in csv.DictReader(open(pmc_csv)):
+        d = per.setdefault(r["Dispatch_Id"], {"name": r["Kernel_Name"]})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    classes = [("bf16 GEMMs (gemm_bf16_*)", "gemm_bf16_"), ("attention forward (attn_fwd_mfma)", "attn_fwd_mfma"),
+               ("attention backward dK/dV (attn_bwd_dkdv_mfma)", "attn_bwd_dkdv_mfma"),
+               ("attention backward dQ (attn_bwd_dq_mfma)", "attn_bwd_dq_mfma")]
+    lines = ["# MFMA utilisation of the FAL training step (serialized launches; workload as in the command)", "",
+             "Commands (repository root on the GPU host, `TMPDIR=/tmp`):", "",
+             "```", *cmds, "```", "",
+             "Per kernel class, summed over its dispatches: executed bf16 MFMA FLOPs =",
+             "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 over the traced kernel time (dense bf16 peak 2500 TFLOP/s);",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x traced time x 2.4 GHz).  Executed FLOPs",
+             "include work the algorithmic count leaves out (zero-padded edge tiles, the masked half of",
+             "diagonal attention tiles, the recomputed scores of the backward).", "",
+             "| class | dispatches | total ms | executed TFLOP/s | of 2500 | MFMA busy |",
+             "|---|---|---|---|---|---|"]
+    for label, key in classes:
+        ds = [(k, v) for k, v in per.items() if key in v["name"] and k in dur
+              and "SQ_VALU_MFMA_BUSY_CYCLES" in v and "SQ_INSTS_VALU_MFMA_MOPS_BF16" in v]
+        if not ds:
+            continue
+        t = sum(dur[k] for k, _ in ds)
+        flops = sum(v["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for _, v in ds) * 512
+        busy = sum(v["SQ_VALU_MFMA_BUSY_CYCLES"] for _, v in ds)
+        tf = flops / t / 1e12
+        lines.append(f"| {label} | {len(ds)} | {t * 1e3:.2f} | {tf:.0f} | {tf / 2500:.3f} | "
+                     f"{100 * busy / (N_SIMD * t * CLOCK_GHZ * 1e9):.1f}% |")
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
 def main():
     args = parse()
     if args.summarize_stats:
@@ -339,6 +390,9 @@ def main():
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.cmd)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma, args.cmd)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
