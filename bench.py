@@ -77,6 +77,9 @@ def parse():
                     help="offline: write the MFMA-utilisation summary from a rocprofv3 --pmc "
                          "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES "
                          "counter_collection.csv and the kernel_trace.csv of the same run")
+    ap.add_argument("--summarize-hbm", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "PROBE_MIB", "OUT_MD"),
+                    help="offline: write HBM bytes and GB/s per kernel class from two rocprofv3 "
+                         "--kernel-trace --pmc runs (FETCH_SIZE, WRITE_SIZE) made with --copy-probe PROBE_MIB")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "PROBE_MIB", "OUT_MD"),
                     help="offline: write the GEMM traffic summary from two rocprofv3 --pmc counter_collection.csv "
                          "of runs made with --copy-probe PROBE_MIB")
@@ -383,6 +386,57 @@ def summarize_mfma(pmc_csv, trace_csv, out_md, cmds):
     open(out_md, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
+HBM_CLASSES = [("bf16 GEMMs + split-K reduces", ("gemm_bf16_", "splitk_reduce")),
+               ("attention (MFMA kernels)", ("attn_fwd_mfma", "attn_bwd_")),
+               ("LayerNorm fwd / bwd / parameter sums", ("ln_fwd", "ln_bwd", "ln_param_partials",
+                                                         "col_reduce_multi", "norm_bwd")),
+               ("cross-entropy rows", ("ce_rows",)),
+               ("bias-gradient column sums", ("col_sum_batch_partials", "col_reduce_batch")),
+               ("embedding fwd / bwd", ("embed_", "wpe_grad")),
+               ("AdamW update", ("adamw",))]
+
+
+def summarize_hbm(fetch_csv, write_csv, probe_mib, out_md, cmds):
+    """HBM bytes and achieved GB/s per kernel class from FETCH_SIZE / WRITE_SIZE.
+
+    Each counter is read per dispatch (KiB) and scaled by the factor that
+    makes the run's plain copy of PROBE_MIB MiB read and write exactly that
+    many bytes; durations come from the dispatch timestamps in the same
+    file.  Achieved GB/s = (fetched + written bytes) / kernel time.
+    """
+    probe_bytes = int(probe_mib) * (1 << 20)
+
+    def load(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        probe = [r for r in rows if "MulFunctor" in r["Kernel_Name"]]
+        assert probe, "no copy-probe dispatch in " + path
+        calib = probe_bytes / (float(probe[-1]["Counter_Value"]) * 1024.0)
+        return calib, rows
+    cf, fr = load(fetch_csv, "FETCH_SIZE")
+    cw, wr = load(write_csv, "WRITE_SIZE")
+    lines = ["# HBM traffic per kernel class of the FAL training step (serialized launches; workload as in the "
+             "command)", "",
+             "Commands (repository root on the GPU host, `TMPDIR=/tmp`), one counter per run:", "",
+             "```", *cmds, "```", "",
+             f"Counter calibration by the run's plain copy of {int(probe_mib)} MiB: FETCH_SIZE x {cf:.4f}, "
+             f"WRITE_SIZE x {cw:.4f}.", "Kernel time is the FETCH_SIZE run's dispatch time; HBM peak 8000 GB/s.", "",
+             "| class | dispatches | kernel ms | fetched MB | written MB | GB/s | of 8 TB/s |",
+             "|---|---|---|---|---|---|---|"]
+    for label, keys in HBM_CLASSES:
+        f = [r for r in fr if any(k in r["Kernel_Name"] for k in keys)]
+        w = [r for r in wr if any(k in r["Kernel_Name"] for k in keys)]
+        if not f or not w:
+            continue
+        fb = sum(float(r["Counter_Value"]) for r in f) * 1024.0 * cf
+        wb = sum(float(r["Counter_Value"]) for r in w) * 1024.0 * cw
+        t = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in f) * 1e-9
+        gbs = (fb + wb) / t / 1e9
+        lines.append(f"| {label} | {len(f)} | {t * 1e3:.2f} | {fb / 1e6:.0f} | {wb / 1e6:.0f} | {gbs:.0f} | "
+                     f"{gbs / 8000:.2f} |")
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
     if args.summarize_stats:
@@ -393,6 +447,9 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma, args.cmd)
+        return
+    if args.summarize_hbm:
+        summarize_hbm(*args.summarize_hbm, args.cmd)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "

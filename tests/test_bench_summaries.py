@@ -48,3 +48,32 @@ def test_summarize_mfma_known_counts(tmp_path):
     assert attn.split("|")[2:7] == [" 1 ", " 0.04 ", " 500 ", " 0.200 ", " 20.0% "]
     assert "zero_kernel" not in text
     assert "attention backward" not in text  # classes with no dispatches are left out
+
+
+def test_summarize_hbm_calibrated_rates(tmp_path):
+    # counters read half the copy's bytes on fetch (factor 2) and all on write
+    hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    probe = "void at::native::vectorized_elementwise_kernel<4, at::native::MulFunctor<float> >(int)"
+    ln = "void fal::ln_bwd_v4<bf16, 3>(fal::LnBwdArgs)"
+    ce = "void fal::ce_rows_x8<7>(bf16 const*, int const*, int, int, float, bf16*, float*)"
+    mib = 1 << 20
+    fetch = [[1, ln, "FETCH_SIZE", 50 * mib / 1024 / 2, 0, 20000],        # 50 MiB in 20 us
+             [2, ce, "FETCH_SIZE", 100 * mib / 1024 / 2, 30000, 80000],   # 100 MiB in 50 us
+             [3, probe, "FETCH_SIZE", 1024 * mib / 1024 / 2, 90000, 99000]]
+    write = [[1, ln, "WRITE_SIZE", 30 * mib / 1024, 0, 21000],
+             [2, ce, "WRITE_SIZE", 100 * mib / 1024, 30000, 81000],
+             [3, probe, "WRITE_SIZE", 1024 * mib / 1024, 90000, 99000]]
+    _write(tmp_path / "f.csv", hdr, fetch)
+    _write(tmp_path / "w.csv", hdr, write)
+    out = tmp_path / "out.md"
+    bench.summarize_hbm(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), 1024, str(out), ["cmd"])
+    lines = out.read_text().splitlines()
+    assert "FETCH_SIZE x 2.0000, WRITE_SIZE x 1.0000" in "\n".join(lines)
+    lnl = next(l for l in lines if l.startswith("| LayerNorm")).split("|")
+    cel = next(l for l in lines if l.startswith("| cross-entropy")).split("|")
+    # kernel time from the fetch run's timestamps
+    assert lnl[2:5] == [" 1 ", " 0.02 ", f" {50 * mib / 1e6:.0f} "]
+    assert lnl[5].strip() == f"{30 * mib / 1e6:.0f}"
+    assert lnl[6].strip() == f"{80 * mib / 20e-6 / 1e9:.0f}"
+    assert cel[6].strip() == f"{200 * mib / 50e-6 / 1e9:.0f}"
+    assert not any(l.startswith("| bf16 GEMMs") for l in lines)
