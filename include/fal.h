@@ -176,32 +176,60 @@ fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
 
 fal_status_t fal_destroy(fal_ctx_t* ctx);
 
-/* Forward of block `layer` (0-based).
+/* Forward of block `layer` (0-based): X_{i+1} from X_i for i = layer + 1.
+ * Defines: GPT, the Pre-LN block of Sec. 2 (Eq. 1); FAL, the block output of
+ * Sec. 4.1 (Eq. 2) with the first-attention LayerNorm applied once, in the
+ * first block (Sec. 4.1 and its footnote); FAL+, the block equation of
+ * Appendix D (Ablation study, "FAL+"): the first block is the GPT block,
+ * every later block adds its own LayerNorm of the first attention output to
+ * the MLP input; PARALLEL, the shared-input block Sec. 6.1 compares against.
  *   block_params  device, dtype, one block in the FAL_B_* layout
  *   x_in, x_out   device fp32 [M, d]; x_out = block output (may not alias x_in)
- *   first_attn    device dtype [M, d].  FAL: block 0 writes F = LN_F(A_1),
+ *   first_attn    device dtype [M, d], caller-owned for the whole step.
+ *                 FAL: block 0 writes F = LN_F(A_1) (A_1 = MHA_1(LN(X_1))),
  *                 later blocks read it.  FAL+: block 0 writes the shared
- *                 normalisation of A_1, later blocks read it.  GPT and
- *                 parallel: ignored (may be NULL).
- * Saves the activations block `layer`'s backward needs in the workspace. */
+ *                 normalisation (A_1 - mean) * rstd of A_1, later blocks read
+ *                 it and apply their own gain and shift.  GPT and parallel:
+ *                 ignored (may be NULL).  Required (non-NULL) for FAL, FAL+.
+ * Saves the activations block `layer`'s backward needs in the workspace
+ * (block 0 of FAL / FAL+ also keeps A_1 and its LayerNorm statistics there).
+ * Blocks must run in order 0 .. L-1 within a step.  Errors:
+ * FAL_ERR_INVALID_ARG for a layer out of range, a NULL or aliased pointer. */
 fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
                            const float* x_in, float* x_out, void* first_attn);
 
-/* Backward of block `layer`; requires fal_block_fwd(layer) of the same step.
+/* Backward of block `layer`; requires fal_block_fwd(layer) of the same step
+ * (and, for block 0 of FAL / FAL+, the A_1 it saved).  The gradient of the
+ * block equation named at fal_block_fwd; for FAL the first-attention term
+ * receives dF = sum over blocks of dH2_i, and block 0 turns it into the
+ * gradient of A_1 through LN_F's backward.  For FAL+ the per-block terms
+ * gamma_{F,i} * xhat + beta_{F,i} share one normalisation xhat of A_1, and the
+ * normalisation's backward is linear in its input gradient, so blocks >= 1
+ * accumulate d(xhat) = sum gamma_{F,i} * dH2_i and block 0 applies one
+ * normalisation backward to the sum.
  *   x_in          device fp32 [M, d], the same input given to the forward
+ *   first_attn    device dtype [M, d], the tensor block 0's forward wrote
+ *                 (FAL+: read for the gradient of gamma_{F,i}; FAL: unused,
+ *                 may be NULL; GPT and parallel: ignored)
  *   dx_out        device fp32 [M, d], gradient w.r.t. the block output
  *   dx_in         device fp32 [M, d], receives the gradient w.r.t. x_in
+ *                 (may not alias dx_out)
  *   d_first_attn  device fp32 [M, d] accumulator of the gradient w.r.t. the
  *                 first-attention tensor (FAL: F; FAL+: the normalisation).
- *                 Block n_layer-1 overwrites it, blocks below accumulate,
- *                 block 0 consumes it.  GPT and parallel: ignored (may be
- *                 NULL).
- *   block_grads   device fp32, one block in the FAL_B_* layout, overwritten */
+ *                 Blocks run in order L-1 .. 0: block L-1 overwrites it,
+ *                 blocks below accumulate into it, block 0 consumes it.
+ *                 GPT and parallel: ignored (may be NULL).
+ *   block_grads   device fp32, one block in the FAL_B_* layout, overwritten
+ *                 (unused LN_F slots are written as zeros) */
 fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_params,
-                           const float* x_in, const float* dx_out, float* dx_in,
-                           float* d_first_attn, float* block_grads);
+                           const float* x_in, const void* first_attn, const float* dx_out,
+                           float* dx_in, float* d_first_attn, float* block_grads);
 
-/* One whole training step of the language model (has_embed_head == 1).
+/* One whole training step of the language model (has_embed_head == 1):
+ * embedding, the block stack of the config's architecture (the equations
+ * named at fal_block_fwd), final LayerNorm, LM head tied to the token
+ * embedding, mean next-token cross-entropy (the GPT-2 language-modelling
+ * setup of Sec. 6.1), then the backward of all of it.
  *   params  device, dtype, full layout of fal_param_layout
  *   tokens  device int32 [B, T+1]; the model reads [:, :T] and predicts
  *           [:, 1:]; ids must lie in [0, V) (out-of-range ids are clamped)
@@ -209,17 +237,21 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
  *   logits  device fp32 [B*T, V] or NULL to skip writing them; the step
  *           keeps the logits in the config's dtype (bf16 in bf16 mode, the
  *           precision of the LM-head product) and widens them here
- *   grads   device fp32, full layout, overwritten */
+ *   grads   device fp32, full layout, overwritten
+ * Errors: FAL_ERR_INVALID_ARG for NULL pointers or has_embed_head == 0. */
 fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* tokens,
                             float* loss, float* logits, float* grads);
 
 /* One training step of a block stack without embedding or head
- * (has_embed_head == 0): forward of every block from x_in, surrogate loss
- * sum(dy * X_L) so the gradient entering the last block is dy, backward.
+ * (has_embed_head == 0; one GPU's share of a tensor-parallel model, Sec. 4.2
+ * and Appendix B): forward of every block from x_in (the equations named at
+ * fal_block_fwd), surrogate loss sum(dy * X_L) so the gradient entering the
+ * last block is dy, backward.
  *   x_in   device fp32 [M, d]      dy   device fp32 [M, d]
  *   loss   device fp32 scalar or NULL
  *   grads  device fp32, full layout, overwritten
- *   dx_in  device fp32 [M, d] or NULL: gradient w.r.t. x_in */
+ *   dx_in  device fp32 [M, d] or NULL: gradient w.r.t. x_in
+ * Errors: FAL_ERR_INVALID_ARG for NULL pointers or has_embed_head == 1. */
 fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_in,
                             const float* dy, float* loss, float* grads, float* dx_in);
 

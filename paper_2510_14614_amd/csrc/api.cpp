@@ -102,6 +102,24 @@ const char* validate_hd(const fal_config_t* c) {
   return nullptr;
 }
 
+// The bf16 GEMM kernels address each operand through a buffer descriptor
+// with 32-bit byte offsets, and a weight-gradient operand (contraction over
+// the M token rows) is read up to 256 rows past its end inside that range.
+// So every [M, width] operand of the step -- the saved activations [M, d],
+// [M, dA + 2 dKV], [M, dA + f] and the logits [M, V] -- must span less than
+// 2 GiB including those rows.  (The fp32 parity path indexes with 64 bits.)
+const char* validate_extent(const fal_config_t* c) {
+  if (c->dtype != FAL_BF16) return nullptr;
+  const Dims D = dims_of(*c);
+  const int64_t es = 2;
+  int64_t width = std::max<int64_t>({(int64_t)D.d, (int64_t)D.dqkv, (int64_t)D.dA + D.f});
+  if (c->has_embed_head) width = std::max<int64_t>(width, D.Vp);
+  const int64_t limit = ((int64_t)1 << 31) - ((int64_t)1 << 20);
+  if (((int64_t)D.M + 256) * width * es >= limit)
+    return "batch*seq_len too large: a bf16 GEMM operand would span 2 GiB or more (not supported)";
+  return nullptr;
+}
+
 struct Layout {
   int64_t goff[FAL_P_NGLOBAL];
   int64_t boff[FAL_B_NTENSOR];
@@ -169,7 +187,6 @@ struct Work {
   float* dfirst;               // [M, d]
   float *dxa, *dxb, *dxm, *da, *dh1, *dh2;
   void *lp_a, *lp_b, *dxm_lp, *da_lp, *dog, *dqkv;
-  void* first_in;              // first-attention tensor of the current step
   float* Dvec;
   float *part_main, *part_aux;
   float* bias_part;  // packed column-sum partials of one block's bias gradients
@@ -246,7 +263,6 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.loss_tmp = cv.take<float>(64);
   W.opt_part = cv.take<double>(kNormBlocks);
   W.opt_ctrl = cv.take<float>(16);
-  W.first_in = W.first;
   *total = cv.off + kAlignBytes;
 }
 
@@ -630,14 +646,16 @@ struct Run {
     return a;
   }
 
-  // dy: fp32 gradient of the block output; dy_lp: its dtype copy.
-  void block_bwd(int layer, const void* bp, const float* x, const float* dy, const void* dy_lp,
-                 float* dx, void* dx_lp, float* dfirst, float* gb) {
-    block_bwd_parts(layer, bp, x, dy, dy_lp, dx, dx_lp, dfirst, gb);
+  // dy: fp32 gradient of the block output; dy_lp: its dtype copy.  first:
+  // the first-attention tensor the forward read (FAL+: the normalisation of
+  // A_1, whose product with dH2 gives the block's LN_{F,i} gain gradient).
+  void block_bwd(int layer, const void* bp, const float* x, const void* first, const float* dy,
+                 const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
+    block_bwd_parts(layer, bp, x, first, dy, dy_lp, dx, dx_lp, dfirst, gb);
     flush_bias(ctx->sm);  // after the join: the aux stream's gradients are complete
   }
-  void block_bwd_parts(int layer, const void* bp, const float* x, const float* dy, const void* dy_lp,
-                       float* dx, void* dx_lp, float* dfirst, float* gb) {
+  void block_bwd_parts(int layer, const void* bp, const float* x, const void* first, const float* dy,
+                       const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
     const Dims& D = ctx->D;
     Work& W = ctx->W;
     const LayerSlot& S = W.slots[layer];
@@ -699,7 +717,7 @@ struct Run {
     a2.dy2 = W.dh2; a2.g2 = P(bp, FAL_B_LN2_G); a2.dres = dy; a2.dx = W.dxm; a2.dx_lp = W.dxm_lp;
     a2.dg2 = G(gb, FAL_B_LN2_G); a2.db2 = G(gb, FAL_B_LN2_B);
     if (arch == FAL_ARCH_FALPLUS && layer > 0) {
-      a2.xhatF = ctx->W.first_in; a2.gF = P(bp, FAL_B_LNF1_G);
+      a2.xhatF = first; a2.gF = P(bp, FAL_B_LNF1_G);
       a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
       a2.dgF = G(gb, FAL_B_LNF1_G); a2.dbF = G(gb, FAL_B_LNF1_B);
     }
@@ -754,6 +772,7 @@ const char* fal_last_error(const fal_ctx_t* ctx) { return ctx ? ctx->err.c_str()
 fal_status_t fal_validate_config(const fal_config_t* cfg) {
   const char* why = validate(cfg);
   if (!why) why = validate_hd(cfg);
+  if (!why) why = validate_extent(cfg);
   if (!why) return FAL_OK;
   return unsupported(why) ? FAL_ERR_UNSUPPORTED : FAL_ERR_INVALID_ARG;
 }
@@ -854,7 +873,6 @@ fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
   if (x_in == x_out) return bad(ctx, "x_out may not alias x_in");
   const bool uses_first = ctx->cfg.arch == FAL_ARCH_FAL || ctx->cfg.arch == FAL_ARCH_FALPLUS;
   if (uses_first && !first_attn) return bad(ctx, "first_attn is required for FAL and FAL+");
-  ctx->W.first_in = first_attn;
   try {
     Run r(ctx);
     r.block_fwd(layer, block_params, x_in, x_out, first_attn);
@@ -865,7 +883,8 @@ fal_status_t fal_block_fwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
 }
 
 fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_params, const float* x_in,
-                           const float* dx_out, float* dx_in, float* d_first_attn, float* block_grads) {
+                           const void* first_attn, const float* dx_out, float* dx_in, float* d_first_attn,
+                           float* block_grads) {
   fal_status_t st = check_ctx(ctx);
   if (st != FAL_OK) return st;
   if (layer < 0 || layer >= ctx->D.L) return bad(ctx, "layer out of range");
@@ -874,11 +893,13 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
   if (dx_in == dx_out) return bad(ctx, "dx_in may not alias dx_out");
   const bool uses_first = ctx->cfg.arch == FAL_ARCH_FAL || ctx->cfg.arch == FAL_ARCH_FALPLUS;
   if (uses_first && !d_first_attn) return bad(ctx, "d_first_attn is required for FAL and FAL+");
+  if (ctx->cfg.arch == FAL_ARCH_FALPLUS && !first_attn)
+    return bad(ctx, "first_attn (the normalised first attention output) is required for FAL+");
   try {
     Run r(ctx);
     const int64_t Md = (int64_t)ctx->D.M * ctx->D.d;
     FAL_TRY(cast_from_f32(r.dt, dx_out, ctx->W.lp_a, Md, ctx->sm));
-    r.block_bwd(layer, block_params, x_in, dx_out, ctx->W.lp_a, dx_in, ctx->W.lp_b, d_first_attn,
+    r.block_bwd(layer, block_params, x_in, first_attn, dx_out, ctx->W.lp_a, dx_in, ctx->W.lp_b, d_first_attn,
                 block_grads);
   } catch (Fail&) {
     return FAL_ERR_HIP;
@@ -901,7 +922,6 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
   auto gparam = [&](int k) { return pb + Lo.goff[k] * (int64_t)D.es; };
   auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
   auto bgrad = [&](int i) { return grads + Lo.block_base + (int64_t)i * Lo.block_stride; };
-  W.first_in = W.first;
   try {
     Run r(ctx);
     // The embedding backward's (id, position) sort depends on the tokens
@@ -950,7 +970,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
     float *cur = W.dxa, *nxt = W.dxb;
     void *cur_lp = W.lp_a, *nxt_lp = W.lp_b;
     for (int i = D.L - 1; i >= 0; --i) {
-      r.block_bwd(i, bparam(i), W.resid + i * Md, cur, cur_lp, nxt, nxt_lp, W.dfirst, bgrad(i));
+      r.block_bwd(i, bparam(i), W.resid + i * Md, W.first, cur, cur_lp, nxt, nxt_lp, W.dfirst, bgrad(i));
       std::swap(cur, nxt);
       std::swap(cur_lp, nxt_lp);
     }
@@ -981,7 +1001,6 @@ fal_status_t fal_model_forward(fal_ctx_t* ctx, const void* params, const int32_t
   const char* pb = static_cast<const char*>(params);
   auto gparam = [&](int k) { return pb + Lo.goff[k] * (int64_t)D.es; };
   auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
-  W.first_in = W.first;
   try {
     Run r(ctx);
     r.fwd_only = true;
@@ -1023,7 +1042,6 @@ fal_status_t fal_stack_forward(fal_ctx_t* ctx, const void* params, const float* 
   const char* pb = static_cast<const char*>(params);
   auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
   auto xin = [&](int i) { return i == 0 ? x_in : W.resid + i * Md; };
-  W.first_in = W.first;
   try {
     Run r(ctx);
     r.fwd_only = true;
@@ -1051,7 +1069,6 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
   auto bparam = [&](int i) { return pb + (Lo.block_base + (int64_t)i * Lo.block_stride) * (int64_t)D.es; };
   auto bgrad = [&](int i) { return grads + Lo.block_base + (int64_t)i * Lo.block_stride; };
   auto xin = [&](int i) { return i == 0 ? x_in : W.resid + i * Md; };
-  W.first_in = W.first;
   try {
     Run r(ctx);
     for (int i = 0; i < D.L; ++i) r.block_fwd(i, bparam(i), xin(i), W.resid + (i + 1) * Md, W.first);
@@ -1064,7 +1081,7 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
     int k = 0;
     for (int i = D.L - 1; i >= 0; --i) {
       float* out = (i == 0 && dx_in) ? dx_in : bufs[k];
-      r.block_bwd(i, bparam(i), xin(i), cur, lps[k], out, lps[k ^ 1], W.dfirst, bgrad(i));
+      r.block_bwd(i, bparam(i), xin(i), W.first, cur, lps[k], out, lps[k ^ 1], W.dfirst, bgrad(i));
       cur = out;
       k ^= 1;
     }

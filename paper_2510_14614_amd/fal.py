@@ -85,7 +85,7 @@ def lib():
         L.fal_destroy.argtypes = [c_void_p]
         L.fal_block_fwd.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_block_bwd.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
-                                    c_void_p, c_void_p]
+                                    c_void_p, c_void_p, c_void_p]
         L.fal_model_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_stack_step.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_model_forward.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
@@ -274,9 +274,11 @@ class Fal:
                                    c_void_p(x_in.data_ptr()), c_void_p(x_out.data_ptr()),
                                    c_void_p(first.data_ptr()) if first is not None else None), self.ctx)
 
-    def block_bwd(self, layer, x_in, dx_out, dx_in, dfirst):
+    def block_bwd(self, layer, x_in, first, dx_out, dx_in, dfirst):
         _check(lib().fal_block_bwd(self.ctx, layer, c_void_p(self.block_param_ptr(layer)),
-                                   c_void_p(x_in.data_ptr()), c_void_p(dx_out.data_ptr()),
+                                   c_void_p(x_in.data_ptr()),
+                                   c_void_p(first.data_ptr()) if first is not None else None,
+                                   c_void_p(dx_out.data_ptr()),
                                    c_void_p(dx_in.data_ptr()),
                                    c_void_p(dfirst.data_ptr()) if dfirst is not None else None,
                                    c_void_p(self.block_grad_ptr(layer))), self.ctx)

@@ -119,5 +119,27 @@ def test_init_rejects_bad_arguments_without_gpu():
     assert lib.fal_destroy(None) == fal.FAL_ERR_INVALID_ARG
     assert lib.fal_model_step(None, None, None, None, None, None) == fal.FAL_ERR_INVALID_ARG
     assert lib.fal_block_fwd(None, 0, None, None, None, None) == fal.FAL_ERR_INVALID_ARG
+    assert lib.fal_block_bwd(None, 0, None, None, None, None, None, None, None) == fal.FAL_ERR_INVALID_ARG
     assert lib.fal_last_error(None) == b""
     assert lib.fal_status_string(fal.FAL_ERR_WORKSPACE) == b"workspace too small"
+
+
+def test_gemm_operand_extent_limit():
+    # The bf16 GEMM kernels address operands with 32-bit offsets: a block
+    # stack whose [M, dA + f] activations (with the 256-row read-ahead of a
+    # weight-gradient operand) would reach 2 GiB is rejected as unsupported,
+    # one just below the limit is accepted.  d 1024, dA 1024, f 4096: rows of
+    # 10240 bytes in bf16, so the limit lies at M + 256 = 209612 rows.
+    base = dict(n_layer=4, d_model=1024, n_head=16, head_dim=64, d_ff=4096, vocab=0, seq_len=2048,
+                arch=1, dtype=1, has_embed_head=0)
+    from paper_2510_14614_amd.config import Config
+    assert fal.validate_config(Config(batch=102, **base)) == fal.FAL_OK          # M = 208896
+    assert fal.validate_config(Config(batch=103, **base)) == fal.FAL_ERR_UNSUPPORTED  # M = 210944
+    assert fal.validate_config(Config(batch=128, **base)) == fal.FAL_ERR_UNSUPPORTED  # M = 262144
+    # with the LM head the logits [M, V] (V padded to 65536) are the widest
+    # operand: 15616 x 65536 x 2 bytes fit, 16640 x 65536 x 2 do not
+    lm = dict(n_layer=1, d_model=64, n_head=1, head_dim=64, d_ff=64, vocab=65535, seq_len=1024, arch=1, dtype=1)
+    assert fal.validate_config(Config(batch=15, **lm)) == fal.FAL_OK
+    assert fal.validate_config(Config(batch=16, **lm)) == fal.FAL_ERR_UNSUPPORTED
+    # fp32 parity mode indexes with 64 bits and is not limited this way
+    assert fal.validate_config(Config(batch=103, **{**base, "dtype": 0})) == fal.FAL_OK

@@ -62,8 +62,8 @@ def test_model_forward_matches_oracle_and_step(arch, dtype):
 @pytest.mark.parametrize("arch", ARCHS)
 def test_stack_forward_matches_oracle_and_step(arch, dtype):
     import torch
-    # the tensor-parallel shard layout: d_model != n_head * head_dim
-    cfg = Config(n_layer=2, d_model=256, n_head=2, head_dim=128, d_ff=344, vocab=0, seq_len=136,
+    # the tensor-parallel shard layout: d_model (384) != n_head * head_dim (256)
+    cfg = Config(n_layer=2, d_model=384, n_head=2, head_dim=128, d_ff=344, vocab=0, seq_len=136,
                  batch=2, arch=arch, dtype=dtype, has_embed_head=0)
     log(f"stack forward arch={arch} dtype={dtype}")
     _, blocks = synth.make_params(cfg, seed=42)

@@ -1,17 +1,18 @@
 """GPU parity at the full workload sizes.
 
-The oracle cannot run a whole batch of the large configs in seconds, so:
-  * the GPT-2-small FAL step runs on the GPU at its full size and in the
-    launch configuration bench.py times (B=8, T=1024, 12 layers, V=50257,
-    two-stream merged schedule); sequences are independent, so the oracle
-    run on sequence 0 alone gives exactly that sequence's logits;
-  * gradients are compared per sequence (GPU and oracle at B=1, full model),
-    and the batch gradient is checked against the property that holds at
-    any size: the gradient of the batch-mean loss is the mean of the
-    per-sequence gradients;
-  * GPT-2-medium (FAL+) is compared at full depth with B=1; the ~1.3B and the
-    7B tensor-parallel shard shapes on two-layer slices with every other
-    dimension full size.
+The full batch of every config runs on the GPU in the launch configuration
+bench.py times (same M = B*T rows, so the same GEMM tile shapes, split-K
+factors and attention grids), and is compared with the oracle:
+  * GPT-2-small (FAL) and the ~1.3B shape (FAL): the whole batch (B=8 T=1024
+    and B=4 T=2048, M = 8192) with two blocks, so both the sequential first
+    block and the two-branch later blocks run; logits, loss and every
+    gradient against the oracle run on the same full batch;
+  * the 7B tensor-parallel shard shape: the whole batch (B=2, T=2048) of a
+    two-block stack;
+  * GPT-2-small at full depth (12 blocks) on one sequence, GPT-2-medium
+    (FAL+) at full depth on one sequence;
+  * the property that holds at any size: the gradient of the batch-mean loss
+    is the mean of the per-sequence gradients (full GPT-2-small, 12 blocks).
 Tolerance: 2e-2 max relative error (inf-norm per tensor), bf16 mode.
 """
 import numpy as np
@@ -113,26 +114,39 @@ def test_gpt2_medium_falplus_full_depth():
     compare_step(cfg, gpu, oracle.train_step(cfg, g, blocks, tok), label="gpt2-medium FAL+")
 
 
-def test_gpt_1p3b_two_layer_slice():
-    cfg = get_config("gpt-1.3b", arch=ARCH_FAL, sched=SCHED_STREAMS_MERGED, batch=1, n_layer=2)
+@pytest.mark.timeout(900)
+def test_gpt2_small_full_batch_two_blocks_match_oracle():
+    cfg = get_config("gpt2-small", sched=SCHED_STREAMS_MERGED, n_layer=2)
+    g, blocks = synth.make_params(cfg, seed=30)
+    tok = synth.make_tokens(cfg, seed=31)
+    log("gpt2-small L=2 full batch (M=8192): GPU")
+    gpu = gpu_model_step(cfg, g, blocks, tok)
+    log("gpt2-small L=2 full batch: oracle")
+    compare_step(cfg, gpu, oracle.train_step(cfg, g, blocks, tok), label="gpt2-small L=2 B=8")
+
+
+@pytest.mark.timeout(900)
+def test_gpt_1p3b_full_batch_two_blocks_match_oracle():
+    cfg = get_config("gpt-1.3b", arch=ARCH_FAL, sched=SCHED_STREAMS_MERGED, n_layer=2)
     g, blocks = synth.make_params(cfg, seed=5)
     tok = synth.make_tokens(cfg, seed=6)
-    log("1.3B slice: GPU")
+    log("1.3B L=2 full batch (M=8192): GPU")
     gpu = gpu_model_step(cfg, g, blocks, tok)
-    log("1.3B slice: oracle")
-    compare_step(cfg, gpu, oracle.train_step(cfg, g, blocks, tok), label="1.3B slice")
+    log("1.3B L=2 full batch: oracle")
+    compare_step(cfg, gpu, oracle.train_step(cfg, g, blocks, tok), label="1.3B L=2 B=4")
 
 
-def test_7b_shard_two_layer_slice():
-    cfg = get_config("7b-tp-shard", sched=SCHED_STREAMS_MERGED, batch=1, n_layer=2)
+@pytest.mark.timeout(900)
+def test_7b_shard_full_batch_two_blocks_match_oracle():
+    cfg = get_config("7b-tp-shard", sched=SCHED_STREAMS_MERGED, n_layer=2)
     _, blocks = synth.make_params(cfg, seed=7)
     x1, gout = synth.make_stack_inputs(cfg, seed=8)
-    log("7B shard slice: GPU")
+    log("7B shard L=2 full batch (M=4096): GPU")
     gpu = gpu_stack_step(cfg, blocks, x1, gout)
-    log("7B shard slice: oracle")
+    log("7B shard L=2 full batch: oracle")
     ref = oracle.stack_step(cfg, blocks, x1, gout)
     ref["loss_scale"] = float(np.abs(gout * ref["y"]).sum())
-    compare_step(cfg, gpu, ref, label="7B shard slice")
+    compare_step(cfg, gpu, ref, label="7B shard L=2 B=2")
 
 
 @pytest.mark.parametrize("name", ["mlm-48", "mlm-48-gqa2"])

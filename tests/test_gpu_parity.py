@@ -101,8 +101,8 @@ def test_ragged_model_step(arch, dtype):
 @pytest.mark.parametrize("dtype", [0, 1])
 @pytest.mark.parametrize("arch", ARCHS)
 def test_stack_step_shard_shapes(arch, dtype):
-    # the tensor-parallel shard layout: d_model != n_head * head_dim
-    cfg = Config(n_layer=2, d_model=256, n_head=2, head_dim=128, d_ff=344, vocab=0, seq_len=136,
+    # the tensor-parallel shard layout: d_model (384) != n_head * head_dim (256)
+    cfg = Config(n_layer=2, d_model=384, n_head=2, head_dim=128, d_ff=344, vocab=0, seq_len=136,
                  batch=2, arch=arch, dtype=dtype, has_embed_head=0)
     log(f"stack step arch={arch} dtype={dtype}")
     _, blocks = synth.make_params(cfg, seed=6)
@@ -259,3 +259,52 @@ def test_run_to_run_deterministic():
     F.close()
     for x, y in zip(_all_outputs(o1), _all_outputs(o2)):
         np.testing.assert_array_equal(x, y)
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL, ARCH_FALPLUS])
+def test_erf_gelu_model_step(arch, dtype):
+    # the erf form of GELU (gelu_tanh = 0) in the FFN-up epilogue and the
+    # derivative it stores for the backward; ragged shapes so the bf16 run
+    # takes the matrix-core epilogue on partial tiles
+    cfg = _ragged(arch, dtype, gelu_tanh=0, sched=SCHED_STREAMS_MERGED)
+    log(f"erf GELU model step arch={arch} dtype={dtype}")
+    g, blocks = synth.make_params(cfg, seed=20)
+    tok = synth.make_tokens(cfg, seed=21, dist="zipf")
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"erf a{arch} dt{dtype}")
+
+
+def _forward_logits(F, tok):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(tok)).cuda()
+    out = torch.zeros(F.cfg.tokens, F.cfg.vocab, device="cuda")
+    F.model_forward(t, out, loss=False)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("arch", ARCHS)
+def test_causality_bitwise(arch):
+    # perturbing the input token at position t of one sequence leaves that
+    # sequence's logits at positions < t and every other sequence's logits
+    # bitwise unchanged (no GEMM reduction crosses rows, attention masks
+    # keys > query), while position t itself changes
+    import torch
+    cfg = _ragged(arch, 1, sched=SCHED_STREAMS_MERGED, seq_len=300)
+    log(f"causality arch={arch}")
+    g, blocks = synth.make_params(cfg, seed=22)
+    tok = synth.make_tokens(cfg, seed=23, dist="zipf")
+    F = fal.Fal(cfg)
+    F.load_params(g, blocks)
+    base = _forward_logits(F, tok)
+    T = cfg.seq_len
+    for b, t in ((1, 0), (1, 137), (2, T - 1)):
+        pert = tok.copy()
+        pert[b, t] = (pert[b, t] + 1 + 17 * t) % cfg.vocab
+        out = _forward_logits(F, pert)
+        row0 = b * T
+        assert torch.equal(out[:row0 + t], base[:row0 + t]), (b, t)
+        assert torch.equal(out[row0 + T:], base[row0 + T:]), (b, t)
+        assert not torch.equal(out[row0 + t], base[row0 + t]), (b, t)
+    F.close()
