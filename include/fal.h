@@ -295,6 +295,29 @@ fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step,
                             float* master, void* params, const float* grads, float* m, float* v,
                             float* grad_norm);
 
+/* The AdamW update of fal_adamw_step without a context and without any
+ * device allocation, for callers that cannot allocate device memory or
+ * create a context: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same kernels in the same order as
+ * fal_adamw_step, so the results are bitwise identical.  Its scratch (the
+ * 2048 fp64 partial sums of the norm pass and the {norm, clip factor}
+ * control block: 16 KiB + 256 B) is a fixed array in the library's device
+ * memory, one per GPU, held until the process ends; its size does not
+ * depend on n.  Every call rewrites that scratch before reading it, so
+ * nothing needs clearing, but calls that overlap on one GPU (two streams or
+ * two host threads) share it and race: the caller must serialise them.
+ *   dtype   fal_dtype_t of params (FAL_BF16: bf16 copy of master; FAL_F32:
+ *           fp32 copy, or NULL / master for an in-place update)
+ *   stream  hipStream_t the work is enqueued on (NULL: the default stream)
+ *   other arguments as for fal_adamw_step.
+ * Errors: FAL_ERR_INVALID_ARG for the argument errors of fal_adamw_step, an
+ * unknown dtype, or n above the update's limit of (2^31 - 1) * 2048
+ * elements; FAL_ERR_HIP when a HIP call fails.  fal_last_error(NULL) returns
+ * the message of the last failed call of this kind on the calling thread. */
+fal_status_t fal_adamw_step_noalloc(const fal_adamw_t* hp, int64_t step, int64_t n, int32_t dtype,
+                                    float* master, void* params, const float* grads, float* m, float* v,
+                                    float* grad_norm, void* stream);
+
 /* Forward pass only, without gradients (the paper's inference measurement,
  * Appendix D.3, times this forward step as the time to first token).
  * Same kernels and schedule as the forward half of fal_model_step; the GELU
@@ -340,7 +363,9 @@ fal_status_t fal_profile_read(fal_ctx_t* ctx, int32_t cls, int64_t* launches, do
                               double* flops, double* bytes);
 
 const char* fal_status_string(fal_status_t status);
-const char* fal_last_error(const fal_ctx_t* ctx); /* "" if none; ctx may be NULL */
+/* "" if none.  ctx NULL: the message of the last failed context-free call
+ * (fal_adamw_step_noalloc) on the calling thread. */
+const char* fal_last_error(const fal_ctx_t* ctx);
 
 #ifdef __cplusplus
 }

@@ -767,7 +767,10 @@ const char* fal_status_string(fal_status_t s) {
   return "unknown status";
 }
 
-const char* fal_last_error(const fal_ctx_t* ctx) { return ctx ? ctx->err.c_str() : ""; }
+// Message of the last failed call made without a context on this thread.
+static thread_local std::string g_noctx_err;
+
+const char* fal_last_error(const fal_ctx_t* ctx) { return ctx ? ctx->err.c_str() : g_noctx_err.c_str(); }
 
 fal_status_t fal_validate_config(const fal_config_t* cfg) {
   const char* why = validate(cfg);
@@ -1096,53 +1099,66 @@ static bool overlaps(const void* a, int64_t abytes, const void* b, int64_t bbyte
   return x < y + (uintptr_t)bbytes && y < x + (uintptr_t)abytes;
 }
 
-fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step, int64_t n, float* master,
-                            void* params, const float* grads, float* m, float* v, float* norm_out) {
-  fal_status_t st = check_ctx(ctx);
-  if (st != FAL_OK) return st;
-  if (!hp) return bad(ctx, "NULL hyper-parameters");
-  if (step < 1) return bad(ctx, "step is 1-based");
-  if (n < 0) return bad(ctx, "negative element count");
+// Host checks shared by both AdamW entry points; on success fills the
+// kernel constants and the dtype-copy mode (0 none, 1 fp32, 2 bf16).
+static const char* adamw_args(const fal_adamw_t* hp, int64_t step, int64_t n, bool bf, float* master,
+                              void* params, const float* grads, float* m, float* v, float* norm_out,
+                              AdamwConsts* k, int* lp_mode_out) {
+  if (!hp) return "NULL hyper-parameters";
+  if (step < 1) return "step is 1-based";
+  if (n < 0) return "negative element count";
   auto finite = [](float x) { return std::isfinite(x); };
   if (!finite(hp->lr) || !finite(hp->beta1) || !finite(hp->beta2) || !finite(hp->eps) ||
       !finite(hp->weight_decay) || !finite(hp->max_grad_norm))
-    return bad(ctx, "non-finite hyper-parameter");
-  if (hp->lr < 0.f || hp->eps < 0.f || hp->weight_decay < 0.f) return bad(ctx, "lr, eps and weight_decay must be >= 0");
+    return "non-finite hyper-parameter";
+  if (hp->lr < 0.f || hp->eps < 0.f || hp->weight_decay < 0.f) return "lr, eps and weight_decay must be >= 0";
   if (!(hp->beta1 >= 0.f && hp->beta1 < 1.f && hp->beta2 >= 0.f && hp->beta2 < 1.f))
-    return bad(ctx, "beta1 and beta2 must lie in [0, 1)");
-  const bool bf = ctx->cfg.dtype == FAL_BF16;
-  if (n > 0 && (!master || !grads || !m || !v)) return bad(ctx, "NULL master, grads, m or v");
-  if (bf && n > 0 && !params) return bad(ctx, "params (bf16 copy) is required for a bf16 config");
+    return "beta1 and beta2 must lie in [0, 1)";
+  if (n > kAdamwMaxElems) return "element count above the update kernel's grid limit";
+  if (n > 0 && (!master || !grads || !m || !v)) return "NULL master, grads, m or v";
+  if (bf && n > 0 && !params) return "params (bf16 copy) is required for a bf16 config";
   const int lp_mode = (!params || params == master) ? 0 : (bf ? 2 : 1);
-  if (bf && lp_mode == 0 && n > 0) return bad(ctx, "params may not alias master for a bf16 config");
+  if (bf && lp_mode == 0 && n > 0) return "params may not alias master for a bf16 config";
   auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
   if (!al(master, 16) || !al(grads, 16) || !al(m, 16) || !al(v, 16) ||
       (lp_mode != 0 && !al(params, lp_mode == 2 ? 8 : 16)))
-    return bad(ctx, "fp32 arrays must be 16-byte aligned, params 8-byte (bf16) or 16-byte (fp32)");
-  if (norm_out && !al(norm_out, 4)) return bad(ctx, "grad_norm must be 4-byte aligned");
+    return "fp32 arrays must be 16-byte aligned, params 8-byte (bf16) or 16-byte (fp32)";
+  if (norm_out && !al(norm_out, 4)) return "grad_norm must be 4-byte aligned";
   const int64_t b4 = n * 4;
   const void* arr[5] = {master, grads, m, v, params};
   const int64_t len[5] = {b4, b4, b4, b4, lp_mode == 0 ? 0 : n * (lp_mode == 2 ? 2 : 4)};
   for (int i = 0; i < 5; ++i)
     for (int j = i + 1; j < 5; ++j)
       if (len[i] > 0 && len[j] > 0 && overlaps(arr[i], len[i], arr[j], len[j]))
-        return bad(ctx, "master, grads, m, v and params may not overlap");
+        return "master, grads, m, v and params may not overlap";
   if (norm_out && n > 0)
     for (int i = 0; i < 5; ++i)
-      if (len[i] > 0 && overlaps(norm_out, 4, arr[i], len[i])) return bad(ctx, "grad_norm overlaps an array");
+      if (len[i] > 0 && overlaps(norm_out, 4, arr[i], len[i])) return "grad_norm overlaps an array";
   // bias corrections and step size in double on the host
   const double bc1 = 1.0 - std::pow((double)hp->beta1, (double)step);
   const double bc2 = 1.0 - std::pow((double)hp->beta2, (double)step);
-  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return bad(ctx, "bias correction underflows (beta too close to 1 for step)");
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return "bias correction underflows (beta too close to 1 for step)";
+  k->beta1 = hp->beta1;
+  k->one_minus_beta1 = (float)(1.0 - (double)hp->beta1);
+  k->beta2 = hp->beta2;
+  k->one_minus_beta2 = (float)(1.0 - (double)hp->beta2);
+  k->eps = hp->eps;
+  k->rsqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  k->step_size = (float)((double)hp->lr / bc1);
+  k->decay = (float)(1.0 - (double)hp->lr * hp->weight_decay);
+  *lp_mode_out = lp_mode;
+  return nullptr;
+}
+
+fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step, int64_t n, float* master,
+                            void* params, const float* grads, float* m, float* v, float* norm_out) {
+  fal_status_t st = check_ctx(ctx);
+  if (st != FAL_OK) return st;
   AdamwConsts k;
-  k.beta1 = hp->beta1;
-  k.one_minus_beta1 = (float)(1.0 - (double)hp->beta1);
-  k.beta2 = hp->beta2;
-  k.one_minus_beta2 = (float)(1.0 - (double)hp->beta2);
-  k.eps = hp->eps;
-  k.rsqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
-  k.step_size = (float)((double)hp->lr / bc1);
-  k.decay = (float)(1.0 - (double)hp->lr * hp->weight_decay);
+  int lp_mode = 0;
+  const char* why = adamw_args(hp, step, n, ctx->cfg.dtype == FAL_BF16, master, params, grads, m, v, norm_out, &k,
+                               &lp_mode);
+  if (why) return bad(ctx, why);
   hipStream_t sm = ctx->sm;
   try {
     const double bytes = 4.0 * n + (double)n * (28.0 + (lp_mode == 2 ? 2.0 : lp_mode == 1 ? 4.0 : 0.0));
@@ -1150,6 +1166,30 @@ fal_status_t fal_adamw_step(fal_ctx_t* ctx, const fal_adamw_t* hp, int64_t step,
     FAL_TRY(grad_norm(grads, n, hp->max_grad_norm, ctx->W.opt_part, ctx->W.opt_ctrl, norm_out, sm));
     FAL_TRY(adamw_update(lp_mode, master, params, grads, m, v, n, k, ctx->W.opt_ctrl, sm));
   } catch (Fail&) {
+    return FAL_ERR_HIP;
+  }
+  return FAL_OK;
+}
+
+fal_status_t fal_adamw_step_noalloc(const fal_adamw_t* hp, int64_t step, int64_t n, int32_t dtype, float* master,
+                                    void* params, const float* grads, float* m, float* v, float* norm_out,
+                                    void* stream) {
+  g_noctx_err.clear();
+  if (dtype != FAL_F32 && dtype != FAL_BF16) {
+    g_noctx_err = "unknown dtype";
+    return FAL_ERR_INVALID_ARG;
+  }
+  AdamwConsts k;
+  int lp_mode = 0;
+  const char* why = adamw_args(hp, step, n, dtype == FAL_BF16, master, params, grads, m, v, norm_out, &k, &lp_mode);
+  if (why) {
+    g_noctx_err = why;
+    return FAL_ERR_INVALID_ARG;
+  }
+  const hipError_t e = adamw_static_scratch(lp_mode, master, params, grads, m, v, n, hp->max_grad_norm, k, norm_out,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    g_noctx_err = std::string("fal_adamw_step_noalloc: ") + hipGetErrorString(e);
     return FAL_ERR_HIP;
   }
   return FAL_OK;

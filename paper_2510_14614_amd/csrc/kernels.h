@@ -252,5 +252,15 @@ hipError_t grad_norm(const float* g, int64_t n, float max_norm, double* part, fl
 // 8-byte (bf16) or 16-byte (fp32) aligned.
 hipError_t adamw_update(int lp_mode, float* master, void* lp, const float* g, float* m, float* v, int64_t n,
                         const AdamwConsts& k, const float* ctrl, hipStream_t s);
+// The update kernel's grid covers 2048 elements per workgroup with at most
+// 2^31 - 1 workgroups.
+constexpr int64_t kAdamwMaxElems = (int64_t)0x7fffffff * 2048;
+// grad_norm + adamw_update with their scratch (the norm partials and the
+// control block) in a fixed device array of the library, one per GPU,
+// instead of caller memory: no allocation anywhere.  The array's address on
+// the current device is looked up once per device.  Calls that overlap on
+// one GPU share the array.
+hipError_t adamw_static_scratch(int lp_mode, float* master, void* lp, const float* g, float* m, float* v, int64_t n,
+                                float max_norm, const AdamwConsts& k, float* norm_out, hipStream_t s);
 
 }  // namespace fal

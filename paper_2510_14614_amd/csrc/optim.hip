@@ -17,6 +17,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -28,6 +29,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 2;                      // float4 units per thread in the update
 constexpr int kChunk = kThreads * 4 * kUnroll;  // elements per update workgroup
+static_assert(kAdamwMaxElems == (int64_t)0x7fffffff * kChunk, "update grid limit");
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
@@ -181,6 +183,54 @@ hipError_t adamw_update(int lp_mode, float* master, void* lp, const float* g, fl
   else
     hipLaunchKernelGGL(adamw_kernel<0>, grid, block, 0, s, master, lp, g, m, v, n, k, ctrl);
   return hipGetLastError();
+}
+
+// Scratch of the allocation-free update (adamw_static_scratch): the norm
+// pass's kNormBlocks fp64 partials, then the two-float control block.
+// Every call rewrites all of it before reading it (each norm workgroup
+// writes its partial, the norm kernel writes the control block), so nothing
+// needs clearing between calls.  16 KiB + 256 B per GPU, held until the
+// process ends.
+constexpr size_t kScratchPartBytes = (size_t)kNormBlocks * sizeof(double);
+constexpr size_t kScratchBytes = kScratchPartBytes + 256;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+// The array's device address per GPU.  In host code the name `scratch` is a
+// host-side stand-in, not a device address, so kernels only ever receive the
+// address hipGetSymbolAddress returns for the current device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+hipError_t scratch_on_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t adamw_static_scratch(int lp_mode, float* master, void* lp, const float* g, float* m, float* v, int64_t n,
+                                float max_norm, const AdamwConsts& k, float* norm_out, hipStream_t s) {
+  void* base = nullptr;
+  hipError_t e = scratch_on_current_device(&base);
+  if (e != hipSuccess) return e;
+  double* part = static_cast<double*>(base);
+  float* ctrl = reinterpret_cast<float*>(static_cast<char*>(base) + kScratchPartBytes);
+  e = grad_norm(g, n, max_norm, part, ctrl, norm_out, s);
+  if (e != hipSuccess) return e;
+  return adamw_update(lp_mode, master, lp, g, m, v, n, k, ctrl, s);
 }
 
 }  // namespace fal

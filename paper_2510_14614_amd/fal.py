@@ -28,7 +28,7 @@ ABI_FUNCTIONS = (
     "fal_validate_config", "fal_param_layout", "fal_workspace_bytes", "fal_init", "fal_destroy",
     "fal_block_fwd", "fal_block_bwd", "fal_model_step", "fal_stack_step", "fal_residual_out",
     "fal_profile_enable", "fal_profile_read", "fal_status_string", "fal_last_error", "fal_adamw_step",
-    "fal_model_forward", "fal_stack_forward",
+    "fal_model_forward", "fal_stack_forward", "fal_adamw_step_noalloc",
 )
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_NORM, PROF_CE, PROF_EMBED, PROF_BIAS, PROF_OPTIM = range(8)
 PROF_NAMES = {PROF_GEMM: "gemm", PROF_ATTN_FWD: "attn_fwd", PROF_ATTN_BWD: "attn_bwd", PROF_NORM: "norm",
@@ -96,6 +96,8 @@ def lib():
                                        POINTER(c_double), POINTER(c_double)]
         L.fal_adamw_step.argtypes = [c_void_p, POINTER(fal_adamw_t), c_int64, c_int64, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_void_p, c_void_p]
+        L.fal_adamw_step_noalloc.argtypes = [POINTER(fal_adamw_t), c_int64, c_int64, c_int32, c_void_p, c_void_p,
+                                             c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
         L.fal_status_string.argtypes = [c_int32]
         L.fal_status_string.restype = c_char_p
         L.fal_last_error.argtypes = [c_void_p]
@@ -179,6 +181,21 @@ def unflatten(cfg: Config, flat: np.ndarray, gshapes: dict, bshapes: dict, layou
             d[name] = flat[o:o + n].reshape(bshapes[name]).copy()
         blocks.append(d)
     return g, blocks
+
+
+def adamw_step_noalloc(hp: fal_adamw_t, step: int, n: int, dtype: int, master, params, grads, m, v,
+                       grad_norm=None, stream=None):
+    """fal_adamw_step_noalloc on torch device tensors (no context, no
+    allocation): one AdamW update of n elements on `stream` (a torch stream;
+    None: the current stream)."""
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    ptr = lambda t: c_void_p(t.data_ptr()) if t is not None else None  # noqa: E731
+    st = lib().fal_adamw_step_noalloc(byref(hp), step, n, dtype, ptr(master), ptr(params), ptr(grads), ptr(m), ptr(v),
+                                      ptr(grad_norm), c_void_p(s.cuda_stream))
+    if st != FAL_OK:
+        L = lib()
+        raise FalError(st, f"{L.fal_status_string(st).decode()}: {L.fal_last_error(None).decode()}")
 
 
 class Fal:

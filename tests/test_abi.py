@@ -143,3 +143,27 @@ def test_gemm_operand_extent_limit():
     assert fal.validate_config(Config(batch=16, **lm)) == fal.FAL_ERR_UNSUPPORTED
     # fp32 parity mode indexes with 64 bits and is not limited this way
     assert fal.validate_config(Config(batch=103, **{**base, "dtype": 0})) == fal.FAL_OK
+
+
+def test_noalloc_adamw_rejects_bad_arguments_without_gpu():
+    # argument errors return before any HIP call, with a message readable
+    # through fal_last_error(NULL)
+    from ctypes import byref
+    lib = fal.lib()
+    hp = fal.adamw_params()
+    assert lib.fal_adamw_step_noalloc(None, 1, 0, 1, None, None, None, None, None, None, None) == \
+        fal.FAL_ERR_INVALID_ARG
+    assert b"hyper-parameters" in lib.fal_last_error(None)
+    assert lib.fal_adamw_step_noalloc(byref(hp), 1, 0, 7, None, None, None, None, None, None, None) == \
+        fal.FAL_ERR_INVALID_ARG
+    assert lib.fal_last_error(None) == b"unknown dtype"
+    assert lib.fal_adamw_step_noalloc(byref(hp), 0, 0, 1, None, None, None, None, None, None, None) == \
+        fal.FAL_ERR_INVALID_ARG
+    assert lib.fal_adamw_step_noalloc(byref(hp), 1, -1, 1, None, None, None, None, None, None, None) == \
+        fal.FAL_ERR_INVALID_ARG
+    assert lib.fal_adamw_step_noalloc(byref(hp), 1, 2048 * 0x7fffffff + 1, 0, None, None, None, None, None, None,
+                                      None) == fal.FAL_ERR_INVALID_ARG
+    assert b"grid limit" in lib.fal_last_error(None)
+    bad = fal.adamw_params(beta1=1.0)
+    assert lib.fal_adamw_step_noalloc(byref(bad), 1, 0, 1, None, None, None, None, None, None, None) == \
+        fal.FAL_ERR_INVALID_ARG
