@@ -1,6 +1,6 @@
 """Training-step throughput of the FAL hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config gpt2-small]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config gpt-1.3b]
                     [--arch fal] [--sched streams_merged] [--no-compare] [--no-cpu-baseline]
                     [--single-stream]
 
@@ -24,8 +24,14 @@ Also reported, from the same process:
     every parameter (tokens/s and the update's own time and bandwidth);
   * forward_only: the forward step without gradients (fal_model_forward /
     fal_stack_forward), this architecture and the sequential GPT;
-  * cpu_baseline: the fp64 CPU oracle timed on this host on a bounded sample
-    (batch 1 of the same config).
+  * cpu_baseline: the fp64 CPU oracle timed on this host on a bounded sample:
+    one training step of one sequence through the full-width model with one
+    and with two blocks (full vocabulary), the full-depth step time
+    extrapolated linearly in the block count.
+
+The default workload is the ~1.3B GPT shape (24 blocks, d 2048, 16 heads of
+128, FFN 8192, vocabulary 50257, T 2048, B 4) in the FAL architecture, the
+configuration at which FAL is compared with the same-kernel GPT baseline.
 """
 from __future__ import annotations
 
@@ -42,10 +48,17 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "training tokens/s on 1 MI355X (FAL vs GPT baseline); MFMA util % of bf16 peak"
-# Measured HBM traffic of the GEMM calls of the default workload (rocprofv3
-# FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy); valid only while the
-# sources it was measured on are unchanged.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_gpt2-small_traffic.md")
+# Measured HBM traffic of the GEMM calls of a workload (rocprofv3
+# FETCH_SIZE / WRITE_SIZE, calibrated on a plain copy), one file per config
+# and architecture; valid only while the sources it was measured on are
+# unchanged.
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+
+
+def traffic_file(config, arch):
+    return os.path.join(TRAFFIC_DIR, f"gemm_bf16_{config}_{arch}_traffic.md")
+
+
 TRAFFIC_SOURCES = ("paper_2510_14614_amd/csrc/gemm.hip", "paper_2510_14614_amd/csrc/kernels.h",
                    "paper_2510_14614_amd/csrc/common.h")
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
@@ -57,7 +70,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="gpt2-small")
+    ap.add_argument("--config", default="gpt-1.3b")
     ap.add_argument("--arch", default="fal", choices=["gpt", "fal", "falplus", "fal+", "parallel"])
     ap.add_argument("--sched", default="streams_merged", choices=["seq", "streams", "merged", "streams_merged"])
     ap.add_argument("--no-compare", action="store_true")
@@ -68,7 +81,6 @@ def parse():
                     help="time replays of the step captured as a HIP graph instead of eager launches")
     ap.add_argument("--no-forward", action="store_true",
                     help="skip the extra forward-only measurement (FAL and GPT)")
-    ap.add_argument("--cpu-sample-batch", type=int, default=1)
     ap.add_argument("--single-stream", action="store_true",
                     help="run the timed steps with the aux stream equal to the main stream")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "OUT_MD"),
@@ -84,6 +96,7 @@ def parse():
                     help="offline: write the GEMM traffic summary from two rocprofv3 --pmc counter_collection.csv "
                          "of runs made with --copy-probe PROBE_MIB")
     ap.add_argument("--cmd", action="append", default=[], help="command line(s) recorded in a summary")
+    ap.add_argument("--label", default="gpt-1.3b FAL", help="workload named in a summary's title")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the measurements, run one plain device copy of MIB MiB (fp32 x 2.0 into a second "
                          "buffer): the known-size reference for HBM traffic counters")
@@ -97,11 +110,41 @@ def describe(cfg, arch_name, sched_name):
             f"{sched_name} schedule")
 
 
+_INPUTS = {}
+
+
+def device_inputs(cfg):
+    """Synthetic parameters (flat, in the library's layout and the config's
+    dtype) and token ids or block-stack inputs, on the GPU.  Drawn once per
+    model shape: the layout does not depend on the block architecture or the
+    schedule, so every leg of the bench reuses the same device copies."""
+    import torch
+
+    from paper_2510_14614_amd import fal, synth
+    key = (cfg.n_layer, cfg.d_model, cfg.n_head, cfg.head_dim, cfg.d_ff, cfg.vocab, cfg.seq_len, cfg.batch,
+           cfg.dtype, cfg.has_embed_head, cfg.n_kv_head)
+    if key not in _INPUTS:
+        g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
+        flat = torch.from_numpy(fal.flatten_params(cfg, g, blocks))
+        del g, blocks
+        pdtype = torch.bfloat16 if cfg.dtype == 1 else torch.float32
+        ent = {"params": flat.to(pdtype).cuda()}
+        del flat
+        if cfg.has_embed_head:
+            ent["tok"] = torch.from_numpy(synth.make_tokens(cfg, seed=1)).cuda()
+        else:
+            x1, gout = synth.make_stack_inputs(cfg, seed=2)
+            ent["x1"] = torch.from_numpy(x1).cuda()
+            ent["dy"] = torch.from_numpy(gout).cuda()
+        _INPUTS[key] = ent
+    return _INPUTS[key]
+
+
 class Runner:
     def __init__(self, cfg, single_stream=False, optimizer=False, forward_only=False, graph=False):
         import torch
 
-        from paper_2510_14614_amd import fal, synth
+        from paper_2510_14614_amd import fal
         self.torch = torch
         self.cfg = cfg
         self.optimizer = optimizer
@@ -111,15 +154,13 @@ class Runner:
         main = torch.cuda.Stream() if graph else torch.cuda.current_stream()
         self.F = fal.Fal(cfg, stream_main=main, stream_aux=main if single_stream else None)
         self.graph = None
-        g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
-        self.F.load_params(g, blocks)
+        inp = device_inputs(cfg)
+        self.F.params.copy_(inp["params"])
         if cfg.has_embed_head:
-            tok = synth.make_tokens(cfg, seed=1)
-            self.tok = torch.from_numpy(tok).cuda()
+            self.tok = inp["tok"]
         else:
-            x1, gout = synth.make_stack_inputs(cfg, seed=2)
-            self.x1 = torch.from_numpy(x1).cuda()
-            self.dy = torch.from_numpy(gout).cuda()
+            self.x1 = inp["x1"]
+            self.dy = inp["dy"]
             self.dx = torch.empty_like(self.x1)
         if optimizer:
             self.F.init_optimizer()
@@ -225,27 +266,37 @@ def measured_peaks():
     return {"mfma_bf16_tflops": flops / (ms / 1e3) / 1e12, "hbm_copy_gbs": 2.0 * n * 4 / (cms / 1e3) / 1e9}
 
 
-def cpu_baseline(cfg, sample_batch):
-    """Time the fp64 oracle on `sample_batch` sequences of the same config."""
-    import numpy as np
+def cpu_baseline(cfg):
+    """Time the fp64 oracle on a bounded sample of the workload: one training
+    step of one sequence through the full-width model (full vocabulary) with
+    one block and with two blocks.  The full-depth step time of one sequence
+    is extrapolated linearly in the block count, t1 + (L - 1) (t2 - t1), and
+    reported as tokens/s."""
     import threadpoolctl
 
     import oracle
     from paper_2510_14614_amd import synth
-    sc = cfg.replace(batch=sample_batch, dtype=0)
-    g, blocks = synth.make_params(cfg, seed=0, mode="throughput")
     threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    t0 = time.perf_counter()
-    if sc.has_embed_head:
-        tok = synth.make_tokens(sc, seed=1)
-        oracle.train_step(sc, g, blocks, tok)
-    else:
-        x1, gout = synth.make_stack_inputs(sc, seed=2)
-        oracle.stack_step(sc, blocks, x1, gout)
-    sec = time.perf_counter() - t0
-    return {"value": sc.tokens / sec, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one fwd+bwd step of the same model at batch {sample_batch} "
-                      f"({sc.tokens} tokens), numpy float64, {sec:.1f} s",
+    times = []
+    for nl in (1, 2):
+        sc = cfg.replace(batch=1, dtype=0, n_layer=nl)
+        g, blocks = synth.make_params(sc, seed=0, mode="throughput")
+        if sc.has_embed_head:
+            tok = synth.make_tokens(sc, seed=1)
+            t0 = time.perf_counter()
+            oracle.train_step(sc, g, blocks, tok)
+        else:
+            x1, gout = synth.make_stack_inputs(sc, seed=2)
+            t0 = time.perf_counter()
+            oracle.stack_step(sc, blocks, x1, gout)
+        times.append(time.perf_counter() - t0)
+    t1, t2 = times
+    per_block = max(t2 - t1, 0.0)
+    est = t1 + (cfg.n_layer - 1) * per_block
+    return {"value": cfg.seq_len / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one fwd+bwd step of one sequence ({cfg.seq_len} tokens), numpy float64, full width "
+                      f"and vocabulary, with 1 block ({t1:.1f} s) and 2 blocks ({t2:.1f} s); the "
+                      f"{cfg.n_layer}-block step extrapolated linearly in the block count: {est:.1f} s",
             "host_cpus": os.cpu_count()}
 
 
@@ -257,11 +308,12 @@ def sources_hash():
     return h.hexdigest()
 
 
-def measured_traffic():
-    """Bytes per GEMM call from the committed counter summary, or None when
-    it is missing or was taken on different kernel sources."""
+def measured_traffic(config, arch):
+    """Bytes per GEMM call from the committed counter summary of this config
+    and architecture, or None when it is missing or was taken on different
+    kernel sources."""
     try:
-        lines = open(TRAFFIC_FILE).read().splitlines()
+        lines = open(traffic_file(config, arch)).read().splitlines()
     except OSError:
         return None
     kv = {}
@@ -277,10 +329,10 @@ def measured_traffic():
         return None
 
 
-def summarize_stats(stats_csv, out_md, cmds):
+def summarize_stats(stats_csv, out_md, cmds, label):
     rows = list(csv.DictReader(open(stats_csv)))
     tot = sum(float(r["TotalDurationNs"]) for r in rows)
-    lines = ["# Kernel time, gpt2-small FAL training step (serialized launches)", "",
+    lines = [f"# Kernel time, {label} training step (serialized launches)", "",
              "Command (repository root on the GPU host, `TMPDIR=/tmp`):", ""]
     lines += ["```", *cmds, "```", "",
               f"All dispatches of the run; total GPU kernel time {tot / 1e6:.2f} ms.", "",
@@ -304,7 +356,7 @@ def summarize_stats(stats_csv, out_md, cmds):
     print("\n".join(lines[-3:]))
 
 
-def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
+def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds, label):
     probe_bytes = int(probe_mib) * (1 << 20)
 
     def load(path, counter):
@@ -321,7 +373,7 @@ def summarize_traffic(fetch_csv, write_csv, probe_mib, out_md, cmds):
     assert n == len(gw) and n > 0
     fetch = (sum(gf) + sum(rf)) * cf / n
     write = (sum(gw) + sum(rw)) * cw / n
-    lines = ["# HBM traffic of the bf16 GEMM kernels, gpt2-small FAL training step", "",
+    lines = [f"# HBM traffic of the bf16 GEMM kernels, {label} training step", "",
              "Commands (repository root on the GPU host, `TMPDIR=/tmp`), one counter per run:", "",
              "```", *cmds, "```", "",
              "Each run ends with a plain elementwise copy (`--copy-probe`) that reads and writes a known number",
@@ -440,10 +492,10 @@ def summarize_hbm(fetch_csv, write_csv, probe_mib, out_md, cmds):
 def main():
     args = parse()
     if args.summarize_stats:
-        summarize_stats(*args.summarize_stats, args.cmd)
+        summarize_stats(*args.summarize_stats, args.cmd, args.label)
         return
     if args.summarize_traffic:
-        summarize_traffic(*args.summarize_traffic, args.cmd)
+        summarize_traffic(*args.summarize_traffic, args.cmd, args.label)
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma, args.cmd)
@@ -513,12 +565,13 @@ def main():
         "mfu": flops_step / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS,
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm_bf16_pipe / gemm_bf16_mfma (all bf16 GEMM launches of the step)",
+            "kernel": "gemm_bf16_dbl / gemm_bf16_pipe (all bf16 GEMM launches of the step, with the split-K "
+                      "reduces they launch)",
             "achieved": gemm_tflops,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": gemm_tflops / PEAK_BF16_TFLOPS,
-            "traffic": measured_traffic() if args.config == "gpt2-small" and args.arch == "fal" else None,
+            "traffic": measured_traffic(args.config, args.arch),
             "traffic_unit": "HBM bytes per GEMM call (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_ms": gemm_avg_ms,
             "avg_launch_gflop": g["flops"] / max(g["launches"], 1) / 1e9,
@@ -581,7 +634,7 @@ def main():
         out["forward_only"] = fo
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)
+        out["cpu_baseline"] = cpu_baseline(cfg)
 
     if args.copy_probe > 0:
         out["copy_probe_bytes"] = copy_probe(args.copy_probe)
