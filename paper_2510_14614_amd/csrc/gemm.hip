@@ -231,46 +231,102 @@ __device__ __forceinline__ void wave_lds_order() {
 
 // Epilogue through a wavefront-private LDS strip.  One 16-row strip of the
 // wavefront tile at a time is written from the accumulators and read back
-// with consecutive lanes on consecutive columns, so every
-// global access (output, residual, pre-activation) covers whole row segments
-// of the wavefront tile (128 B of bf16 for a 64-column tile).
-// TR = 1: the accumulators are transposed blocks (the MFMA ran as B^T A^T):
-// lane 16g+c of block (i, j) holds row 16i + c, columns 16j + 4g .. +3,
-// written to the strip as one 16-byte store.
-template <int EPI, int F32OUT, int FM, int FN, int TR = 0>
+// with consecutive lanes on consecutive columns, so every global access
+// (output, residual, GELU derivative) covers whole row segments of the
+// wavefront tile (256 B of bf16 for a 128-column tile).  The accumulators
+// are transposed blocks (the MFMA ran as B^T A^T): lane 16g+c of block
+// (i, j) holds row 16i + c, columns 16j + 4g .. +3, written to the strip as
+// one 16-byte store.
+//
+// A wavefront tile that lies wholly inside the output takes the fast path
+// (plain stores, residual add, GELU-derivative product): each strip's
+// read-back passes are issued together, and the rows an epilogue reads (the
+// residual, the GELU derivative) for strip i + 1 are loaded while strip i
+// is computed and stored, so their memory latency is paid about once per
+// tile instead of once per pass.  Edge tiles and the GELU epilogue take the
+// per-pass path with bounds checks.
+template <int EPI, int F32OUT, int FM, int FN>
 __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t (&acc)[FM][FN], float* stage,
                                              int mw, int nw, int lane, int gelu_tanh) {
   constexpr int WTN = FN * 16, PITCH = WTN + 4;
   constexpr int LPR = WTN / 4, RPI = 64 / LPR;    // lanes per row, rows per access
-  constexpr int NPASS = (16 + RPI - 1) / RPI;     // accesses per 16-row strip
-  const int rr = lane / LPR, cc = (lane % LPR) * 4;  // read-back position (rr >= RPI: idle)
+  constexpr int NPASS = 16 / RPI;                 // accesses per 16-row strip
+  static_assert(RPI * LPR == 64 && NPASS * RPI == 16, "strip shape");
+  const int rr = lane / LPR, cc = (lane % LPR) * 4;  // read-back position
   const int n = nw + cc;
   const bool full = P.vec_out && n + 4 <= P.N;
   float bn[4];
   bias4(P, n, full, bn);
+  auto write_strip = [&](int i) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    // straight from the MFMA layout: lane 16g+c holds rows 4g..4g+3 of
-    // column c (with the 4-float pad, 64 different banks per store)
-    if (TR) {
+    for (int j = 0; j < FN; ++j)
+      *reinterpret_cast<float4*>(stage + (lane & 15) * PITCH + 16 * j + 4 * (lane >> 4)) =
+          make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+  };
+  // GELU tiles keep the per-pass path: there the batched passes measured
+  // slower (the GELU arithmetic, not memory latency, sets the pace)
+  const bool inside = EPI != EPI_GELU && P.vec_out && mw + 16 * FM <= P.M && nw + WTN <= P.N;
+  if (inside) {
+    // operand rows the epilogue reads, one strip ahead
+    constexpr int NA = EPI == EPI_MUL_AUX ? NPASS : 1;
+    constexpr int NR = EPI == EPI_RESID ? NPASS : 1;
+    uint2 aux[2][NA];
+    float4 res[2][NR];
+    auto prefetch = [&](int i, int buf) {
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        *reinterpret_cast<float4*>(stage + (lane & 15) * PITCH + 16 * j + 4 * (lane >> 4)) =
-            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-    } else {
+      for (int k = 0; k < NPASS; ++k) {
+        const int64_t m = mw + 16 * i + k * RPI + rr;
+        if (EPI == EPI_MUL_AUX)
+          aux[buf][k] = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(P.aux) + m * P.ldaux + n);
+        if (EPI == EPI_RESID) res[buf][k] = *reinterpret_cast<const float4*>(P.resid + m * P.ldr + n);
+      }
+    };
+    if (EPI == EPI_MUL_AUX || EPI == EPI_RESID) prefetch(0, 0);
+    // fully unrolled whatever the body size: a rolled loop would index the
+    // accumulators dynamically and move them to scratch
+#pragma clang loop unroll(full)
+    for (int i = 0; i < FM; ++i) {
+      const int cur = i & 1;
+      write_strip(i);
+      wave_lds_order();
+      float4 t[NPASS];
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int k = 0; k < NPASS; ++k) t[k] = *reinterpret_cast<const float4*>(stage + (k * RPI + rr) * PITCH + cc);
+      wave_lds_order();
+      if ((EPI == EPI_MUL_AUX || EPI == EPI_RESID) && i + 1 < FM) prefetch(i + 1, cur ^ 1);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) stage[((lane >> 4) * 4 + r) * PITCH + 16 * j + (lane & 15)] = acc[i][j][r];
+      for (int k = 0; k < NPASS; ++k) {
+        const int64_t m = mw + 16 * i + k * RPI + rr;
+        const int64_t o = m * P.ldo + n;
+        float v[4] = {t[k].x + bn[0], t[k].y + bn[1], t[k].z + bn[2], t[k].w + bn[3]};
+        if (EPI == EPI_STORE) {
+          if (F32OUT) *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) = make_float4(v[0], v[1], v[2], v[3]);
+          else st4(static_cast<bf16*>(P.out) + o, v);
+        } else if (EPI == EPI_RESID) {
+          const float4 r = res[cur][k];
+          *reinterpret_cast<float4*>(static_cast<float*>(P.out) + o) =
+              make_float4(r.x + v[0], r.y + v[1], r.z + v[2], r.w + v[3]);
+        } else {
+          const uint2 w = aux[cur][k];
+          const float a[4] = {__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
+                              __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u)};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] *= a[c];
+          st4(static_cast<bf16*>(P.out) + o, v);
+        }
+      }
     }
+    return;
+  }
+#pragma clang loop unroll(full)
+  for (int i = 0; i < FM; ++i) {
+    write_strip(i);
     wave_lds_order();
-    // kept rolled: unrolling it multiplies the epilogue code (one copy per
-    // output kind) several-fold, and the once-per-tile epilogue then runs
-    // out of the instruction cache
+    // kept rolled: the edge path runs on few tiles, and unrolling it
+    // multiplies its code (one copy per output kind)
 #pragma unroll 1
     for (int k = 0; k < NPASS; ++k) {
       const int r = k * RPI + rr;
-      if (rr >= RPI || r >= 16) continue;
       const float4 t = *reinterpret_cast<const float4*>(stage + r * PITCH + cc);
       const int m = mw + 16 * i + r;
       if (m < P.M && n < P.N) {
@@ -281,8 +337,6 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
     wave_lds_order();
   }
 }
-
-
 
 #ifndef FAL_GEMM_DBL
 #define FAL_GEMM_DBL 1
@@ -684,17 +738,17 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
     Q.ldo = P.N;
     Q.bias = Q.bias2 = nullptr;
     Q.vec_out = (P.N & 3) == 0;
-    store_staged<EPI_STORE, 1, FM, FN, 1>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
     return;
   }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
-      else store_staged<EPI_STORE, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
       break;
-    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
@@ -871,17 +925,17 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dbl(GemmGroup g, int gelu_
     Q.ldo = P.N;
     Q.bias = Q.bias2 = nullptr;
     Q.vec_out = (P.N & 3) == 0;
-    store_staged<EPI_STORE, 1, FM, FN, 1>(Q, acc, stage, mw, nw, lane, gelu_tanh);
+    store_staged<EPI_STORE, 1, FM, FN>(Q, acc, stage, mw, nw, lane, gelu_tanh);
     return;
   }
   switch (P.epi) {
     case EPI_STORE:
-      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
-      else store_staged<EPI_STORE, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      if (P.out_f32) store_staged<EPI_STORE, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
+      else store_staged<EPI_STORE, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh);
       break;
-    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
-    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN, 1>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_GELU: store_staged<EPI_GELU, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_RESID: store_staged<EPI_RESID, 1, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
+    case EPI_MUL_AUX: store_staged<EPI_MUL_AUX, 0, FM, FN>(P, acc, stage, mw, nw, lane, gelu_tanh); break;
   }
 }
 
