@@ -338,6 +338,21 @@ __device__ __forceinline__ void store_staged(const GemmProblem& P, const f32x4_t
   }
 }
 
+#ifndef FAL_NS11
+#define FAL_NS11 4
+#endif
+#ifndef FAL_NS10
+#define FAL_NS10 4
+#endif
+#ifndef FAL_NS01
+#define FAL_NS01 4
+#endif
+#ifndef FAL_NS00
+#define FAL_NS00 5
+#endif
+#ifndef FAL_LATE_B
+#define FAL_LATE_B 1
+#endif
 #ifndef FAL_GEMM_DBL
 #define FAL_GEMM_DBL 1
 #endif
@@ -643,6 +658,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   bf16x8_t ra[2][FM], rb[2][FN];
 
+  // B's fragments of the next slice: all at the start of a step (two slices
+  // live at once), or each right after its last use in the step's final row
+  constexpr bool LATE_B = FAL_LATE_B;
   auto read = [&](const char* stage, int buf) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) ra[buf][i] = fa.read(stage, i);
@@ -655,13 +673,17 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
   // A's current fragment i, so the two can share registers.
   auto step = [&](const char* stage, int cur) {
     const int nxt = cur ^ 1;
+    if (!LATE_B) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j) rb[nxt][j] = fb.read(stage + SA::BYTES, j);
+      for (int j = 0; j < FN; ++j) rb[nxt][j] = fb.read(stage + SA::BYTES, j);
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rb[cur][j], ra[cur][i], acc[i][j], 0, 0, 0);
+        if (LATE_B && i == FM - 1) rb[nxt][j] = fb.read(stage + SA::BYTES, j);
+      }
       ra[nxt][i] = fa.read(stage, i);
     }
   };
@@ -673,12 +695,20 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
   constexpr int NMF = FM * FN;
   constexpr int DMA_EVERY = NMF / L > 0 ? NMF / L : 1;
   static_assert(NRB <= NMF, "more B reads than MFMAs");
+  constexpr int RBJ = NRB / FN;           // LDS read instructions per B fragment
   auto interleave = [&]() {
     int dma = 0;
 #pragma unroll
     for (int q = 0; q < NMF; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      if (q < NRB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (B)
+      if (LATE_B) {
+        if (q >= NMF - FN) {
+#pragma unroll
+          for (int r = 0; r < RBJ; ++r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (B)
+        }
+      } else if (q < NRB) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (B)
+      }
       if ((q + 1) % FN == 0) {
 #pragma unroll
         for (int r = 0; r < RA; ++r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read (A)
@@ -689,10 +719,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe(GemmGroup g, int gelu
       }
     }
   };
-  // The last A reads of a step may still be in flight at the next step's
-  // barrier; reads of the slice before (whose stage is refilled after the
-  // barrier) are older and complete.
-  constexpr int LGK = FM * RA < 15 ? FM * RA : 15;
+  // The reads issued by a step (the last A reads, and with LATE_B all of
+  // B's) may still be in flight at the next step's barrier; reads of the
+  // slice before (whose stage is refilled after the barrier) are older and
+  // complete.  The counter field holds at most 15.
+  constexpr int LGK_N = FM * RA + (LATE_B ? NRB : 0);
+  constexpr int LGK = LGK_N < 15 ? LGK_N : 15;
 
   if (n > 0) {
     // prologue: slices sbeg .. sbeg+NS-2 into stages 0..NS-2; slice sbeg's fragments
@@ -1178,7 +1210,15 @@ hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, h
       }
     } else {
       switch (shape) {
-        case PIPE_256x256: FAL_PIPE_LAUNCH(256, 256, 1, 4) break;
+        case PIPE_256x256:
+          // stage count per orientation: the ones with which the register
+          // allocator keeps every accumulator in place across the unrolled
+          // main loop (no accumulator copies between iterations)
+          if (a_kmaj && b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 1, 256, 256, 1, FAL_NS11>), grid, block, 0, s, g, gelu_tanh);
+          else if (a_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<1, 0, 256, 256, 1, FAL_NS10>), grid, block, 0, s, g, gelu_tanh);
+          else if (b_kmaj) hipLaunchKernelGGL((gemm_bf16_pipe<0, 1, 256, 256, 1, FAL_NS01>), grid, block, 0, s, g, gelu_tanh);
+          else hipLaunchKernelGGL((gemm_bf16_pipe<0, 0, 256, 256, 1, FAL_NS00>), grid, block, 0, s, g, gelu_tanh);
+          break;
         case PIPE_256x128: FAL_PIPE_LAUNCH(256, 128, 1, 4) break;
         case PIPE_128x256: FAL_PIPE_LAUNCH(128, 256, 1, 4) break;
         default: FAL_PIPE_LAUNCH(128, 128, 2, 4) break;
