@@ -725,10 +725,12 @@ struct Run {
     const void* da_lp = W.dxm_lp;
     const float* da = W.dxm;
     if (arch == FAL_ARCH_FALPLUS && layer == 0 && D.L > 1) {
-      // dA_1 = dXm + backward of norm(A_1) applied to the accumulated dxhatF
-      FAL_TRY(copy_f32(W.da, W.dxm, Md, sm));
-      FAL_TRY(norm_bwd(W.a1, W.meanF, W.rstdF, dfirst, D.M, D.d, W.da, 1, sm));
-      FAL_TRY(cast_from_f32(dt, W.da, W.da_lp, Md, sm));
+      // dA_1 = dXm + backward of norm(A_1) applied to the accumulated
+      // dxhatF, with its dtype copy, in one pass
+      {
+        Span span(ctx, FAL_PROF_NORM, sm, 0.0, (16.0 + (double)ctx->D.es) * Md);
+        FAL_TRY(norm_bwd(dt, W.a1, W.meanF, W.rstdF, dfirst, D.M, D.d, W.dxm, W.da, W.da_lp, sm));
+      }
       da_lp = W.da_lp;
       da = W.da;
     }

@@ -137,10 +137,12 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s);
 int64_t ln_bwd_scratch(int M, int d);
 
 // Backward of the affine-free normalisation xhat = (a - mean) * rstd given
-// dxhat (fp32): da (+)= rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat*xhat))
-// with xhat recomputed from a (fp32).  accumulate=0 overwrites da.
-hipError_t norm_bwd(const float* a, const float* mean, const float* rstd, const float* dxhat,
-                    int M, int d, float* da, int accumulate, hipStream_t s);
+// dxhat (fp32), added to a residual gradient in one pass:
+//   da = dres + rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat*xhat))
+// with xhat recomputed from a (fp32); dres may be NULL (zero) or alias da;
+// da_lp (dtype copy of da) is written if non-NULL.
+hipError_t norm_bwd(DType dt, const float* a, const float* mean, const float* rstd, const float* dxhat,
+                    int M, int d, const float* dres, float* da, void* da_lp, hipStream_t s);
 
 // Sum `nblk` partial rows of width d: out[j] = sum_b part[b * stride + j].
 hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float* out, hipStream_t s);

@@ -235,10 +235,10 @@ hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float*
   return hipGetLastError();
 }
 
-template <int VPT>
+template <typename S, int VPT>
 __global__ __launch_bounds__(256) void norm_bwd_kernel(const float* A, const float* mean,
                                                        const float* rstd, const float* dxhat, int M,
-                                                       int d, float* da, int accumulate) {
+                                                       int d, const float* dres, float* da, S* lp) {
   const int row = blockIdx.x * kRowsPerBlock + threadIdx.x / FAL_WAVE;
   const int lane = threadIdx.x % FAL_WAVE;
   if (row >= M) return;
@@ -264,8 +264,10 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float* A, const flo
   for (int i = 0; i < VPT; ++i) {
     const int j = lane + FAL_WAVE * i;
     if (j >= d) break;
-    const float v = rs * (g[i] - s1 - xh[i] * s2);
-    da[off + j] = accumulate ? da[off + j] + v : v;
+    float v = rs * (g[i] - s1 - xh[i] * s2);
+    if (dres) v += dres[off + j];
+    da[off + j] = v;
+    if (lp) lp[off + j] = from_f<S>(v);
   }
 }
 
@@ -404,9 +406,10 @@ __global__ __launch_bounds__(256) void ln_bwd_v4(LnBwdArgs a) {
   }
 }
 
-template <int NC>
+template <typename S, int NC>
 __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* mean, const float* rstd,
-                                                  const float* dxhat, int M, int d, float* da, int accumulate) {
+                                                  const float* dxhat, int M, int d, const float* dres, float* da,
+                                                  S* lp) {
   const int row = blockIdx.x * kRowsPerBlock + threadIdx.x / FAL_WAVE;
   const int lane = threadIdx.x % FAL_WAVE;
   if (row >= M) return;
@@ -432,8 +435,10 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
   for (int i = 0; i < NC; ++i) {
     const int j = 4 * (lane + FAL_WAVE * i);
     if (j >= d) break;
-    const float4 v = f4(rs) * (g[i] - f4(s1) - xh[i] * f4(s2));
-    st4(da + off + j, accumulate ? ld4(da + off + j) + v : v);
+    float4 v = f4(rs) * (g[i] - f4(s1) - xh[i] * f4(s2));
+    if (dres) v = v + ld4(dres + off + j);
+    st4(da + off + j, v);
+    if (lp) st4s<S>(lp + off + j, v);
   }
 }
 
@@ -526,20 +531,25 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t norm_bwd(const float* A, const float* mean, const float* rstd, const float* dxhat, int M,
-                    int d, float* da, int accumulate, hipStream_t s) {
+hipError_t norm_bwd(DType dt, const float* A, const float* mean, const float* rstd, const float* dxhat, int M,
+                    int d, const float* dres, float* da, void* da_lp, hipStream_t s) {
   const dim3 grid(cdiv(M, kRowsPerBlock)), block(256);
-  if (vec_ok(F32, d, {A, dxhat, da}, {}))
-    return dispatch_nc(d, [&](auto nc) {
-      constexpr int C = decltype(nc)::value;
-      hipLaunchKernelGGL((norm_bwd_v4<C>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, da, accumulate);
+  auto run = [&](auto tag) {
+    using S = decltype(tag);
+    S* lp = static_cast<S*>(da_lp);
+    if (vec_ok(dt, d, {A, dxhat, dres, da}, {da_lp}))
+      return dispatch_nc(d, [&](auto nc) {
+        constexpr int C = decltype(nc)::value;
+        hipLaunchKernelGGL((norm_bwd_v4<S, C>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, dres, da, lp);
+        return hipGetLastError();
+      });
+    return dispatch_vpt(d, [&](auto vpt) {
+      constexpr int V = decltype(vpt)::value;
+      hipLaunchKernelGGL((norm_bwd_kernel<S, V>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, dres, da, lp);
       return hipGetLastError();
     });
-  return dispatch_vpt(d, [&](auto vpt) {
-    constexpr int V = decltype(vpt)::value;
-    hipLaunchKernelGGL((norm_bwd_kernel<V>), grid, block, 0, s, A, mean, rstd, dxhat, M, d, da, accumulate);
-    return hipGetLastError();
-  });
+  };
+  return dt == BF16 ? run(bf16{}) : run(float{});
 }
 
 // ------------------------------------------------------------- col_sum --
