@@ -493,10 +493,25 @@ struct Run {
         gemm1(1, 0, p, sm);
         return;
       }
+      // Two streams: when the QKV GEMM leaves compute units idle in its
+      // last round, the MLP branch forks off before it and the FFN-up GEMM
+      // fills them; when the QKV GEMM fills whole rounds, the FFN-up GEMM
+      // goes after it and overlaps the attention kernel (whose causal tail
+      // leaves compute units idle) instead of splitting the CUs with it.
       hipStream_t s2 = sm;
+      const GemmProblem pq = qkv_prob(S, bp);
+      bool fc_first = true;
+      if (streams()) {
+        GemmGroup gq;
+        memset(&gq, 0, sizeof(gq));
+        gq.p[0] = pq;
+        gq.n = 1;
+        fc_first = gemm_last_round_fill(dt, 1, 0, gq, 0) < 0.9;
+      }
+      if (!fc_first) gemm1(1, 0, pq, sm);
       if (streams()) { fork(); s2 = ctx->sa; }
       gemm1(1, 0, fc_prob(S, bp), s2);
-      gemm1(1, 0, qkv_prob(S, bp), sm);
+      if (fc_first) gemm1(1, 0, pq, sm);
       attention_fwd(S, sm);
       if (merged_out()) {
         if (streams()) join();

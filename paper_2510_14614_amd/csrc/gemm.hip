@@ -1106,6 +1106,22 @@ static bool pipe_ok(const GemmGroup& g, int a_kmaj, int b_kmaj) {
   return true;
 }
 
+double gemm_last_round_fill(DType dt, int a_kmaj, int b_kmaj, const GemmGroup& g, int64_t splitk_floats) {
+  if (dt != BF16 || g.n < 1 || g.n > kMaxGroup || !pipe_ok(g, a_kmaj, b_kmaj)) return 1.0;
+  const GemmProblem& P0 = g.p[0];
+  const bool splittable = splitk_floats > 0 && g.n == 1 && P0.K2 == 0 && P0.epi == EPI_STORE && P0.out_f32;
+  int shape, sp;
+  choose_pipe(g, splittable, splitk_floats, shape, sp);
+  const PipeShape& t = kPipe[shape];
+  int kmax = 0;
+  for (int i = 0; i < g.n; ++i) kmax = std::max(kmax, g.p[i].K + g.p[i].K2);
+  const bool occ3 = shape == PIPE_128x128 && a_kmaj && !b_kmaj && sp == 1 && kmax <= FAL_OCC3_KMAX;
+  const int64_t slots = (int64_t)(occ3 ? 3 : t.per_cu) * kCUs;
+  const int64_t tiles = count_tiles_shape(g, t.bm, t.bn) * sp;
+  const int64_t rem = tiles % slots;
+  return rem == 0 ? 1.0 : (double)rem / (double)slots;
+}
+
 hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
                 const char** why, float* splitk_scratch, int64_t splitk_floats) {
   *why = nullptr;

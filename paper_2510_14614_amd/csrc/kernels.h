@@ -72,6 +72,11 @@ struct GemmGroup {
 // receives a static message for argument errors.
 hipError_t gemm(DType dt, int a_kmaj, int b_kmaj, GemmGroup& g, int gelu_tanh, hipStream_t s,
                 const char** why, float* splitk_scratch = nullptr, int64_t splitk_floats = 0);
+// The share of the chip's workgroup slots the launch of `g` would occupy
+// in its last round (1.0 when its tiles fill whole rounds; 1.0 as well for
+// launches off the matrix-core path).  Lets a scheduler tell whether
+// another launch can use compute units this one leaves idle.
+double gemm_last_round_fill(DType dt, int a_kmaj, int b_kmaj, const GemmGroup& g, int64_t splitk_floats);
 
 // ----------------------------------------------------------- LayerNorm ----
 // Row LayerNorm over d of fp32 rows x.  Writes
