@@ -464,9 +464,16 @@ struct Run {
 
   // The block's weights were last read a whole step (or half of one) ago
   // and have left the caches; streaming them in first lets the block's
-  // GEMMs find them in the last-level cache.
+  // GEMMs find them in the last-level cache.  That pays where the GEMMs are
+  // short against their weights' first-touch latency: measured gains with
+  // 14 MiB of bf16 weights per block at 8192 tokens and with 75 MiB at
+  // 4096; a wash at 24 MiB / 8192; losses of 0.5-0.8 ms per step at
+  // 24 MiB / 16384 and 96 MiB / 8192, where the serial read costs more
+  // than it saves.
   void warm_params(const void* bp, hipStream_t s) {
-    FAL_TRY(cache_warm(bp, ctx->Lo.block_stride * (int64_t)ctx->D.es, s));
+    const int64_t bytes = ctx->Lo.block_stride * (int64_t)ctx->D.es;
+    if (bytes > (16ll << 20) && ctx->D.M > 4096) return;
+    FAL_TRY(cache_warm(bp, bytes, s));
   }
 
   void block_fwd(int layer, const void* bp, const float* x, float* y, void* first) {
