@@ -12,6 +12,7 @@
 //  * col_sum_batch: bias gradients, up to four matrices per pair of launches.
 // All of these are HBM-bound; rows are read with 64 consecutive elements
 // per wavefront instruction.
+#include <algorithm>
 #include <initializer_list>
 
 #include "common.h"
@@ -442,6 +443,87 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
   }
 }
 
+// LayerNorm backward in one pass for widths that are a multiple of 1024 (up
+// to 4096): a workgroup walks `rows` consecutive rows with all 256 threads
+// on one row (NCH 4-element chunks each), combines the four wavefronts' row
+// sums through LDS in a fixed order (one barrier per row, double-buffered),
+// and keeps the parameter-gradient sums of its rows in registers, written
+// once as partial rows [blk][6][d] for col_reduce_multi.  This replaces the
+// separate partial-sum pass and its second read of X, dY1 and dY2.
+template <typename S, int NCH>
+__global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
+  __shared__ float red[2][4][2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d;
+  const S* g1 = static_cast<const S*>(a.g1);
+  const S* g2 = static_cast<const S*>(a.g2);
+  const S* gF = static_cast<const S*>(a.gF);
+  const S* xF = static_cast<const S*>(a.xhatF);
+  S* lp = static_cast<S*>(a.dx_lp);
+  float4 q[5][NCH];
+#pragma unroll
+  for (int k = 0; k < 5; ++k)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) q[k][c] = f4(0.f);
+  const int r0 = blockIdx.x * rows, r1 = min(a.M, r0 + rows);
+  for (int r = r0; r < r1; ++r) {
+    const int64_t off = (int64_t)r * d;
+    const float mean = a.mean[r], rstd = a.rstd[r];
+    float4 xh[NCH], t[NCH];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int j = 4 * (tid + 256 * c);
+      xh[c] = (ld4(a.x + off + j) - f4(mean)) * f4(rstd);
+      float4 tt = f4(0.f);
+      if (a.dy1) {
+        const float4 v = ld4(a.dy1 + off + j);
+        tt = tt + v * ld4s<S>(g1 + j);
+        q[0][c] = q[0][c] + v * xh[c];
+        q[1][c] = q[1][c] + v;
+      }
+      if (a.dy2) {
+        const float4 v = ld4(a.dy2 + off + j);
+        tt = tt + v * ld4s<S>(g2 + j);
+        q[2][c] = q[2][c] + v * xh[c];
+        q[3][c] = q[3][c] + v;
+        if (xF) q[4][c] = q[4][c] + v * ld4s<S>(xF + off + j);
+        if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? v : ld4(a.dacc + off + j) + v);
+        if (a.dxhatF_acc) {
+          const float4 w = ld4s<S>(gF + j) * v;
+          st4(a.dxhatF_acc + off + j, a.dxhatF_overwrite ? w : ld4(a.dxhatF_acc + off + j) + w);
+        }
+      }
+      t[c] = tt;
+      s1 += hsum(tt);
+      s2 += hsum(tt * xh[c]);
+    }
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
+    const int b = (r - r0) & 1;
+    if (lane == 0) {
+      red[b][wave][0] = s1;
+      red[b][wave][1] = s2;
+    }
+    __syncthreads();
+    s1 = (((red[b][0][0] + red[b][1][0]) + red[b][2][0]) + red[b][3][0]) / d;
+    s2 = (((red[b][0][1] + red[b][1][1]) + red[b][2][1]) + red[b][3][1]) / d;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int j = 4 * (tid + 256 * c);
+      float4 dx = f4(rstd) * (t[c] - f4(s1) - xh[c] * f4(s2));
+      if (a.dres) dx = dx + ld4(a.dres + off + j);
+      st4(a.dx + off + j, dx);
+      if (lp) st4s<S>(lp + off + j, dx);
+    }
+  }
+  float* p = a.partials + (int64_t)blockIdx.x * 6 * d;
+#pragma unroll
+  for (int k = 0; k < 5; ++k)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) st4(p + (int64_t)k * d + 4 * (tid + 256 * c), q[k][c]);
+}
+
 // Chunks of 4 per lane for width d (a multiple of 4), 0 if too wide.
 template <typename F>
 static hipError_t dispatch_nc(int d, F&& f) {
@@ -494,11 +576,51 @@ hipError_t ln_fwd(DType dt, const LnFwdArgs& a, hipStream_t s) {
   });
 }
 
-int64_t ln_bwd_scratch(int M, int d) { return (int64_t)cdiv(M, kPartRows) * 6 * d; }
+// Rows per workgroup of the fused pass: as many workgroups as fit on the
+// chip at once (256 CUs times the workgroups per CU the kernel's registers
+// allow: 4, 4, 3, 2 for d = 1024 .. 4096), so that every CU walks rows with
+// several workgroups from the start, and no more, since each workgroup
+// writes 5 d partial sums.  Measured against 8 and 16 fixed rows at
+// (M, d) = (8192, 2048), (4096, 4096) and (16384, 1024).
+static int fused_rows(int M, int d) {
+  static const int per_cu[4] = {4, 4, 3, 2};
+  const int nch = std::min(4, std::max(1, d / 1024));
+  return std::max(1, cdiv(M, 256 * per_cu[nch - 1]));
+}
+
+int64_t ln_bwd_scratch(int M, int d) {
+  return (int64_t)std::max(cdiv(M, kPartRows), cdiv(M, fused_rows(M, d))) * 6 * d;
+}
 
 hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   const dim3 grid(cdiv(a.M, kRowsPerBlock)), block(256);
   hipError_t e;
+  const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
+  if (any && a.d % 1024 == 0 && a.d <= 4096 && a.partials &&
+      vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc, a.partials},
+             {a.g1, a.g2, a.gF, a.dx_lp, a.xhatF})) {
+    const int rows = fused_rows(a.M, a.d);
+    const int nblk = cdiv(a.M, rows);
+    auto launch = [&](auto nc) {
+      constexpr int C = decltype(nc)::value;
+      if (dt == BF16) hipLaunchKernelGGL((ln_bwd_fused<bf16, C>), dim3(nblk), block, 0, s, a, rows);
+      else hipLaunchKernelGGL((ln_bwd_fused<float, C>), dim3(nblk), block, 0, s, a, rows);
+    };
+    switch (a.d / 1024) {
+      case 1: launch(std::integral_constant<int, 1>{}); break;
+      case 2: launch(std::integral_constant<int, 2>{}); break;
+      case 3: launch(std::integral_constant<int, 3>{}); break;
+      default: launch(std::integral_constant<int, 4>{}); break;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    ColReduceArgs r{};
+    r.part = a.partials; r.nblk = nblk; r.stride = (int64_t)6 * a.d; r.d = a.d;
+    float* outs[6] = {a.dg1, a.db1, a.dg2, a.db2, a.dgF, a.dbF};
+    const int src[6] = {0, 1, 2, 3, 4, 3};  // dbF == db2 == sum dy2
+    for (int k = 0; k < 6; ++k) { r.out[k] = outs[k]; r.src[k] = src[k]; }
+    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(256), 0, s, r);
+    return hipGetLastError();
+  }
   if (vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc}, {a.g1, a.g2, a.gF, a.dx_lp}))
     e = dispatch_nc(a.d, [&](auto nc) {
       constexpr int C = decltype(nc)::value;
@@ -514,7 +636,6 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
       return hipGetLastError();
     });
   if (e != hipSuccess) return e;
-  const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
   if (!any) return hipSuccess;
   if (a.d % 4) return hipErrorInvalidValue;
   const int nblk = cdiv(a.M, kPartRows);
