@@ -170,7 +170,10 @@ fal_status_t fal_workspace_bytes(const fal_config_t* cfg, size_t* bytes);
  * buffer of at least fal_workspace_bytes bytes, 256-byte aligned, owned by
  * the caller and kept alive until fal_destroy.  stream_main / stream_aux:
  * hipStream_t handles (NULL means the default stream; aux may equal main).
- * *out receives the context. */
+ * The context also creates one stream of its own (default priority): when
+ * aux differs from main, the bias-gradient sums of a block run there beside
+ * the next block's backward; every call joins it back into the main stream
+ * before it returns.  *out receives the context. */
 fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
                       void* stream_main, void* stream_aux, fal_ctx_t** out);
 

@@ -187,6 +187,7 @@ struct Work {
   float* dfirst;               // [M, d]
   float *dxa, *dxb, *dxm, *da, *dh1, *dh2;
   void *lp_a, *lp_b, *dxm_lp, *da_lp, *dog, *dqkv;
+  void *dog2[2], *dqkv2[2];  // per block parity: the pending bias sums of block i read block i's
   float* Dvec;
   float *part_main, *part_aux;
   float* bias_part;  // packed column-sum partials of one block's bias gradients
@@ -248,8 +249,12 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.lp_b = cv.take<char>(M * d * es);
   W.dxm_lp = cv.take<char>(M * d * es);
   W.da_lp = cv.take<char>(M * d * es);
-  W.dog = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
-  W.dqkv = cv.take<char>(M * D.dqkv * es);
+  for (int k = 0; k < 2; ++k) {
+    W.dog2[k] = cv.take<char>(M * (int64_t)(D.dA + D.f) * es);
+    W.dqkv2[k] = cv.take<char>(M * D.dqkv * es);
+  }
+  W.dog = W.dog2[0];
+  W.dqkv = W.dqkv2[0];
   W.Dvec = cv.take<float>((int64_t)D.B * D.H * D.T);
   const int64_t part = std::max<int64_t>({ln_bwd_scratch((int)M, (int)d), dot_scratch(M * d)});
   W.part_main = cv.take<float>(part);
@@ -284,6 +289,10 @@ struct fal_ctx {
   size_t ws_bytes;
   hipStream_t sm, sa;
   hipEvent_t ev_fork, ev_join, ev_keys;
+  // library stream for a block's bias-gradient sums, which run beside the
+  // next block's backward; forked from and joined back to the main stream
+  hipStream_t sb = nullptr;
+  hipEvent_t ev_bfork = nullptr, ev_bdone = nullptr;
   int device;
   std::string err;
   // kernel timing (fal_profile_enable)
@@ -432,6 +441,10 @@ struct Run {
     FAL_TRY(ln_fwd(dt, a, s));
   }
   void lnbwd(const LnBwdArgs& a, hipStream_t s) {
+    // every buffer the previous block's pending bias sums read that is not
+    // double-buffered (its output gradient, dXm / dA) is first written by a
+    // LayerNorm backward of this block
+    bias_join();
     const double row = 8.0 + 4.0 * (!!a.dy1 + !!a.dy2 + !!a.dres) + 8.0 * (!!a.dacc + !!a.dxhatF_acc) +
                        (double)ctx->D.es * (!!a.dx_lp + !!a.xhatF);
     Span span(ctx, FAL_PROF_NORM, s, 0.0, row * a.M * a.d);
@@ -605,15 +618,45 @@ struct Run {
       ColSumInput& in = bias.in[k];
       if (in.x == x && in.ld == ld && in.N == N && !in.out2) { in.out2 = out; return; }
     }
-    if (bias.n == kColSumMax) flush_bias(ctx->sm);
+    if (bias.n == kColSumMax) {
+      bias_join();  // the partial-sum scratch is shared with the library stream
+      flush_bias(ctx->sm);
+    }
     bias.in[bias.n++] = ColSumInput{x, ld, N, in_f32 || dt == F32 ? 1 : 0, out, nullptr};
+  }
+  // The block's queued bias sums on the library stream (contexts given two
+  // streams), after everything the main stream has issued so far (the
+  // block is joined by then); they run beside the next block's backward.
+  // Only sums over at least 128 MiB of gradients go there: same-box A/B,
+  // per step, of 108-110 MiB per block (GPT-2 small, 7B shard) 0.16-0.3 ms
+  // slower, of 144-287 MiB (GPT-2 medium, MLM-48, 1.3B) 0.1-2.0 ms faster.
+  bool bias_pending = false;
+  double bias_bytes() const {
+    double bytes = 0.0;
+    for (int k = 0; k < bias.n; ++k) bytes += (double)ctx->D.M * bias.in[k].N * (bias.in[k].f32 ? 4.0 : (double)ctx->D.es);
+    return bytes;
+  }
+  void flush_bias_async() {
+    if (bias.n == 0) return;
+    if (ctx->sa == ctx->sm || bias_bytes() < 128.0 * (1 << 20)) {  // one-stream contexts stay on one stream
+      flush_bias(ctx->sm);
+      return;
+    }
+    FAL_TRY(hipEventRecord(ctx->ev_bfork, ctx->sm));
+    FAL_TRY(hipStreamWaitEvent(ctx->sb, ctx->ev_bfork, 0));
+    flush_bias(ctx->sb);
+    FAL_TRY(hipEventRecord(ctx->ev_bdone, ctx->sb));
+    bias_pending = true;
+  }
+  void bias_join() {
+    if (!bias_pending) return;
+    FAL_TRY(hipStreamWaitEvent(ctx->sm, ctx->ev_bdone, 0));
+    bias_pending = false;
   }
   void flush_bias(hipStream_t s) {
     if (bias.n == 0) return;
     bias.M = ctx->D.M;
-    double bytes = 0.0;
-    for (int k = 0; k < bias.n; ++k) bytes += (double)ctx->D.M * bias.in[k].N * (bias.in[k].f32 ? 4.0 : (double)ctx->D.es);
-    Span span(ctx, FAL_PROF_BIAS, s, 0.0, bytes);
+    Span span(ctx, FAL_PROF_BIAS, s, 0.0, bias_bytes());
     FAL_TRY(col_sum_batch(dt, bias, ctx->W.bias_part, s));
     bias = ColSumBatch{};
   }
@@ -673,8 +716,11 @@ struct Run {
   // A_1, whose product with dH2 gives the block's LN_{F,i} gain gradient).
   void block_bwd(int layer, const void* bp, const float* x, const void* first, const float* dy,
                  const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
+    ctx->W.dog = ctx->W.dog2[layer & 1];
+    ctx->W.dqkv = ctx->W.dqkv2[layer & 1];
     block_bwd_parts(layer, bp, x, first, dy, dy_lp, dx, dx_lp, dfirst, gb);
-    flush_bias(ctx->sm);  // after the join: the aux stream's gradients are complete
+    // after the join: the aux stream's gradients are complete
+    flush_bias_async();
   }
   void block_bwd_parts(int layer, const void* bp, const float* x, const void* first, const float* dy,
                        const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
@@ -855,7 +901,10 @@ fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
   if (hipGetDevice(&ctx->device) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_keys, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&ctx->ev_keys, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_bfork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_bdone, hipEventDisableTiming) != hipSuccess ||
+      hipStreamCreateWithFlags(&ctx->sb, hipStreamNonBlocking) != hipSuccess) {
     delete[] ctx->W.slots;
     delete ctx;
     return FAL_ERR_HIP;
@@ -870,6 +919,9 @@ fal_status_t fal_destroy(fal_ctx_t* ctx) {
   (void)hipEventDestroy(ctx->ev_fork);
   (void)hipEventDestroy(ctx->ev_join);
   (void)hipEventDestroy(ctx->ev_keys);
+  if (ctx->ev_bfork) (void)hipEventDestroy(ctx->ev_bfork);
+  if (ctx->ev_bdone) (void)hipEventDestroy(ctx->ev_bdone);
+  if (ctx->sb) (void)hipStreamDestroy(ctx->sb);
   delete[] ctx->W.slots;
   delete ctx;
   return FAL_OK;
@@ -928,6 +980,7 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
     FAL_TRY(cast_from_f32(r.dt, dx_out, ctx->W.lp_a, Md, ctx->sm));
     r.block_bwd(layer, block_params, x_in, first_attn, dx_out, ctx->W.lp_a, dx_in, ctx->W.lp_b, d_first_attn,
                 block_grads);
+    r.bias_join();
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }
@@ -1001,6 +1054,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       std::swap(cur, nxt);
       std::swap(cur_lp, nxt_lp);
     }
+    r.bias_join();
     {
       // dX read twice (position sums, scatter), touched wte-gradient rows read and written
       Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * 16.0);
@@ -1112,6 +1166,7 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
       cur = out;
       k ^= 1;
     }
+    r.bias_join();
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }
