@@ -1026,13 +1026,16 @@ static const char* check_vec_operand(const void* X, int64_t ld, int kmaj, int ro
 // 64 bytes).  Launch time model, fitted to measurements on MI355X
 // (GPT-2-sized problems, 8192^3): a k-slice of one tile costs t1 us when
 // the tile has its CU alone and t2 us when per_cu tiles share it; each
-// round of tiles adds ovh us (prologue, epilogue, launch ramp).
+// round of tiles adds ovh us (prologue, epilogue, launch ramp).  The
+// 128 x 128 t1 comes from a lone round of weight-gradient tiles at the 1.3B
+// shape (2048 x 2048 x 8192: 0.39 us per slice; with 0.30 the model kept
+// that GEMM unsplit, 99.9 us, against 70.4 us split in two).
 struct PipeShape { int bm, bn, per_cu; double t1, t2, ovh; };
 enum { PIPE_256x256 = 0, PIPE_256x128 = 1, PIPE_128x256 = 2, PIPE_128x128 = 3, kPipeShapes = 4 };
 constexpr PipeShape kPipe[kPipeShapes] = {{256, 256, 1, 0.85, 0.85, 10.0},
                                           {256, 128, 1, 0.56, 0.56, 5.0},
                                           {128, 256, 1, 0.56, 0.56, 5.0},
-                                          {128, 128, 2, 0.30, 0.54, 3.0}};
+                                          {128, 128, 2, 0.39, 0.54, 3.0}};
 constexpr int kPipeKS = 32;
 constexpr double kHbmBytesPerUs = 5.0e6;       // sustained HBM rate for operand re-reads
 constexpr double kPartialBytesPerUs = 8.0e6;   // split-K partials (written and re-read while cached)
