@@ -191,7 +191,7 @@ struct Work {
   float* Dvec;
   float *part_main, *part_aux;
   float* bias_part;  // packed column-sum partials of one block's bias gradients
-  float *splitk_main, *splitk_aux;  // split-K partials, one region per stream
+  float *splitk_main, *splitk_aux, *splitk_side;  // split-K partials, one region per stream
   int64_t splitk_floats;
   int32_t* keys;
   float* loss_tmp;
@@ -265,6 +265,7 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.splitk_floats = (int64_t)1024 * 128 * 128;
   W.splitk_main = cv.take<float>(W.splitk_floats);
   W.splitk_aux = cv.take<float>(W.splitk_floats);
+  W.splitk_side = cv.take<float>(W.splitk_floats);
   W.loss_tmp = cv.take<float>(64);
   W.opt_part = cv.take<double>(kNormBlocks);
   W.opt_ctrl = cv.take<float>(16);
@@ -292,7 +293,7 @@ struct fal_ctx {
   // library stream for a block's bias-gradient sums, which run beside the
   // next block's backward; forked from and joined back to the main stream
   hipStream_t sb = nullptr;
-  hipEvent_t ev_bfork = nullptr, ev_bdone = nullptr;
+  hipEvent_t ev_bfork = nullptr, ev_bdone = nullptr, ev_hdone = nullptr;
   int device;
   std::string err;
   // kernel timing (fal_profile_enable)
@@ -366,9 +367,11 @@ struct Run {
                (double)q.M * q.N * ((q.out_f32 || q.epi == EPI_RESID) ? 4.0 : (double)ctx->D.es);
     }
     Span span(ctx, FAL_PROF_GEMM, s, flops, bytes);
+    // split-K scratch: one region per stream, so that a launch makes the
+    // same choice (and sums in the same order) on any of them
     const bool aux = s == ctx->sa && ctx->sa != ctx->sm;
-    hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why, aux ? ctx->W.splitk_aux : ctx->W.splitk_main,
-                             ctx->W.splitk_floats);
+    float* sk = s == ctx->sb ? ctx->W.splitk_side : aux ? ctx->W.splitk_aux : ctx->W.splitk_main;
+    hipError_t e = fal::gemm(dt, ak, bk, g, tanh, s, &why, sk, ctx->W.splitk_floats);
     if (e != hipSuccess) {
       ctx->err = std::string("gemm: ") + (why ? why : hipGetErrorString(e));
       throw Fail{};
@@ -904,6 +907,7 @@ fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
       hipEventCreateWithFlags(&ctx->ev_keys, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->ev_bfork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->ev_bdone, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_hdone, hipEventDisableTiming) != hipSuccess ||
       hipStreamCreateWithFlags(&ctx->sb, hipStreamNonBlocking) != hipSuccess) {
     delete[] ctx->W.slots;
     delete ctx;
@@ -921,6 +925,7 @@ fal_status_t fal_destroy(fal_ctx_t* ctx) {
   (void)hipEventDestroy(ctx->ev_keys);
   if (ctx->ev_bfork) (void)hipEventDestroy(ctx->ev_bfork);
   if (ctx->ev_bdone) (void)hipEventDestroy(ctx->ev_bdone);
+  if (ctx->ev_hdone) (void)hipEventDestroy(ctx->ev_hdone);
   if (ctx->sb) (void)hipStreamDestroy(ctx->sb);
   delete[] ctx->W.slots;
   delete ctx;
@@ -1040,7 +1045,19 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
     pd.epi = EPI_STORE; pd.out_f32 = 1; pd.out = W.dh1; pd.ldo = D.d;
     pd.kpad = 1;  // dlogits columns V .. Vp-1 are written as zeros
     r.gemm1(1, 0, pd, sm);
-    r.gemm1(0, 0, r.wgrad(W.dlogits, D.Vp, W.hf, D.d, D.V, D.d, D.M, grads + Lo.goff[FAL_P_WTE]), sm);
+    // dwte = dlogits^T Hf beside the final LayerNorm and the last blocks'
+    // backward (two-stream contexts): nothing reads dwte before the
+    // embedding backward adds to it, and dlogits and Hf stay untouched
+    const GemmProblem pw = r.wgrad(W.dlogits, D.Vp, W.hf, D.d, D.V, D.d, D.M, grads + Lo.goff[FAL_P_WTE]);
+    const bool side = ctx->sa != ctx->sm;
+    if (side) {
+      FAL_TRY(hipEventRecord(ctx->ev_bfork, sm));
+      FAL_TRY(hipStreamWaitEvent(ctx->sb, ctx->ev_bfork, 0));
+      r.gemm1(0, 0, pw, ctx->sb);
+      FAL_TRY(hipEventRecord(ctx->ev_hdone, ctx->sb));
+    } else {
+      r.gemm1(0, 0, pw, sm);
+    }
     {
       LnBwdArgs a = r.lnb(xl, W.meanf, W.rstdf);
       a.dy1 = W.dh1; a.g1 = gparam(FAL_P_LNF_G); a.dx = W.dxa; a.dx_lp = W.lp_a;
@@ -1055,6 +1072,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       std::swap(cur_lp, nxt_lp);
     }
     r.bias_join();
+    if (side) FAL_TRY(hipStreamWaitEvent(sm, ctx->ev_hdone, 0));
     {
       // dX read twice (position sums, scatter), touched wte-gradient rows read and written
       Span span(ctx, FAL_PROF_EMBED, sm, 0.0, (double)D.M * D.d * 16.0);
