@@ -171,9 +171,10 @@ fal_status_t fal_workspace_bytes(const fal_config_t* cfg, size_t* bytes);
  * the caller and kept alive until fal_destroy.  stream_main / stream_aux:
  * hipStream_t handles (NULL means the default stream; aux may equal main).
  * The context also creates one stream of its own (default priority): when
- * aux differs from main, the bias-gradient sums of a block run there beside
- * the next block's backward; every call joins it back into the main stream
- * before it returns.  *out receives the context. */
+ * aux differs from main, the LM-head weight gradient and large blocks'
+ * bias-gradient sums run there beside the following backward work; every
+ * call joins it back into the main stream before it returns.  *out
+ * receives the context. */
 fal_status_t fal_init(const fal_config_t* cfg, void* workspace, size_t ws_bytes,
                       void* stream_main, void* stream_aux, fal_ctx_t** out);
 
