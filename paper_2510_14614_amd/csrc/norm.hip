@@ -5,9 +5,11 @@
 //    LayerNorms read the same X_i (H1 = LN1(X_i), H2 = LN2(X_i) + F); FAL+
 //    adds the per-block LayerNorm of the shared first-attention
 //    normalisation to its MLP input in the same pass.
-//  * ln_bwd: row kernel for the input gradient (both LayerNorms of one input
-//    at once), plus a column kernel for gamma/beta gradients with a fixed
-//    reduction order.
+//  * ln_bwd: the input gradient (both LayerNorms of one input at once) and
+//    the gamma/beta gradients: for widths that are a multiple of 1024 one
+//    pass forms both (partial sums per workgroup of rows); other widths use
+//    a row kernel plus a column partial-sum kernel.  Either way a
+//    fixed-order reduce finishes the parameter gradients.
 //  * norm_bwd: backward of the affine-free normalisation of A_1 (FAL+).
 //  * col_sum_batch: bias gradients, up to four matrices per pair of launches.
 // All of these are HBM-bound; rows are read with 64 consecutive elements
