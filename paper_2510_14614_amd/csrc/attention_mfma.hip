@@ -69,7 +69,43 @@ __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 *
 // registers: load() issues the global loads (rows past T read a clamped
 // row), store() writes LDS (zeroing rows past T).  Loading the next tile
 // before computing on the current one keeps its memory latency behind the
-// MFMA work.  Tiles are stored row-major, [row][HD + 8].
+// MFMA work.
+//
+// LDS tiles hold rows of HD contiguous elements, 16 rows to a group of
+// 16 (HD + 8) elements; inside a group, row r sits in slot m(r) at a stride
+// of HD + 8 elements.  Measured with the SQ LDS counters, a wavefront's
+// 16-byte read occupies the LDS 4 cycles and an 8-byte transposing read 2
+// when free of bank conflicts, a 16-byte write 8; for the access patterns
+// of these tiles the conflicts follow 16 consecutive lanes (32 for the
+// transposing read) per cycle over 256 bytes of banks.  A slot stride of
+// HD + 8 elements puts slot j's 16-byte chunk c at bank group
+// (j (HD/8 + 1) + c) mod 16, and the slots are permuted so that, with
+// s(r) = 8 (r & 1) + 4 ((r >> 1) & 1) + ((r >> 2) & 3) the bank group of
+// row r's chunk 0:
+//  * row reads (16 consecutive rows, one chunk each) meet 16 values of s;
+//  * transposing reads (4 consecutive rows, 4 adjacent chunks each) meet s
+//    values 4 apart, so the rows' chunk runs tile the 16 bank groups;
+//  * stores (8 lanes: 128 bytes of one row) cover distinct bank groups.
+// The counters read no conflicts in any of the kernels below; rows in order
+// at the same stride left the transposing reads four-way conflicted at
+// head_dim 128 and two-way at 64.  m(r) = s(r) at HD = 128 (stride 17
+// chunks, 17 = 1 mod 16) and 9 s(r) mod 16 at HD = 64 (stride 9,
+// 9 * 9 = 1 mod 16).
+// trow(a + b) = trow(a) + trow(b) for a a multiple of 16, and trow(r + 8) =
+// trow(r) + 2 (HD + 8) for r % 16 < 8: callers split a row into a part known
+// at compile time and a per-lane part, so every fragment offset is an
+// immediate.
+template <int HD>
+__device__ __forceinline__ int trow(int r) {
+  const int x = r & 15;
+  const int s = ((x & 1) << 3) | ((x & 2) << 1) | ((x >> 2) & 3);
+  const int m = HD == 128 ? s : (9 * s) & 15;
+  return (HD + 8) * (16 * (r >> 4) + m);
+}
+// elements of an AT-row tile
+template <int HD>
+constexpr int tile_elems() { return AT * (HD + 8); }
+
 template <int HD>
 struct RowTile {
   static constexpr int CH = HD / 8, N = (AT * CH + 255) / 256;
@@ -88,21 +124,21 @@ struct RowTile {
     for (int k = 0; k < N; ++k) {
       const int i = tid + 256 * k;
       if (i >= AT * CH) continue;
-      const int r = i / CH, c = (i % CH) * 8;
-      *reinterpret_cast<uint4*>(s + r * (HD + 8) + c) = row0 + r < T ? v[k] : make_uint4(0, 0, 0, 0);
+      const int r = i / CH, c = i % CH;
+      *reinterpret_cast<uint4*>(s + trow<HD>(r) + 8 * c) = row0 + r < T ? v[k] : make_uint4(0, 0, 0, 0);
     }
   }
 };
 
-// A or B operand fragment from a row-major LDS tile: row `row`, dims
-// 16*kk + 8*g .. +7.
+// A or B operand fragment from an LDS tile: row rowbase + r (rowbase a
+// multiple of 16), dims 16*kk + 8*g .. +7.
 template <int HD>
-__device__ __forceinline__ bf16x8v frag_rows(const bf16* s, int row, int kk, int g) {
-  return *reinterpret_cast<const bf16x8v*>(s + row * (HD + 8) + 16 * kk + 8 * g);
+__device__ __forceinline__ bf16x8v frag_rows(const bf16* s, int rowbase, int r, int kk, int g) {
+  return *reinterpret_cast<const bf16x8v*>(s + trow<HD>(rowbase) + trow<HD>(r) + 16 * kk + 8 * g);
 }
 
-// Operand fragment for a contraction over the rows of a row-major LDS tile
-// [row][HD + 8]: lane (c = lane % 32, g = lane / 32) gets column colbase + c
+// Operand fragment for a contraction over the rows of an LDS tile (rowbase
+// a multiple of 16): lane (c = lane % 32, g = lane / 32) gets column colbase + c
 // of rows rowbase + {4g..4g+3, 8+4g..8+4g+3}, the order in which the
 // accumulator registers of a 32x32 tile hold them.  ds_read_b64_tr_b16
 // hands lane i of each 16-lane group element i % 4 of the 8-byte chunks
@@ -113,12 +149,11 @@ template <int HD>
 __device__ __forceinline__ bf16x8v frag_tr(const bf16* s, int rowbase, int colbase, int lane) {
   const int L = lane & 15;
   const int col = colbase + 16 * ((lane >> 4) & 1) + 4 * (L & 3);
-  const int row = rowbase + 4 * (lane >> 5) + (L >> 2);
+  const bf16* p = s + trow<HD>(rowbase) + trow<HD>(4 * (lane >> 5) + (L >> 2)) + col;
   typedef __attribute__((address_space(3))) i16x4v lds_i16x4;
-  const lds_i16x4* p0 = reinterpret_cast<const lds_i16x4*>(
-      (__attribute__((address_space(3))) const char*)(s + row * (HD + 8) + col));
-  const lds_i16x4* p1 = reinterpret_cast<const lds_i16x4*>(
-      (__attribute__((address_space(3))) const char*)(s + (row + 8) * (HD + 8) + col));
+  const lds_i16x4* p0 = reinterpret_cast<const lds_i16x4*>((__attribute__((address_space(3))) const char*)p);
+  const lds_i16x4* p1 =
+      reinterpret_cast<const lds_i16x4*>((__attribute__((address_space(3))) const char*)(p + 2 * (HD + 8)));
   const i16x4v a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(p0));
   const i16x4v b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(p1));
   const i16x4v* pa = &a;
@@ -143,8 +178,8 @@ template <int HD, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, int H, int Hkv, bf16* O,
                                                      int64_t ldo, float* lse) {
   constexpr int KK = HD / 16, NT = HD / 32;
-  __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sK[tile_elems<HD>()];
+  __shared__ __attribute__((aligned(16))) bf16 sV[tile_elems<HD>()];
   // grid (H, B, blocks): the causal block index varies slowest, so the
   // round-robin dispatch over XCDs gives every XCD the same mix of long and
   // short blocks; the longest (latest) query blocks are dispatched first.
@@ -193,7 +228,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
       if (kb >= wave_kend) break;
       f32x16v s = zero16();
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
+      for (int kk = 0; kk < KK; ++kk) s = mfma32(frag_rows<HD>(sK, 32 * sub, c, kk, g), qf[kk], s);
       // Causal: only the sub-tile on the diagonal (kb == q0) holds keys
       // after a query or past T; every earlier one is fully visible.
       // Without the mask only the last sub-tile can hold keys past T.
@@ -262,8 +297,8 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
     bf16* dqkv) {
   constexpr bool DO_V = PART != 2, DO_K = PART != 1;
   constexpr int KK = HD / 16, NT = HD / 32;
-  __shared__ __attribute__((aligned(16))) bf16 sQ[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sdO[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sQ[tile_elems<HD>()];
+  __shared__ __attribute__((aligned(16))) bf16 sdO[tile_elems<HD>()];
   __shared__ float sL[AT], sD[AT];
   // grid (Hkv, B, blocks): causal block index slowest (even XCD mix); the
   // earliest key blocks see the most queries and are dispatched first.  A
@@ -332,8 +367,8 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
       f32x16v s = zero16(), dp = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(frag_rows<HD>(sQ, 32 * sub + c, kk, g), kf[kk], s);
-        if constexpr (DO_K) dp = mfma32(frag_rows<HD>(sdO, 32 * sub + c, kk, g), vf[kk], dp);
+        s = mfma32(frag_rows<HD>(sQ, 32 * sub, c, kk, g), kf[kk], s);
+        if constexpr (DO_K) dp = mfma32(frag_rows<HD>(sdO, 32 * sub, c, kk, g), vf[kk], dp);
       }
       // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
       // Q and dO rows and zero L and D, so they add nothing; only the
@@ -388,8 +423,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
                                                         const bf16* dO, int64_t lddo, const float* lse,
                                                         float* Dvec, int T, int H, int Hkv, bf16* dqkv) {
   constexpr int KK = HD / 16, NT = HD / 32;
-  __shared__ __attribute__((aligned(16))) bf16 sK[AT * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sV[AT * (HD + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sK[tile_elems<HD>()];
+  __shared__ __attribute__((aligned(16))) bf16 sV[tile_elems<HD>()];
   // grid (H, B, blocks): the causal block index varies slowest, so the
   // round-robin dispatch over XCDs gives every XCD the same mix of long and
   // short blocks; the longest (latest) query blocks are dispatched first.
@@ -444,8 +479,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
       f32x16v s = zero16(), dp = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(frag_rows<HD>(sK, 32 * sub + c, kk, g), qf[kk], s);
-        dp = mfma32(frag_rows<HD>(sV, 32 * sub + c, kk, g), of[kk], dp);
+        s = mfma32(frag_rows<HD>(sK, 32 * sub, c, kk, g), qf[kk], s);
+        dp = mfma32(frag_rows<HD>(sV, 32 * sub, c, kk, g), of[kk], dp);
       }
       // s[r] = S^T[key kb + acc_row(r, g)][query tq].  Keys past T have
       // zero K and V rows (dS there multiplies a zero K row); only the
