@@ -187,6 +187,8 @@ struct Work {
   float* dfirst;               // [M, d]
   float *dxa, *dxb, *dxm, *da, *dh1, *dh2;
   void *lp_a, *lp_b, *dxm_lp, *da_lp, *dog, *dqkv;
+  float* dh2b[2];  // FAL+: per block parity (the block's deferred first-attention terms read it)
+  float* fp_part;  // FAL+: partial sums of those terms
   void *dog2[2], *dqkv2[2];  // per block parity: the pending bias sums of block i read block i's
   float* Dvec;
   float *part_main, *part_aux;
@@ -245,6 +247,9 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.da = cv.take<float>(M * d);
   W.dh1 = cv.take<float>(M * d);
   W.dh2 = cv.take<float>(M * d);
+  W.dh2b[0] = W.dh2;
+  W.dh2b[1] = c.arch == FAL_ARCH_FALPLUS ? cv.take<float>(M * d) : W.dh2;
+  W.fp_part = c.arch == FAL_ARCH_FALPLUS ? cv.take<float>(falplus_side_scratch((int)M, (int)d)) : nullptr;
   W.lp_a = cv.take<char>(M * d * es);
   W.lp_b = cv.take<char>(M * d * es);
   W.dxm_lp = cv.take<char>(M * d * es);
@@ -639,15 +644,34 @@ struct Run {
     for (int k = 0; k < bias.n; ++k) bytes += (double)ctx->D.M * bias.in[k].N * (bias.in[k].f32 ? 4.0 : (double)ctx->D.es);
     return bytes;
   }
+  // A FAL+ block's first-attention terms of its LN2 backward, queued like
+  // the bias sums: they feed only the accumulator block 1 consumes and the
+  // block's own LN_F gain gradient, so in a context given two streams they
+  // run beside the next block's backward (whatever the bias sums do).
+  struct FpJob {
+    const float* dy2;
+    const void *xF, *gF;
+    float* acc;
+    int ow;
+    float* dgF;
+  } fp{};
+  bool fp_queued = false;
+  void run_fp(hipStream_t s) {
+    Span span(ctx, FAL_PROF_NORM, s, 0.0, (double)ctx->D.M * ctx->D.d * (12.0 + ctx->D.es));
+    FAL_TRY(falplus_side(dt, fp.dy2, fp.xF, fp.gF, fp.acc, fp.ow, ctx->D.M, ctx->D.d, fp.dgF, ctx->W.fp_part, s));
+    fp_queued = false;
+  }
   void flush_bias_async() {
-    if (bias.n == 0) return;
-    if (ctx->sa == ctx->sm || bias_bytes() < 128.0 * (1 << 20)) {  // one-stream contexts stay on one stream
-      flush_bias(ctx->sm);
-      return;
-    }
+    const bool two = ctx->sa != ctx->sm;  // one-stream contexts stay on one stream
+    const bool bias_side = bias.n > 0 && two && bias_bytes() >= 128.0 * (1 << 20);
+    const bool fp_side = fp_queued && two;
+    if (bias.n > 0 && !bias_side) flush_bias(ctx->sm);
+    if (fp_queued && !fp_side) run_fp(ctx->sm);
+    if (!bias_side && !fp_side) return;
     FAL_TRY(hipEventRecord(ctx->ev_bfork, ctx->sm));
     FAL_TRY(hipStreamWaitEvent(ctx->sb, ctx->ev_bfork, 0));
-    flush_bias(ctx->sb);
+    if (bias_side) flush_bias(ctx->sb);
+    if (fp_side) run_fp(ctx->sb);
     FAL_TRY(hipEventRecord(ctx->ev_bdone, ctx->sb));
     bias_pending = true;
   }
@@ -720,6 +744,7 @@ struct Run {
   void block_bwd(int layer, const void* bp, const float* x, const void* first, const float* dy,
                  const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
     ctx->W.dog = ctx->W.dog2[layer & 1];
+    ctx->W.dh2 = ctx->W.dh2b[layer & 1];
     ctx->W.dqkv = ctx->W.dqkv2[layer & 1];
     block_bwd_parts(layer, bp, x, first, dy, dy_lp, dx, dx_lp, dfirst, gb);
     // after the join: the aux stream's gradients are complete
@@ -788,9 +813,15 @@ struct Run {
     a2.dy2 = W.dh2; a2.g2 = P(bp, FAL_B_LN2_G); a2.dres = dy; a2.dx = W.dxm; a2.dx_lp = W.dxm_lp;
     a2.dg2 = G(gb, FAL_B_LN2_G); a2.db2 = G(gb, FAL_B_LN2_B);
     if (arch == FAL_ARCH_FALPLUS && layer > 0) {
-      a2.xhatF = first; a2.gF = P(bp, FAL_B_LNF1_G);
-      a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
-      a2.dgF = G(gb, FAL_B_LNF1_G); a2.dbF = G(gb, FAL_B_LNF1_B);
+      a2.dbF = G(gb, FAL_B_LNF1_B);  // = db2, from the same partial sums
+      if (W.fp_part && falplus_side_ok(dt, D.d, W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst)) {
+        fp = FpJob{W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst, last ? 1 : 0, G(gb, FAL_B_LNF1_G)};
+        fp_queued = true;
+      } else {
+        a2.xhatF = first; a2.gF = P(bp, FAL_B_LNF1_G);
+        a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
+        a2.dgF = G(gb, FAL_B_LNF1_G);
+      }
     }
     lnbwd(a2, sm);
     const void* da_lp = W.dxm_lp;

@@ -141,6 +141,17 @@ struct LnBwdArgs {
 hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s);
 int64_t ln_bwd_scratch(int M, int d);
 
+// The FAL+ terms of a block's LN2 backward as a separate pass (so they can
+// run beside the next block's backward): dxhatF_acc (+)= gF * dy2 ("=" when
+// overwrite), and dgF = sum_rows dy2 * xhatF (fixed order through
+// falplus_side_scratch floats of scratch).  dy2, dxhatF_acc: fp32 [M, d];
+// xhatF, gF: dtype.  falplus_side_ok tells whether the vector layout it
+// needs (d % 4, aligned rows) holds.
+bool falplus_side_ok(DType dt, int d, const float* dy2, const void* xhatF, const void* gF, const float* acc);
+hipError_t falplus_side(DType dt, const float* dy2, const void* xhatF, const void* gF, float* dxhatF_acc,
+                        int overwrite, int M, int d, float* dgF, float* scratch, hipStream_t s);
+int64_t falplus_side_scratch(int M, int d);
+
 // Backward of the affine-free normalisation xhat = (a - mean) * rstd given
 // dxhat (fp32), added to a residual gradient in one pass:
 //   da = dres + rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat*xhat))

@@ -590,6 +590,49 @@ static int fused_rows(int M, int d) {
   return std::max(1, cdiv(M, 256 * per_cu[nch - 1]));
 }
 
+// FAL+ side pass: each thread owns 4 columns of a block of kSideRows rows,
+// updates the accumulator rows in place and writes its column partials of
+// dy2 * xhatF; col_reduce sums the blocks in order.  No barriers.
+constexpr int kSideRows = 32;
+template <typename S>
+__global__ __launch_bounds__(256) void falplus_side_kernel(const float* dy2, const S* xF, const S* gF, float* acc,
+                                                           int ow, int M, int d, float* part) {
+  const int j = 4 * (blockIdx.x * 256 + threadIdx.x);
+  if (j >= d) return;
+  const int r0 = blockIdx.y * kSideRows, r1 = min(M, r0 + kSideRows);
+  const float4 g = ld4s<S>(gF + j);
+  float4 q = f4(0.f);
+  for (int r = r0; r < r1; ++r) {
+    const int64_t off = (int64_t)r * d + j;
+    const float4 v = ld4(dy2 + off);
+    q = q + v * ld4s<S>(xF + off);
+    const float4 w = g * v;
+    st4(acc + off, ow ? w : ld4(acc + off) + w);
+  }
+  st4(part + (int64_t)blockIdx.y * d + j, q);
+}
+
+bool falplus_side_ok(DType dt, int d, const float* dy2, const void* xhatF, const void* gF, const float* acc) {
+  return vec_ok(dt, d, {dy2, acc}, {xhatF, gF}) && dy2 && xhatF && gF && acc;
+}
+
+int64_t falplus_side_scratch(int M, int d) { return (int64_t)cdiv(M, kSideRows) * d; }
+
+hipError_t falplus_side(DType dt, const float* dy2, const void* xhatF, const void* gF, float* dxhatF_acc,
+                        int overwrite, int M, int d, float* dgF, float* scratch, hipStream_t s) {
+  if (M < 1 || !falplus_side_ok(dt, d, dy2, xhatF, gF, dxhatF_acc) || !dgF || !scratch) return hipErrorInvalidValue;
+  const dim3 grid(cdiv(d / 4, 256), cdiv(M, kSideRows));
+  if (dt == BF16)
+    hipLaunchKernelGGL((falplus_side_kernel<bf16>), grid, dim3(256), 0, s, dy2, static_cast<const bf16*>(xhatF),
+                       static_cast<const bf16*>(gF), dxhatF_acc, overwrite, M, d, scratch);
+  else
+    hipLaunchKernelGGL((falplus_side_kernel<float>), grid, dim3(256), 0, s, dy2, static_cast<const float*>(xhatF),
+                       static_cast<const float*>(gF), dxhatF_acc, overwrite, M, d, scratch);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return col_reduce(scratch, cdiv(M, kSideRows), d, d, dgF, s);
+}
+
 int64_t ln_bwd_scratch(int M, int d) {
   return (int64_t)std::max(cdiv(M, kPartRows), cdiv(M, fused_rows(M, d))) * 6 * d;
 }
