@@ -286,16 +286,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
 }
 
 // ------------------------------------------------------- backward: dK dV --
-// PART 0: dK and dV together (head_dim 64: two wavefronts per SIMD fit;
-// head_dim 128: the accumulators take the whole register file, one
-// wavefront per SIMD).  PART 1: dV only, PART 2: dK only (head_dim 128:
-// each pass fits two wavefronts per SIMD at the cost of recomputing S in
-// both; used when the grid has enough workgroups to put two on every CU).
-template <int HD, int PART, bool CAUSAL, bool GQA>
-__global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bwd_dkdv_mfma(
+// dK and dV of a key block in one pass.  head_dim 64: two wavefronts per
+// SIMD; head_dim 128: the accumulators take most of the register file, one
+// wavefront per SIMD.  (A dV pass and a dK pass, each at two wavefronts per
+// SIMD but both recomputing S, ran faster while the LDS tiles had bank
+// conflicts and slower since: 467 -> 437 us for the backward at B4 T2048
+// H16.)
+template <int HD, bool CAUSAL, bool GQA>
+__global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
     const bf16* qkv, const bf16* dO, int64_t lddo, const float* lse, const float* Dvec, int T, int H, int Hkv,
     bf16* dqkv) {
-  constexpr bool DO_V = PART != 2, DO_K = PART != 1;
   constexpr int KK = HD / 16, NT = HD / 32;
   __shared__ __attribute__((aligned(16))) bf16 sQ[tile_elems<HD>()];
   __shared__ __attribute__((aligned(16))) bf16 sdO[tile_elems<HD>()];
@@ -316,17 +316,17 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
   const int key = kw + c;          // this lane's key (column of S)
   const float sl2 = kLog2e / sqrtf((float)HD);
 
-  bf16x8v kf[KK], vf[DO_K ? KK : 1];
+  bf16x8v kf[KK], vf[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     kf[kk] = frag_global<HD>(Kg, ld, key, T, kk, g);
-    if constexpr (DO_K) vf[kk] = frag_global<HD>(Vg, ld, key, T, kk, g);
+    vf[kk] = frag_global<HD>(Vg, ld, key, T, kk, g);
   }
-  f32x16v dk[DO_K ? NT : 1], dv[DO_V ? NT : 1];
+  f32x16v dk[NT], dv[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if constexpr (DO_K) dk[t] = zero16();
-    if constexpr (DO_V) dv[t] = zero16();
+    dk[t] = zero16();
+    dv[t] = zero16();
   }
 
   // causal: only the queries at or after this block's keys see them.
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         s = mfma32(frag_rows<HD>(sQ, 32 * sub, c, kk, g), kf[kk], s);
-        if constexpr (DO_K) dp = mfma32(frag_rows<HD>(sdO, 32 * sub, c, kk, g), vf[kk], dp);
+        dp = mfma32(frag_rows<HD>(sdO, 32 * sub, c, kk, g), vf[kk], dp);
       }
       // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
       // Q and dO rows and zero L and D, so they add nothing; only the
@@ -380,9 +380,9 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
         float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -sL[qr]));
         if (diag && key > q0 + qr) p = 0.f;
         s[r] = p;
-        if constexpr (DO_K) dp[r] = p * (dp[r] - sD[qr]);
+        dp[r] = p * (dp[r] - sD[qr]);
       }
-      if constexpr (DO_V) {
+      {
         const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -390,7 +390,7 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
           dv[t] = mfma32(p1, frag_tr<HD>(sdO, 32 * sub + 16, 32 * t, lane), dv[t]);
         }
       }
-      if constexpr (DO_K) {
+      {
         const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -409,8 +409,8 @@ __global__ __launch_bounds__(256, (HD == 128 && PART == 0) ? 1 : 2) void attn_bw
       const int kr = kw + acc_row(r, g);
       if (kr < T) {
         bf16* row = dqkv + ((int64_t)b * T + kr) * ld + dA + kvh * HD + 32 * t + c;
-        if constexpr (DO_K) row[0] = static_cast<bf16>(dk[t][r] * scale);
-        if constexpr (DO_V) row[dKV] = static_cast<bf16>(dv[t][r]);
+        row[0] = static_cast<bf16>(dk[t][r] * scale);
+        row[dKV] = static_cast<bf16>(dv[t][r]);
       }
     }
 }
@@ -517,7 +517,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
 
 bool attn_mfma_supported(int hd) { return hd == 64 || hd == 128; }
 
-constexpr int kAttnCUs = 256;  // MI355X compute units
 
 template <int HD, bool CAUSAL>
 static void fwd_launch(dim3 grid, hipStream_t s, const bf16* q, int T, int H, int Hkv, bf16* o, int64_t ldo,
@@ -548,14 +547,7 @@ template <int HD, bool CAUSAL, bool GQA>
 static void dkdv_launch(dim3 gk, hipStream_t s, const bf16* q, const bf16* d, int64_t lddo, const float* lse,
                         const float* Dvec, int T, int H, int Hkv, bf16* o) {
   const dim3 block(256);
-  if constexpr (HD == 128) {
-    if ((int64_t)gk.x * gk.y * gk.z >= 2 * kAttnCUs) {
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 1, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
-      hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 2, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
-      return;
-    }
-  }
-  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, 0, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
+  hipLaunchKernelGGL((attn_bwd_dkdv_mfma<HD, CAUSAL, GQA>), gk, block, 0, s, q, d, lddo, lse, Dvec, T, H, Hkv, o);
 }
 
 template <int HD, bool CAUSAL>
@@ -568,8 +560,6 @@ static void bwd_launch(int B, int T, int H, int Hkv, hipStream_t s, const bf16* 
 }
 
 // dQ first (it also writes D = rowsum(dO * O) into Dvec), then dK / dV.
-// head_dim 128 with at least two workgroups per CU: separate dV and dK
-// passes (each fits two wavefronts per SIMD).
 hipError_t attn_bwd_mfma_launch(const void* qkv, const void* O, int64_t ldo, const void* dO, int64_t lddo,
                                 const float* lse, float* Dvec, int B, int T, int H, int Hkv, int hd, int causal,
                                 void* dqkv, hipStream_t s) {

@@ -156,9 +156,9 @@ def test_gqa_bidirectional_stack_step(hd, dtype, kv):
     compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label=f"gqa bidir hd{hd} kv{kv}")
 
 
-def test_gqa_hd128_wide_grid_split_backward():
-    # 8 key/value heads x 14 sequences x 5 blocks = 560 dK/dV workgroups:
-    # separate dV and dK passes, each summing two query heads
+def test_gqa_hd128_wide_grid_backward():
+    # 8 key/value heads x 14 sequences x 5 blocks = 560 dK/dV workgroups
+    # (more than two per CU), each summing two query heads
     cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, n_kv_head=8, d_ff=512, vocab=0, seq_len=600,
                  batch=14, arch=ARCH_GPT, dtype=1, has_embed_head=0)
     log("gqa hd128 wide grid")
@@ -169,9 +169,8 @@ def test_gqa_hd128_wide_grid_split_backward():
     compare_step(cfg, gpu_stack_step(cfg, blocks, x1, gout), ref, label="gqa hd128 wide")
 
 
-def test_bidirectional_hd128_wide_grid_split_backward():
-    # 16 heads x 7 sequences x 5 blocks = 560 workgroups: the unmasked dV and
-    # dK passes run as two kernels
+def test_bidirectional_hd128_wide_grid_backward():
+    # 16 heads x 7 sequences x 5 blocks = 560 unmasked dK/dV workgroups
     cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, d_ff=512, vocab=0, seq_len=600,
                  batch=7, arch=ARCH_FAL, dtype=1, has_embed_head=0, bidirectional=1)
     log("bidirectional hd128 wide grid")
@@ -197,10 +196,10 @@ def test_long_sequence_multi_block_attention(arch, hd):
 
 
 @pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL])
-def test_hd128_wide_grid_split_backward(arch):
-    # head_dim 128 with at least two attention workgroups per CU (16 heads x
-    # 7 sequences x 5 query blocks = 560): the dK and dV passes run as two
-    # kernels; T = 600 leaves the last query block ragged
+def test_hd128_wide_grid_backward(arch):
+    # head_dim 128 with more than two attention workgroups per CU (16 heads x
+    # 7 sequences x 5 query blocks = 560); T = 600 leaves the last query
+    # block ragged
     cfg = Config(n_layer=1, d_model=256, n_head=16, head_dim=128, d_ff=512, vocab=512, seq_len=600,
                  batch=7, arch=arch, dtype=1)
     log(f"hd128 wide grid arch={arch}")
