@@ -471,11 +471,14 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
   for (int r = r0; r < r1; ++r) {
     const int64_t off = (int64_t)r * d;
     const float mean = a.mean[r], rstd = a.rstd[r];
-    float4 xh[NCH], t[NCH];
+    float4 xh[NCH], t[NCH], res[NCH];
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int j = 4 * (tid + 256 * c);
+      // the residual gradient is read with the row's other inputs, before
+      // the barrier, so its latency overlaps the row reduction
+      res[c] = a.dres ? ld4(a.dres + off + j) : f4(0.f);
       xh[c] = (ld4(a.x + off + j) - f4(mean)) * f4(rstd);
       float4 tt = f4(0.f);
       if (a.dy1) {
@@ -514,7 +517,7 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
     for (int c = 0; c < NCH; ++c) {
       const int j = 4 * (tid + 256 * c);
       float4 dx = f4(rstd) * (t[c] - f4(s1) - xh[c] * f4(s2));
-      if (a.dres) dx = dx + ld4(a.dres + off + j);
+      if (a.dres) dx = dx + res[c];
       st4(a.dx + off + j, dx);
       if (lp) st4s<S>(lp + off + j, dx);
     }
