@@ -23,6 +23,9 @@
 namespace fal {
 
 constexpr int kRowsPerBlock = 4;  // 4 wavefronts per 256-thread workgroup
+// Output chunks of 256 features whose parameter loads ln_fwd_v4 issues as one
+// batch; 1 and 2 were measured slower at d = 2048 and 4096.
+constexpr int kFwdGroup = 4;
 
 template <typename S, int VPT>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(LnFwdArgs a) {
@@ -295,6 +298,17 @@ template <> __device__ __forceinline__ void st4s<bf16>(bf16* p, float4 v) {
   u.h[0] = from_f<bf16>(v.x); u.h[1] = from_f<bf16>(v.y); u.h[2] = from_f<bf16>(v.z); u.h[3] = from_f<bf16>(v.w);
   *reinterpret_cast<uint2*>(p) = u.w;
 }
+// Four elements held as stored (bf16: 2 registers), widened at use.
+template <typename S> struct Raw4 { float4 v; };
+template <> struct Raw4<bf16> { uint2 w; };
+template <typename S> __device__ __forceinline__ Raw4<S> raw4(const S* p);
+template <> __device__ __forceinline__ Raw4<float> raw4<float>(const float* p) { return {ld4(p)}; }
+template <> __device__ __forceinline__ Raw4<bf16> raw4<bf16>(const bf16* p) { return {*reinterpret_cast<const uint2*>(p)}; }
+__device__ __forceinline__ float4 val4(Raw4<float> r) { return r.v; }
+__device__ __forceinline__ float4 val4(Raw4<bf16> r) {
+  return make_float4(__uint_as_float(r.w.x << 16), __uint_as_float(r.w.x & 0xFFFF0000u), __uint_as_float(r.w.y << 16),
+                     __uint_as_float(r.w.y & 0xFFFF0000u));
+}
 __device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); }
 __device__ __forceinline__ float4 operator+(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 __device__ __forceinline__ float4 operator-(float4 a, float4 b) { return make_float4(a.x - b.x, a.y - b.y, a.z - b.z, a.w - b.w); }
@@ -343,19 +357,45 @@ __global__ __launch_bounds__(256) void ln_fwd_v4(LnFwdArgs a) {
   S* y1 = static_cast<S*>(a.y1);
   S* y2 = static_cast<S*>(a.y2);
   S* xo = static_cast<S*>(a.xhat_out);
+  // Outputs in groups of G chunks: every parameter and addend of a group is
+  // requested before any is used, so a group waits for one round trip.
+  constexpr int G = NC < kFwdGroup ? NC : kFwdGroup;
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int j = 4 * (lane + FAL_WAVE * i);
-    if (j >= d) break;
-    const float4 xh = (v[i] - f4(mean)) * f4(rstd);
-    if (y1) st4s<S>(y1 + off + j, xh * ld4s<S>(g1 + j) + ld4s<S>(b1 + j));
-    if (y2) {
-      float4 o = xh * ld4s<S>(g2 + j) + ld4s<S>(b2 + j);
-      if (add2) o = o + ld4s<S>(add2 + off + j);
-      if (xF) o = o + (ld4s<S>(gF + j) * ld4s<S>(xF + off + j) + ld4s<S>(bF + j));
-      st4s<S>(y2 + off + j, o);
+  for (int i0 = 0; i0 < NC; i0 += G) {
+    Raw4<S> rg1[G], rb1[G], rg2[G], rb2[G], ra2[G], rgF[G], rxF[G], rbF[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      const int j = 4 * (lane + FAL_WAVE * (i0 + k));
+      if (j >= d) break;
+      if (y1) {
+        rg1[k] = raw4<S>(g1 + j);
+        rb1[k] = raw4<S>(b1 + j);
+      }
+      if (y2) {
+        rg2[k] = raw4<S>(g2 + j);
+        rb2[k] = raw4<S>(b2 + j);
+        if (add2) ra2[k] = raw4<S>(add2 + off + j);
+        if (xF) {
+          rgF[k] = raw4<S>(gF + j);
+          rxF[k] = raw4<S>(xF + off + j);
+          rbF[k] = raw4<S>(bF + j);
+        }
+      }
     }
-    if (xo) st4s<S>(xo + off + j, xh);
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      const int j = 4 * (lane + FAL_WAVE * (i0 + k));
+      if (j >= d) break;
+      const float4 xh = (v[i0 + k] - f4(mean)) * f4(rstd);
+      if (y1) st4s<S>(y1 + off + j, xh * val4(rg1[k]) + val4(rb1[k]));
+      if (y2) {
+        float4 o = xh * val4(rg2[k]) + val4(rb2[k]);
+        if (add2) o = o + val4(ra2[k]);
+        if (xF) o = o + (val4(rgF[k]) * val4(rxF[k]) + val4(rbF[k]));
+        st4s<S>(y2 + off + j, o);
+      }
+      if (xo) st4s<S>(xo + off + j, xh);
+    }
   }
 }
 
@@ -450,54 +490,71 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
 // on one row (NCH 4-element chunks each), combines the four wavefronts' row
 // sums through LDS in a fixed order (one barrier per row, double-buffered),
 // and keeps the parameter-gradient sums of its rows in registers, written
-// once as partial rows [blk][6][d] for col_reduce_multi.  This replaces the
-// separate partial-sum pass and its second read of X, dY1 and dY2.
+// once as partial rows [blk][6][d] (rows 0..3: dg1, db1, dg2, db2) for
+// col_reduce_multi.  This replaces the separate partial-sum pass and its
+// second read of X, dY1 and dY2.  The gains are read once per workgroup and
+// every input of a row is requested before any of it is used, so a row
+// waits for one memory round trip.  (The FAL+ first-attention terms go to
+// the two-kernel path.)
 template <typename S, int NCH>
 __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
   __shared__ float red[2][4][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = a.d;
-  const S* g1 = static_cast<const S*>(a.g1);
-  const S* g2 = static_cast<const S*>(a.g2);
-  const S* gF = static_cast<const S*>(a.gF);
-  const S* xF = static_cast<const S*>(a.xhatF);
   S* lp = static_cast<S*>(a.dx_lp);
-  float4 q[5][NCH];
+  Raw4<S> gv1[NCH], gv2[NCH];
 #pragma unroll
-  for (int k = 0; k < 5; ++k)
+  for (int c = 0; c < NCH; ++c) {
+    const int j = 4 * (tid + 256 * c);
+    if (a.dy1) gv1[c] = raw4<S>(static_cast<const S*>(a.g1) + j);
+    if (a.dy2) gv2[c] = raw4<S>(static_cast<const S*>(a.g2) + j);
+  }
+  float4 q[4][NCH];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) q[k][c] = f4(0.f);
   const int r0 = blockIdx.x * rows, r1 = min(a.M, r0 + rows);
   for (int r = r0; r < r1; ++r) {
     const int64_t off = (int64_t)r * d;
     const float mean = a.mean[r], rstd = a.rstd[r];
-    float4 xh[NCH], t[NCH], res[NCH];
+    float4 xh[NCH], t[NCH], res[NCH], v1[NCH], v2[NCH], vacc[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) xh[c] = ld4(a.x + off + 4 * (tid + 256 * c));
+    if (a.dy1) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) v1[c] = ld4(a.dy1 + off + 4 * (tid + 256 * c));
+    }
+    if (a.dy2) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) v2[c] = ld4(a.dy2 + off + 4 * (tid + 256 * c));
+    }
+    if (a.dres) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) res[c] = ld4(a.dres + off + 4 * (tid + 256 * c));
+    }
+    if (a.dacc && !a.dacc_overwrite) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) vacc[c] = ld4(a.dacc + off + 4 * (tid + 256 * c));
+    }
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int j = 4 * (tid + 256 * c);
-      // the residual gradient is read with the row's other inputs, before
-      // the barrier, so its latency overlaps the row reduction
-      res[c] = a.dres ? ld4(a.dres + off + j) : f4(0.f);
-      xh[c] = (ld4(a.x + off + j) - f4(mean)) * f4(rstd);
+      xh[c] = (xh[c] - f4(mean)) * f4(rstd);
       float4 tt = f4(0.f);
       if (a.dy1) {
-        const float4 v = ld4(a.dy1 + off + j);
-        tt = tt + v * ld4s<S>(g1 + j);
+        const float4 v = v1[c];
+        tt = tt + v * val4(gv1[c]);
         q[0][c] = q[0][c] + v * xh[c];
         q[1][c] = q[1][c] + v;
       }
       if (a.dy2) {
-        const float4 v = ld4(a.dy2 + off + j);
-        tt = tt + v * ld4s<S>(g2 + j);
+        const float4 v = v2[c];
+        tt = tt + v * val4(gv2[c]);
         q[2][c] = q[2][c] + v * xh[c];
         q[3][c] = q[3][c] + v;
-        if (xF) q[4][c] = q[4][c] + v * ld4s<S>(xF + off + j);
-        if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? v : ld4(a.dacc + off + j) + v);
-        if (a.dxhatF_acc) {
-          const float4 w = ld4s<S>(gF + j) * v;
-          st4(a.dxhatF_acc + off + j, a.dxhatF_overwrite ? w : ld4(a.dxhatF_acc + off + j) + w);
-        }
+        if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? v : vacc[c] + v);
       }
       t[c] = tt;
       s1 += hsum(tt);
@@ -524,7 +581,7 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
   }
   float* p = a.partials + (int64_t)blockIdx.x * 6 * d;
 #pragma unroll
-  for (int k = 0; k < 5; ++k)
+  for (int k = 0; k < 4; ++k)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) st4(p + (int64_t)k * d + 4 * (tid + 256 * c), q[k][c]);
 }
@@ -583,12 +640,12 @@ hipError_t ln_fwd(DType dt, const LnFwdArgs& a, hipStream_t s) {
 
 // Rows per workgroup of the fused pass: as many workgroups as fit on the
 // chip at once (256 CUs times the workgroups per CU the kernel's registers
-// allow: 4, 4, 3, 2 for d = 1024 .. 4096), so that every CU walks rows with
+// allow: 4, 4, 2, 2 for d = 1024 .. 4096), so that every CU walks rows with
 // several workgroups from the start, and no more, since each workgroup
-// writes 5 d partial sums.  Measured against 8 and 16 fixed rows at
+// writes 4 d partial sums.  Measured against 8 and 16 fixed rows at
 // (M, d) = (8192, 2048), (4096, 4096) and (16384, 1024).
 static int fused_rows(int M, int d) {
-  static const int per_cu[4] = {4, 4, 3, 2};
+  static const int per_cu[4] = {4, 4, 2, 2};
   const int nch = std::min(4, std::max(1, d / 1024));
   return std::max(1, cdiv(M, 256 * per_cu[nch - 1]));
 }
@@ -644,7 +701,7 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   const dim3 grid(cdiv(a.M, kRowsPerBlock)), block(256);
   hipError_t e;
   const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
-  if (any && a.d % 1024 == 0 && a.d <= 4096 && a.partials &&
+  if (any && a.d % 1024 == 0 && a.d <= 4096 && a.partials && !a.xhatF && !a.dxhatF_acc && !a.dgF &&
       vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc, a.partials},
              {a.g1, a.g2, a.gF, a.dx_lp, a.xhatF})) {
     const int rows = fused_rows(a.M, a.d);
@@ -664,7 +721,7 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
     ColReduceArgs r{};
     r.part = a.partials; r.nblk = nblk; r.stride = (int64_t)6 * a.d; r.d = a.d;
     float* outs[6] = {a.dg1, a.db1, a.dg2, a.db2, a.dgF, a.dbF};
-    const int src[6] = {0, 1, 2, 3, 4, 3};  // dbF == db2 == sum dy2
+    const int src[6] = {0, 1, 2, 3, 3, 3};  // dbF == db2 == sum dy2 (dgF is NULL here)
     for (int k = 0; k < 6; ++k) { r.out[k] = outs[k]; r.src[k] = src[k]; }
     hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(256), 0, s, r);
     return hipGetLastError();
