@@ -187,7 +187,10 @@ struct Work {
   float* dfirst;               // [M, d]
   float *dxa, *dxb, *dxm, *da, *dh1, *dh2;
   void *lp_a, *lp_b, *dxm_lp, *da_lp, *dog, *dqkv;
-  float* dh2b[2];  // FAL+: per block parity (the block's deferred first-attention terms read it)
+  // FAL+: a ring of kSideGroup + 1 dH2 buffers indexed by layer, so a
+  // group's deferred first-attention terms read its blocks' dH2 while the
+  // next blocks write theirs
+  float* dh2r[kSideGroup + 1];
   float* fp_part;  // FAL+: partial sums of those terms
   void *dog2[2], *dqkv2[2];  // per block parity: the pending bias sums of block i read block i's
   float* Dvec;
@@ -247,8 +250,8 @@ void carve(const fal_config_t& c, char* base, Work& W, size_t* total) {
   W.da = cv.take<float>(M * d);
   W.dh1 = cv.take<float>(M * d);
   W.dh2 = cv.take<float>(M * d);
-  W.dh2b[0] = W.dh2;
-  W.dh2b[1] = c.arch == FAL_ARCH_FALPLUS ? cv.take<float>(M * d) : W.dh2;
+  W.dh2r[0] = W.dh2;
+  for (int k = 1; k <= kSideGroup; ++k) W.dh2r[k] = c.arch == FAL_ARCH_FALPLUS ? cv.take<float>(M * d) : W.dh2;
   W.fp_part = c.arch == FAL_ARCH_FALPLUS ? cv.take<float>(falplus_side_scratch((int)M, (int)d)) : nullptr;
   W.lp_a = cv.take<char>(M * d * es);
   W.lp_b = cv.take<char>(M * d * es);
@@ -644,25 +647,43 @@ struct Run {
     for (int k = 0; k < bias.n; ++k) bytes += (double)ctx->D.M * bias.in[k].N * (bias.in[k].f32 ? 4.0 : (double)ctx->D.es);
     return bytes;
   }
-  // A FAL+ block's first-attention terms of its LN2 backward, queued like
-  // the bias sums: they feed only the accumulator block 1 consumes and the
-  // block's own LN_F gain gradient, so in a context given two streams they
-  // run beside the next block's backward (whatever the bias sums do).
+  // FAL+ blocks' first-attention terms of their LN2 backward, gathered over
+  // up to kSideGroup consecutive blocks and queued like the bias sums: they
+  // feed only the accumulator block 1 consumes and each block's own LN_F
+  // gain gradient, so in a context given two streams a full group runs
+  // beside the next block's backward (whatever the bias sums do).  A block
+  // keeps its dH2 in ring slot layer % (kSideGroup + 1), which the next
+  // kSideGroup blocks do not write.
   struct FpJob {
-    const float* dy2;
-    const void *xF, *gF;
+    FalPlusSide g;
+    const void* xF;
     float* acc;
     int ow;
-    float* dgF;
   } fp{};
-  bool fp_queued = false;
+  bool fp_ready = false;  // the group is complete (full, or block 1's)
   void run_fp(hipStream_t s) {
-    Span span(ctx, FAL_PROF_NORM, s, 0.0, (double)ctx->D.M * ctx->D.d * (12.0 + ctx->D.es));
-    FAL_TRY(falplus_side(dt, fp.dy2, fp.xF, fp.gF, fp.acc, fp.ow, ctx->D.M, ctx->D.d, fp.dgF, ctx->W.fp_part, s));
-    fp_queued = false;
+    const double es = ctx->D.es;
+    const double bytes = (double)ctx->D.M * ctx->D.d * (4.0 * fp.g.n + es * (1 + fp.g.n) + (fp.ow ? 4.0 : 8.0));
+    Span span(ctx, FAL_PROF_NORM, s, 0.0, bytes);
+    FAL_TRY(falplus_side(dt, fp.g, fp.xF, fp.acc, fp.ow, ctx->D.M, ctx->D.d, ctx->W.fp_part, s));
+    fp = FpJob{};
+    fp_ready = false;
+  }
+  void queue_fp(const float* dy2, const void* xF, const void* gF, float* acc, int ow, float* dgF, bool close) {
+    if (fp.g.n > 0 && (xF != fp.xF || acc != fp.acc || ow)) run_fp(ctx->sm);  // not one group
+    if (fp.g.n == 0) { fp.xF = xF; fp.acc = acc; fp.ow = ow; }
+    fp.g.dy2[fp.g.n] = dy2; fp.g.gF[fp.g.n] = gF; fp.g.dgF[fp.g.n] = dgF;
+    ++fp.g.n;
+    fp_ready = close || fp.g.n == kSideGroup;
+  }
+  // the end of an entry point: a group still open runs on the main stream
+  void finish() {
+    if (fp.g.n > 0) run_fp(ctx->sm);
+    bias_join();
   }
   void flush_bias_async() {
     const bool two = ctx->sa != ctx->sm;  // one-stream contexts stay on one stream
+    const bool fp_queued = fp_ready;
     const bool bias_side = bias.n > 0 && two && bias_bytes() >= 128.0 * (1 << 20);
     const bool fp_side = fp_queued && two;
     if (bias.n > 0 && !bias_side) flush_bias(ctx->sm);
@@ -744,7 +765,7 @@ struct Run {
   void block_bwd(int layer, const void* bp, const float* x, const void* first, const float* dy,
                  const void* dy_lp, float* dx, void* dx_lp, float* dfirst, float* gb) {
     ctx->W.dog = ctx->W.dog2[layer & 1];
-    ctx->W.dh2 = ctx->W.dh2b[layer & 1];
+    ctx->W.dh2 = ctx->W.dh2r[layer % (kSideGroup + 1)];
     ctx->W.dqkv = ctx->W.dqkv2[layer & 1];
     block_bwd_parts(layer, bp, x, first, dy, dy_lp, dx, dx_lp, dfirst, gb);
     // after the join: the aux stream's gradients are complete
@@ -815,9 +836,9 @@ struct Run {
     if (arch == FAL_ARCH_FALPLUS && layer > 0) {
       a2.dbF = G(gb, FAL_B_LNF1_B);  // = db2, from the same partial sums
       if (W.fp_part && falplus_side_ok(dt, D.d, W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst)) {
-        fp = FpJob{W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst, last ? 1 : 0, G(gb, FAL_B_LNF1_G)};
-        fp_queued = true;
+        queue_fp(W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst, last ? 1 : 0, G(gb, FAL_B_LNF1_G), layer == 1);
       } else {
+        if (fp.g.n > 0) run_fp(sm);  // keep the accumulator's order of terms
         a2.xhatF = first; a2.gF = P(bp, FAL_B_LNF1_G);
         a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
         a2.dgF = G(gb, FAL_B_LNF1_G);
@@ -1016,7 +1037,7 @@ fal_status_t fal_block_bwd(fal_ctx_t* ctx, int32_t layer, const void* block_para
     FAL_TRY(cast_from_f32(r.dt, dx_out, ctx->W.lp_a, Md, ctx->sm));
     r.block_bwd(layer, block_params, x_in, first_attn, dx_out, ctx->W.lp_a, dx_in, ctx->W.lp_b, d_first_attn,
                 block_grads);
-    r.bias_join();
+    r.finish();
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }
@@ -1102,7 +1123,7 @@ fal_status_t fal_model_step(fal_ctx_t* ctx, const void* params, const int32_t* t
       std::swap(cur, nxt);
       std::swap(cur_lp, nxt_lp);
     }
-    r.bias_join();
+    r.finish();
     if (side) FAL_TRY(hipStreamWaitEvent(sm, ctx->ev_hdone, 0));
     {
       // dX read twice (position sums, scatter), touched wte-gradient rows read and written
@@ -1215,7 +1236,7 @@ fal_status_t fal_stack_step(fal_ctx_t* ctx, const void* params, const float* x_i
       cur = out;
       k ^= 1;
     }
-    r.bias_join();
+    r.finish();
   } catch (Fail&) {
     return FAL_ERR_HIP;
   }

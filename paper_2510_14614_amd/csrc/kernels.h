@@ -141,15 +141,26 @@ struct LnBwdArgs {
 hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s);
 int64_t ln_bwd_scratch(int M, int d);
 
-// The FAL+ terms of a block's LN2 backward as a separate pass (so they can
-// run beside the next block's backward): dxhatF_acc (+)= gF * dy2 ("=" when
-// overwrite), and dgF = sum_rows dy2 * xhatF (fixed order through
-// falplus_side_scratch floats of scratch).  dy2, dxhatF_acc: fp32 [M, d];
-// xhatF, gF: dtype.  falplus_side_ok tells whether the vector layout it
-// needs (d % 4, aligned rows) holds.
+// The FAL+ terms of the LN2 backward of up to kSideGroup consecutive
+// blocks as one separate pass (so they can run beside the next blocks'
+// backward, and the shared accumulator and xhatF are read once per group):
+// dxhatF_acc (+)= gF[0] * dy2[0] + gF[1] * dy2[1] + ... added in that order
+// ("=" when overwrite), and dgF[k] = sum_rows dy2[k] * xhatF (fixed order
+// through falplus_side_scratch floats of scratch).  dy2[k], dxhatF_acc:
+// fp32 [M, d]; xhatF, gF[k]: dtype.  falplus_side_ok tells whether one
+// block's operands have the vector layout the pass needs (d % 4, aligned
+// rows).
+// (Groups of 8 measured no faster than 4 at GPT-2 small to ~1.3B shapes.)
+constexpr int kSideGroup = 4;
+struct FalPlusSide {
+  int n;  // blocks in the group, 1 .. kSideGroup
+  const float* dy2[kSideGroup];
+  const void* gF[kSideGroup];
+  float* dgF[kSideGroup];
+};
 bool falplus_side_ok(DType dt, int d, const float* dy2, const void* xhatF, const void* gF, const float* acc);
-hipError_t falplus_side(DType dt, const float* dy2, const void* xhatF, const void* gF, float* dxhatF_acc,
-                        int overwrite, int M, int d, float* dgF, float* scratch, hipStream_t s);
+hipError_t falplus_side(DType dt, const FalPlusSide& g, const void* xhatF, float* dxhatF_acc, int overwrite, int M,
+                        int d, float* scratch, hipStream_t s);
 int64_t falplus_side_scratch(int M, int d);
 
 // Backward of the affine-free normalisation xhat = (a - mean) * rstd given

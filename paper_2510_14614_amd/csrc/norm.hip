@@ -650,47 +650,98 @@ static int fused_rows(int M, int d) {
   return std::max(1, cdiv(M, 256 * per_cu[nch - 1]));
 }
 
-// FAL+ side pass: each thread owns 4 columns of a block of kSideRows rows,
-// updates the accumulator rows in place and writes its column partials of
-// dy2 * xhatF; col_reduce sums the blocks in order.  No barriers.
+// FAL+ side pass over a group of N blocks: each thread owns 4 columns of a
+// block of kSideRows rows, reads the row's xhatF and accumulator once and
+// every block's dy2, updates the accumulator in place (block order) and
+// writes its column partials of dy2[k] * xhatF as [blk][N][d];
+// col_reduce_multi sums the blocks in order.  No barriers.
 constexpr int kSideRows = 32;
-template <typename S>
-__global__ __launch_bounds__(256) void falplus_side_kernel(const float* dy2, const S* xF, const S* gF, float* acc,
-                                                           int ow, int M, int d, float* part) {
+struct SideArgs {
+  const float* dy2[kSideGroup];
+  const void* gF[kSideGroup];
+  const void* xF;
+  float* acc;
+  int ow, M, d;
+  float* part;
+};
+template <typename S, int N>
+__global__ __launch_bounds__(256) void falplus_side_kernel(SideArgs a) {
+  const int d = a.d;
   const int j = 4 * (blockIdx.x * 256 + threadIdx.x);
   if (j >= d) return;
-  const int r0 = blockIdx.y * kSideRows, r1 = min(M, r0 + kSideRows);
-  const float4 g = ld4s<S>(gF + j);
-  float4 q = f4(0.f);
+  const int r0 = blockIdx.y * kSideRows, r1 = min(a.M, r0 + kSideRows);
+  const S* xF = static_cast<const S*>(a.xF);
+  float4 g[N], q[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    g[k] = ld4s<S>(static_cast<const S*>(a.gF[k]) + j);
+    q[k] = f4(0.f);
+  }
   for (int r = r0; r < r1; ++r) {
     const int64_t off = (int64_t)r * d + j;
-    const float4 v = ld4(dy2 + off);
-    q = q + v * ld4s<S>(xF + off);
-    const float4 w = g * v;
-    st4(acc + off, ow ? w : ld4(acc + off) + w);
+    float4 v[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) v[k] = ld4(a.dy2[k] + off);
+    const float4 x = ld4s<S>(xF + off);
+    float4 w = a.ow ? g[0] * v[0] : ld4(a.acc + off) + g[0] * v[0];
+#pragma unroll
+    for (int k = 1; k < N; ++k) w = w + g[k] * v[k];
+    st4(a.acc + off, w);
+#pragma unroll
+    for (int k = 0; k < N; ++k) q[k] = q[k] + v[k] * x;
   }
-  st4(part + (int64_t)blockIdx.y * d + j, q);
+  float* p = a.part + (int64_t)blockIdx.y * N * d + j;
+#pragma unroll
+  for (int k = 0; k < N; ++k) st4(p + (int64_t)k * d, q[k]);
 }
 
 bool falplus_side_ok(DType dt, int d, const float* dy2, const void* xhatF, const void* gF, const float* acc) {
   return vec_ok(dt, d, {dy2, acc}, {xhatF, gF}) && dy2 && xhatF && gF && acc;
 }
 
-int64_t falplus_side_scratch(int M, int d) { return (int64_t)cdiv(M, kSideRows) * d; }
+int64_t falplus_side_scratch(int M, int d) { return (int64_t)kSideGroup * cdiv(M, kSideRows) * d; }
 
-hipError_t falplus_side(DType dt, const float* dy2, const void* xhatF, const void* gF, float* dxhatF_acc,
-                        int overwrite, int M, int d, float* dgF, float* scratch, hipStream_t s) {
-  if (M < 1 || !falplus_side_ok(dt, d, dy2, xhatF, gF, dxhatF_acc) || !dgF || !scratch) return hipErrorInvalidValue;
+template <typename S, int N>
+static void side_launch(const SideArgs& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((falplus_side_kernel<S, N>), grid, dim3(256), 0, s, a);
+}
+static_assert(kSideGroup == 4, "side_dispatch instantiates groups of 1 to 4 blocks");
+template <typename S>
+static hipError_t side_dispatch(int n, const SideArgs& a, dim3 grid, hipStream_t s) {
+  switch (n) {
+    case 1: side_launch<S, 1>(a, grid, s); break;
+    case 2: side_launch<S, 2>(a, grid, s); break;
+    case 3: side_launch<S, 3>(a, grid, s); break;
+    case 4: side_launch<S, 4>(a, grid, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t falplus_side(DType dt, const FalPlusSide& g, const void* xhatF, float* dxhatF_acc, int overwrite, int M,
+                        int d, float* scratch, hipStream_t s) {
+  if (M < 1 || g.n < 1 || g.n > kSideGroup || !scratch) return hipErrorInvalidValue;
+  SideArgs a{};
+  for (int k = 0; k < g.n; ++k) {
+    if (!falplus_side_ok(dt, d, g.dy2[k], xhatF, g.gF[k], dxhatF_acc) || !g.dgF[k]) return hipErrorInvalidValue;
+    a.dy2[k] = g.dy2[k];
+    a.gF[k] = g.gF[k];
+  }
+  a.xF = xhatF; a.acc = dxhatF_acc; a.ow = overwrite ? 1 : 0; a.M = M; a.d = d; a.part = scratch;
   const dim3 grid(cdiv(d / 4, 256), cdiv(M, kSideRows));
-  if (dt == BF16)
-    hipLaunchKernelGGL((falplus_side_kernel<bf16>), grid, dim3(256), 0, s, dy2, static_cast<const bf16*>(xhatF),
-                       static_cast<const bf16*>(gF), dxhatF_acc, overwrite, M, d, scratch);
-  else
-    hipLaunchKernelGGL((falplus_side_kernel<float>), grid, dim3(256), 0, s, dy2, static_cast<const float*>(xhatF),
-                       static_cast<const float*>(gF), dxhatF_acc, overwrite, M, d, scratch);
-  hipError_t e = hipGetLastError();
+  hipError_t e = dt == BF16 ? side_dispatch<bf16>(g.n, a, grid, s) : side_dispatch<float>(g.n, a, grid, s);
   if (e != hipSuccess) return e;
-  return col_reduce(scratch, cdiv(M, kSideRows), d, d, dgF, s);
+  // the block partial sums, in order, six outputs per launch
+  for (int k0 = 0; k0 < g.n; k0 += 6) {
+    ColReduceArgs r{};
+    r.part = scratch; r.nblk = cdiv(M, kSideRows); r.stride = (int64_t)g.n * d; r.d = d;
+    const int nk = std::min(6, g.n - k0);
+    for (int k = 0; k < nk; ++k) { r.out[k] = g.dgF[k0 + k]; r.src[k] = k0 + k; }
+    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), nk), dim3(256), 0, s, r);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int64_t ln_bwd_scratch(int M, int d) {
