@@ -152,9 +152,43 @@ __global__ __launch_bounds__(256) void ln_param_partials(LnBwdArgs a) {
   const int d = a.d;
   const S* xF = static_cast<const S*>(a.xhatF);
   float q[6][4] = {};
-  if (j < d) {
-    const int r0 = rb * kPartRows + rg * (kPartRows / 4);
-    const int r1 = min(a.M, r0 + kPartRows / 4);
+  constexpr int RG = kPartRows / 4;  // rows per thread
+  const int r0 = rb * kPartRows + rg * RG;
+  const int r1 = min(a.M, r0 + RG);
+  if (j < d && r1 - r0 == RG && !xF) {
+    // a whole row group: every input row requested before the first use
+    float4 xv[RG], g1[RG], g2[RG];
+    float mu[RG], rs[RG];
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+      xv[r] = *reinterpret_cast<const float4*>(a.x + (int64_t)(r0 + r) * d + j);
+      mu[r] = a.mean[r0 + r];
+      rs[r] = a.rstd[r0 + r];
+    }
+    if (a.dy1) {
+#pragma unroll
+      for (int r = 0; r < RG; ++r) g1[r] = *reinterpret_cast<const float4*>(a.dy1 + (int64_t)(r0 + r) * d + j);
+    }
+    if (a.dy2) {
+#pragma unroll
+      for (int r = 0; r < RG; ++r) g2[r] = *reinterpret_cast<const float4*>(a.dy2 + (int64_t)(r0 + r) * d + j);
+    }
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+      const float xh[4] = {(xv[r].x - mu[r]) * rs[r], (xv[r].y - mu[r]) * rs[r], (xv[r].z - mu[r]) * rs[r],
+                           (xv[r].w - mu[r]) * rs[r]};
+      if (a.dy1) {
+        const float gv[4] = {g1[r].x, g1[r].y, g1[r].z, g1[r].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { q[0][c] += gv[c] * xh[c]; q[1][c] += gv[c]; }
+      }
+      if (a.dy2) {
+        const float gv[4] = {g2[r].x, g2[r].y, g2[r].z, g2[r].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { q[2][c] += gv[c] * xh[c]; q[3][c] += gv[c]; }
+      }
+    }
+  } else if (j < d) {
     // unrolled so that several rows' loads are in flight at once
 #pragma unroll 4
     for (int r = r0; r < r1; ++r) {
@@ -867,8 +901,31 @@ __global__ __launch_bounds__(256) void col_sum_batch_partials(ColSumPacked b) {
   const int j = blockIdx.x * 256 + cl * 4;
   if (blockIdx.x * 256 >= in.N) return;  // uniform: this input is narrower
   float s[4] = {0.f, 0.f, 0.f, 0.f};
-  if (j < in.N) {
-    const int r0 = blockIdx.y * kColRows + rg * (kColRows / 4), r1 = min(b.M, r0 + kColRows / 4);
+  constexpr int RG = kColRows / 4;  // rows per thread
+  const int r0 = blockIdx.y * kColRows + rg * RG, r1 = min(b.M, r0 + RG);
+  if (j < in.N && r1 - r0 == RG) {
+    // a whole row group: every row's load in flight before the first add
+    if (in.f32) {
+      const float* x = static_cast<const float*>(in.x) + (int64_t)r0 * in.ld + j;
+      float4 v[RG];
+#pragma unroll
+      for (int r = 0; r < RG; ++r) v[r] = *reinterpret_cast<const float4*>(x + (int64_t)r * in.ld);
+#pragma unroll
+      for (int r = 0; r < RG; ++r) {
+        s[0] += v[r].x; s[1] += v[r].y; s[2] += v[r].z; s[3] += v[r].w;
+      }
+    } else {
+      const S* x = static_cast<const S*>(in.x) + (int64_t)r0 * in.ld + j;
+      Raw4<S> v[RG];
+#pragma unroll
+      for (int r = 0; r < RG; ++r) v[r] = raw4<S>(x + (int64_t)r * in.ld);
+#pragma unroll
+      for (int r = 0; r < RG; ++r) {
+        const float4 w = val4(v[r]);
+        s[0] += w.x; s[1] += w.y; s[2] += w.z; s[3] += w.w;
+      }
+    }
+  } else if (j < in.N) {
     // 4-column vector loads, several rows in flight
     if (in.f32) {
       const float* x = static_cast<const float*>(in.x);
