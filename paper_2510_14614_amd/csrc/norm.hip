@@ -444,29 +444,72 @@ __global__ __launch_bounds__(256) void ln_bwd_v4(LnBwdArgs a) {
   const S* g1 = static_cast<const S*>(a.g1);
   const S* g2 = static_cast<const S*>(a.g2);
   const S* gF = static_cast<const S*>(a.gF);
-  float4 xh[NC], dxh[NC];
-  float s1 = 0.f, s2 = 0.f;
+  // The inputs of G chunks at a time (all of the row's up to 4 chunks per
+  // lane) are requested before any is used, so a group waits for one
+  // memory round trip; a lane past the row's end reads the row's first
+  // chunk instead and discards it (no load sits behind a branch).  Past 4
+  // chunks per lane the residual gradient is read after the reductions,
+  // where holding it would cost occupancy.
+  constexpr int G = NC <= 4 ? NC : 4;
+  constexpr bool PRE = NC <= 4;
+  static_assert(NC % G == 0, "whole groups");
+  float4 xh[NC], dxh[NC], res[PRE ? NC : 1];
+  int jc[NC];
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
     const int j = 4 * (lane + FAL_WAVE * i);
-    xh[i] = f4(0.f);
-    dxh[i] = f4(0.f);
-    if (j < d) {
-      xh[i] = (ld4(a.x + off + j) - f4(mean)) * f4(rstd);
-      float4 t = f4(0.f);
-      if (a.dy1) t = t + ld4(a.dy1 + off + j) * ld4s<S>(g1 + j);
-      if (a.dy2) {
-        const float4 dy2 = ld4(a.dy2 + off + j);
-        t = t + dy2 * ld4s<S>(g2 + j);
-        if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? dy2 : ld4(a.dacc + off + j) + dy2);
-        if (a.dxhatF_acc) {
-          const float4 c = ld4s<S>(gF + j) * dy2;
-          st4(a.dxhatF_acc + off + j, a.dxhatF_overwrite ? c : ld4(a.dxhatF_acc + off + j) + c);
-        }
+    jc[i] = j < d ? j : 0;
+  }
+  if (PRE && a.dres) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) res[PRE ? i : 0] = ld4(a.dres + off + jc[i]);
+  }
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i0 = 0; i0 < NC; i0 += G) {
+    float4 v1[G], v2[G], vacc[G];
+    Raw4<S> gv1[G], gv2[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) xh[i0 + k] = ld4(a.x + off + jc[i0 + k]);
+    if (a.dy1) {
+#pragma unroll
+      for (int k = 0; k < G; ++k) {
+        v1[k] = ld4(a.dy1 + off + jc[i0 + k]);
+        gv1[k] = raw4<S>(g1 + jc[i0 + k]);
       }
-      dxh[i] = t;
-      s1 += hsum(t);
-      s2 += hsum(t * xh[i]);
+    }
+    if (a.dy2) {
+#pragma unroll
+      for (int k = 0; k < G; ++k) {
+        v2[k] = ld4(a.dy2 + off + jc[i0 + k]);
+        gv2[k] = raw4<S>(g2 + jc[i0 + k]);
+      }
+    }
+    if (a.dacc && !a.dacc_overwrite) {
+#pragma unroll
+      for (int k = 0; k < G; ++k) vacc[k] = ld4(a.dacc + off + jc[i0 + k]);
+    }
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      const int i = i0 + k;
+      const int j = 4 * (lane + FAL_WAVE * i);
+      xh[i] = (xh[i] - f4(mean)) * f4(rstd);
+      dxh[i] = f4(0.f);
+      if (j < d) {
+        float4 t = f4(0.f);
+        if (a.dy1) t = t + v1[k] * val4(gv1[k]);
+        if (a.dy2) {
+          t = t + v2[k] * val4(gv2[k]);
+          if (a.dacc) st4(a.dacc + off + j, a.dacc_overwrite ? v2[k] : vacc[k] + v2[k]);
+          if (a.dxhatF_acc) {
+            const float4 c = ld4s<S>(gF + j) * v2[k];
+            st4(a.dxhatF_acc + off + j, a.dxhatF_overwrite ? c : ld4(a.dxhatF_acc + off + j) + c);
+          }
+        }
+        dxh[i] = t;
+        s1 += hsum(t);
+        s2 += hsum(t * xh[i]);
+      }
     }
   }
   s1 = wave_sum(s1) / d;
@@ -477,7 +520,7 @@ __global__ __launch_bounds__(256) void ln_bwd_v4(LnBwdArgs a) {
     const int j = 4 * (lane + FAL_WAVE * i);
     if (j >= d) break;
     float4 dx = f4(rstd) * (dxh[i] - f4(s1) - xh[i] * f4(s2));
-    if (a.dres) dx = dx + ld4(a.dres + off + j);
+    if (a.dres) dx = dx + (PRE ? res[PRE ? i : 0] : ld4(a.dres + off + j));
     st4(a.dx + off + j, dx);
     if (lp) st4s<S>(lp + off + j, dx);
   }
@@ -492,16 +535,29 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
   if (row >= M) return;
   const int64_t off = (int64_t)row * d;
   const float mu = mean[row], rs = rstd[row];
-  float4 xh[NC], g[NC];
+  // every input of the row requested before any is used (a lane past the
+  // row's end reads the row's first chunk and discards it); past 4 chunks
+  // per lane the residual gradient is read after the reductions
+  constexpr bool PRE = NC <= 4;
+  float4 xh[NC], g[NC], res[PRE ? NC : 1];
+  int jc[NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int j = 4 * (lane + FAL_WAVE * i);
+    jc[i] = j < d ? j : 0;
+    xh[i] = ld4(A + off + jc[i]);
+    g[i] = ld4(dxhat + off + jc[i]);
+  }
+  if (PRE && dres) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) res[PRE ? i : 0] = ld4(dres + off + jc[i]);
+  }
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
     const int j = 4 * (lane + FAL_WAVE * i);
-    xh[i] = f4(0.f);
-    g[i] = f4(0.f);
     if (j < d) {
-      xh[i] = (ld4(A + off + j) - f4(mu)) * f4(rs);
-      g[i] = ld4(dxhat + off + j);
+      xh[i] = (xh[i] - f4(mu)) * f4(rs);
       s1 += hsum(g[i]);
       s2 += hsum(g[i] * xh[i]);
     }
@@ -513,7 +569,7 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
     const int j = 4 * (lane + FAL_WAVE * i);
     if (j >= d) break;
     float4 v = f4(rs) * (g[i] - f4(s1) - xh[i] * f4(s2));
-    if (dres) v = v + ld4(dres + off + j);
+    if (dres) v = v + (PRE ? res[PRE ? i : 0] : ld4(dres + off + j));
     st4(da + off + j, v);
     if (lp) st4s<S>(lp + off + j, v);
   }
