@@ -235,8 +235,21 @@ __global__ __launch_bounds__(256) void ln_param_partials(LnBwdArgs a) {
 }
 
 // out_k[j] = sum_b part[b * stride + src_k * d + j] for up to 6 outputs, in
-// block order: 4 threads per column each sum every 4th partial, then the four
-// sums are added in a fixed order.
+// a fixed order: kRedWaves threads per column (one per wavefront) each sum
+// every kRedWaves-th partial in block order, then those sums are added
+// pairwise in a fixed tree.  Sixteen wavefronts per workgroup keep enough
+// loads in flight over the few workgroups a d-wide reduce has.
+constexpr int kRedWaves = 16;
+__device__ __forceinline__ float tree_sum(const float (&red)[kRedWaves][64], int c) {
+  float t[kRedWaves];
+#pragma unroll
+  for (int w = 0; w < kRedWaves; ++w) t[w] = red[w][c];
+#pragma unroll
+  for (int h = kRedWaves / 2; h >= 1; h /= 2)
+#pragma unroll
+    for (int w = 0; w < h; ++w) t[w] = t[2 * w] + t[2 * w + 1];
+  return t[0];
+}
 struct ColReduceArgs {
   const float* part;
   int nblk;
@@ -246,8 +259,8 @@ struct ColReduceArgs {
   int src[6];
 };
 
-__global__ __launch_bounds__(256) void col_reduce_multi(ColReduceArgs a) {
-  __shared__ float red[4][64];
+__global__ __launch_bounds__(64 * kRedWaves) void col_reduce_multi(ColReduceArgs a) {
+  __shared__ float red[kRedWaves][64];
   const int col = blockIdx.x * 64 + (threadIdx.x & 63);
   const int part = threadIdx.x >> 6;
   const int k = blockIdx.y;
@@ -257,21 +270,18 @@ __global__ __launch_bounds__(256) void col_reduce_multi(ColReduceArgs a) {
   if (col < a.d) {
     const float* p = a.part + (int64_t)a.src[k] * a.d + col;
 #pragma unroll 8
-    for (int b = part; b < a.nblk; b += 4) s += p[(int64_t)b * a.stride];
+    for (int b = part; b < a.nblk; b += kRedWaves) s += p[(int64_t)b * a.stride];
   }
   red[part][threadIdx.x & 63] = s;
   __syncthreads();
-  if (part == 0 && col < a.d) {
-    const int c = threadIdx.x & 63;
-    out[col] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
-  }
+  if (part == 0 && col < a.d) out[col] = tree_sum(red, threadIdx.x & 63);
 }
 
 hipError_t col_reduce(const float* part, int nblk, int64_t stride, int d, float* out, hipStream_t s) {
   ColReduceArgs a{};
   a.part = part; a.nblk = nblk; a.stride = stride; a.d = d;
   a.out[0] = out; a.src[0] = 0;
-  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), 1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), 1), dim3(64 * kRedWaves), 0, s, a);
   return hipGetLastError();
 }
 
@@ -744,7 +754,7 @@ static int fused_rows(int M, int d) {
 // block of kSideRows rows, reads the row's xhatF and accumulator once and
 // every block's dy2, updates the accumulator in place (block order) and
 // writes its column partials of dy2[k] * xhatF as [blk][N][d];
-// col_reduce_multi sums the blocks in order.  No barriers.
+// col_reduce_multi sums the blocks in a fixed order.  No barriers.
 constexpr int kSideRows = 32;
 struct SideArgs {
   const float* dy2[kSideGroup];
@@ -827,7 +837,7 @@ hipError_t falplus_side(DType dt, const FalPlusSide& g, const void* xhatF, float
     r.part = scratch; r.nblk = cdiv(M, kSideRows); r.stride = (int64_t)g.n * d; r.d = d;
     const int nk = std::min(6, g.n - k0);
     for (int k = 0; k < nk; ++k) { r.out[k] = g.dgF[k0 + k]; r.src[k] = k0 + k; }
-    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), nk), dim3(256), 0, s, r);
+    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(d, 64), nk), dim3(64 * kRedWaves), 0, s, r);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -864,7 +874,7 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
     float* outs[6] = {a.dg1, a.db1, a.dg2, a.db2, a.dgF, a.dbF};
     const int src[6] = {0, 1, 2, 3, 3, 3};  // dbF == db2 == sum dy2 (dgF is NULL here)
     for (int k = 0; k < 6; ++k) { r.out[k] = outs[k]; r.src[k] = src[k]; }
-    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(256), 0, s, r);
+    hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(64 * kRedWaves), 0, s, r);
     return hipGetLastError();
   }
   if (vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc}, {a.g1, a.g2, a.gF, a.dx_lp}))
@@ -894,7 +904,7 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   float* outs[6] = {a.dg1, a.db1, a.dg2, a.db2, a.dgF, a.dbF};
   const int src[6] = {0, 1, 2, 3, 4, 3};  // dbF == db2 == sum dy2
   for (int k = 0; k < 6; ++k) { r.out[k] = outs[k]; r.src[k] = src[k]; }
-  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(256), 0, s, r);
+  hipLaunchKernelGGL(col_reduce_multi, dim3(cdiv(a.d, 64), 6), dim3(64 * kRedWaves), 0, s, r);
   return hipGetLastError();
 }
 
@@ -1012,21 +1022,20 @@ __global__ __launch_bounds__(256) void col_sum_batch_partials(ColSumPacked b) {
   }
 }
 
-__global__ __launch_bounds__(256) void col_reduce_batch(ColSumPacked b, int nblk) {
-  __shared__ float red[4][64];
+__global__ __launch_bounds__(64 * kRedWaves) void col_reduce_batch(ColSumPacked b, int nblk) {
+  __shared__ float red[kRedWaves][64];
   const int W = b.n == 1 ? b.off[1] : b.n == 2 ? b.off[2] : b.n == 3 ? b.off[3] : b.off[4];
   const int col = blockIdx.x * 64 + (threadIdx.x & 63);
   const int q = threadIdx.x >> 6;
   float s = 0.f;
   if (col < W) {
 #pragma unroll 8
-    for (int blk = q; blk < nblk; blk += 4) s += b.part[(int64_t)blk * W + col];
+    for (int blk = q; blk < nblk; blk += kRedWaves) s += b.part[(int64_t)blk * W + col];
   }
   red[q][threadIdx.x & 63] = s;
   __syncthreads();
   if (q == 0 && col < W) {
-    const int c = threadIdx.x & 63;
-    const float v = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+    const float v = tree_sum(red, threadIdx.x & 63);
 #pragma unroll
     for (int k = 0; k < kColSumMax; ++k) {
       if (k < b.n && col >= b.off[k] && col < b.off[k + 1]) {
@@ -1067,7 +1076,7 @@ hipError_t col_sum_batch(DType dt, const ColSumBatch& b, float* scratch, hipStre
     hipLaunchKernelGGL((col_sum_batch_partials<bf16>), grid, block, 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(col_reduce_batch, dim3(cdiv(w, 64)), dim3(256), 0, s, p, nblk);
+  hipLaunchKernelGGL(col_reduce_batch, dim3(cdiv(w, 64)), dim3(64 * kRedWaves), 0, s, p, nblk);
   return hipGetLastError();
 }
 
