@@ -6,9 +6,9 @@
 //    adds the per-block LayerNorm of the shared first-attention
 //    normalisation to its MLP input in the same pass.
 //  * ln_bwd: the input gradient (both LayerNorms of one input at once) and
-//    the gamma/beta gradients: for widths that are a multiple of 1024 one
-//    pass forms both (partial sums per workgroup of rows); other widths use
-//    a row kernel plus a column partial-sum kernel.  Either way a
+//    the gamma/beta gradients: for widths that are a multiple of 256 (up to
+//    4096) one pass forms both (partial sums per workgroup of rows); other
+//    widths use a row kernel plus a column partial-sum kernel.  Either way a
 //    fixed-order reduce finishes the parameter gradients.
 //  * norm_bwd: backward of the affine-free normalisation of A_1 (FAL+).
 //  * col_sum_batch: bias gradients, up to four matrices per pair of launches.
@@ -585,7 +585,7 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
   }
 }
 
-// LayerNorm backward in one pass for widths that are a multiple of 1024 (up
+// LayerNorm backward in one pass for widths that are a multiple of 256 (up
 // to 4096): a workgroup walks `rows` consecutive rows with all 256 threads
 // on one row (NCH 4-element chunks each), combines the four wavefronts' row
 // sums through LDS in a fixed order (one barrier per row, double-buffered),
@@ -596,18 +596,29 @@ __global__ __launch_bounds__(256) void norm_bwd_v4(const float* A, const float* 
 // every input of a row is requested before any of it is used, so a row
 // waits for one memory round trip.  (The FAL+ first-attention terms go to
 // the two-kernel path.)
-template <typename S, int NCH>
+template <typename S, int NCH, bool TAIL>
 __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
   __shared__ float red[2][4][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = a.d;
   S* lp = static_cast<S*>(a.dx_lp);
-  Raw4<S> gv1[NCH], gv2[NCH];
+  // chunk c of this thread holds columns j = 4 (tid + 256 c).  TAIL: d is
+  // not a multiple of 1024, so the last chunk of some wavefronts (whole
+  // ones, d being a multiple of 256) lies past the row's end; they read the
+  // row's first chunk instead and store nothing.
+  bool inc[NCH];
+  int jc[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int j = 4 * (tid + 256 * c);
-    if (a.dy1) gv1[c] = raw4<S>(static_cast<const S*>(a.g1) + j);
-    if (a.dy2) gv2[c] = raw4<S>(static_cast<const S*>(a.g2) + j);
+    inc[c] = !TAIL || c < NCH - 1 || j < d;
+    jc[c] = inc[c] ? j : 0;
+  }
+  Raw4<S> gv1[NCH], gv2[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (a.dy1) gv1[c] = raw4<S>(static_cast<const S*>(a.g1) + jc[c]);
+    if (a.dy2) gv2[c] = raw4<S>(static_cast<const S*>(a.g2) + jc[c]);
   }
   float4 q[4][NCH];
 #pragma unroll
@@ -620,28 +631,30 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
     const float mean = a.mean[r], rstd = a.rstd[r];
     float4 xh[NCH], t[NCH], res[NCH], v1[NCH], v2[NCH], vacc[NCH];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) xh[c] = ld4(a.x + off + 4 * (tid + 256 * c));
+    for (int c = 0; c < NCH; ++c) xh[c] = ld4(a.x + off + jc[c]);
     if (a.dy1) {
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) v1[c] = ld4(a.dy1 + off + 4 * (tid + 256 * c));
+      for (int c = 0; c < NCH; ++c) v1[c] = ld4(a.dy1 + off + jc[c]);
     }
     if (a.dy2) {
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) v2[c] = ld4(a.dy2 + off + 4 * (tid + 256 * c));
+      for (int c = 0; c < NCH; ++c) v2[c] = ld4(a.dy2 + off + jc[c]);
     }
     if (a.dres) {
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) res[c] = ld4(a.dres + off + 4 * (tid + 256 * c));
+      for (int c = 0; c < NCH; ++c) res[c] = ld4(a.dres + off + jc[c]);
     }
     if (a.dacc && !a.dacc_overwrite) {
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) vacc[c] = ld4(a.dacc + off + 4 * (tid + 256 * c));
+      for (int c = 0; c < NCH; ++c) vacc[c] = ld4(a.dacc + off + jc[c]);
     }
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int j = 4 * (tid + 256 * c);
       xh[c] = (xh[c] - f4(mean)) * f4(rstd);
+      t[c] = f4(0.f);
+      if (!inc[c]) continue;
       float4 tt = f4(0.f);
       if (a.dy1) {
         const float4 v = v1[c];
@@ -673,6 +686,7 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int j = 4 * (tid + 256 * c);
+      if (!inc[c]) continue;
       float4 dx = f4(rstd) * (t[c] - f4(s1) - xh[c] * f4(s2));
       if (a.dres) dx = dx + res[c];
       st4(a.dx + off + j, dx);
@@ -683,7 +697,8 @@ __global__ __launch_bounds__(256) void ln_bwd_fused(LnBwdArgs a, int rows) {
 #pragma unroll
   for (int k = 0; k < 4; ++k)
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) st4(p + (int64_t)k * d + 4 * (tid + 256 * c), q[k][c]);
+    for (int c = 0; c < NCH; ++c)
+      if (inc[c]) st4(p + (int64_t)k * d + 4 * (tid + 256 * c), q[k][c]);
 }
 
 // Chunks of 4 per lane for width d (a multiple of 4), 0 if too wide.
@@ -746,7 +761,7 @@ hipError_t ln_fwd(DType dt, const LnFwdArgs& a, hipStream_t s) {
 // (M, d) = (8192, 2048), (4096, 4096) and (16384, 1024).
 static int fused_rows(int M, int d) {
   static const int per_cu[4] = {4, 4, 2, 2};
-  const int nch = std::min(4, std::max(1, d / 1024));
+  const int nch = std::min(4, std::max(1, cdiv(d, 1024)));
   return std::max(1, cdiv(M, 256 * per_cu[nch - 1]));
 }
 
@@ -852,17 +867,23 @@ hipError_t ln_bwd(DType dt, const LnBwdArgs& a, hipStream_t s) {
   const dim3 grid(cdiv(a.M, kRowsPerBlock)), block(256);
   hipError_t e;
   const bool any = a.dg1 || a.db1 || a.dg2 || a.db2 || a.dgF || a.dbF;
-  if (any && a.d % 1024 == 0 && a.d <= 4096 && a.partials && !a.xhatF && !a.dxhatF_acc && !a.dgF &&
+  if (any && a.d % 256 == 0 && a.d <= 4096 && a.partials && !a.xhatF && !a.dxhatF_acc && !a.dgF &&
       vec_ok(dt, a.d, {a.x, a.dy1, a.dy2, a.dres, a.dx, a.dacc, a.dxhatF_acc, a.partials},
              {a.g1, a.g2, a.gF, a.dx_lp, a.xhatF})) {
     const int rows = fused_rows(a.M, a.d);
     const int nblk = cdiv(a.M, rows);
+    const bool tail = a.d % 1024 != 0;
     auto launch = [&](auto nc) {
       constexpr int C = decltype(nc)::value;
-      if (dt == BF16) hipLaunchKernelGGL((ln_bwd_fused<bf16, C>), dim3(nblk), block, 0, s, a, rows);
-      else hipLaunchKernelGGL((ln_bwd_fused<float, C>), dim3(nblk), block, 0, s, a, rows);
+      if (dt == BF16) {
+        if (tail) hipLaunchKernelGGL((ln_bwd_fused<bf16, C, true>), dim3(nblk), block, 0, s, a, rows);
+        else hipLaunchKernelGGL((ln_bwd_fused<bf16, C, false>), dim3(nblk), block, 0, s, a, rows);
+      } else {
+        if (tail) hipLaunchKernelGGL((ln_bwd_fused<float, C, true>), dim3(nblk), block, 0, s, a, rows);
+        else hipLaunchKernelGGL((ln_bwd_fused<float, C, false>), dim3(nblk), block, 0, s, a, rows);
+      }
     };
-    switch (a.d / 1024) {
+    switch (cdiv(a.d, 1024)) {
       case 1: launch(std::integral_constant<int, 1>{}); break;
       case 2: launch(std::integral_constant<int, 2>{}); break;
       case 3: launch(std::integral_constant<int, 3>{}); break;
