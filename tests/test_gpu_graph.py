@@ -25,7 +25,7 @@ def _cfg(arch, n_layer, large):
 
 
 @pytest.mark.parametrize("arch,n_layer,large", [(ARCH_FAL, 2, 0), (ARCH_FAL, 1, 0), (ARCH_FALPLUS, 2, 0),
-                                                (ARCH_FAL, 3, 1)])
+                                                (ARCH_FALPLUS, 9, 0), (ARCH_FAL, 3, 1)])
 def test_captured_step_replays_bitwise(arch, n_layer, large):
     import torch
     cfg = _cfg(arch, n_layer, large)
@@ -59,15 +59,18 @@ def test_captured_step_replays_bitwise(arch, n_layer, large):
     F.close()
 
 
-@pytest.mark.parametrize("arch", [ARCH_GPT, ARCH_FAL])
-def test_two_streams_bitwise_equal_one_stream_large(arch):
+@pytest.mark.parametrize("arch,n_layer,large", [(ARCH_GPT, 3, 1), (ARCH_FAL, 3, 1), (ARCH_FALPLUS, 9, 0)])
+def test_two_streams_bitwise_equal_one_stream(arch, n_layer, large):
     # blocks above the bias-sum threshold: with two streams the sums run on
     # the context's own stream beside the next block's backward (and FAL's
-    # branches on the aux stream); on one stream everything runs in order
-    # on the main stream.  Loss, logits and every gradient agree bitwise.
+    # branches on the aux stream); FAL+'s first-attention terms of layers
+    # 8..5 and 4..1 run there as two grouped passes, and layers 3..1 write
+    # the dH2 ring slots of layers 8..6 after the first group was joined.
+    # On one stream everything runs in order on the main stream.  Loss,
+    # logits and every gradient agree bitwise.
     import torch
-    cfg = _cfg(arch, 3, 1)
-    log(f"one vs two streams, large blocks, arch={arch}")
+    cfg = _cfg(arch, n_layer, large)
+    log(f"one vs two streams, arch={arch} L={n_layer} large={large}")
     g, blocks = synth.make_params(cfg, seed=72)
     tok = torch.from_numpy(synth.make_tokens(cfg, seed=73, dist="zipf")).cuda()
     outs = []

@@ -44,6 +44,19 @@ def test_tiny_fal_schedules(sched, dtype):
                  label=f"tiny sched{sched} dt{dtype}")
 
 
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_tiny_falplus_deep_stack(dtype):
+    # nine FAL+ blocks (Appendix D.1): the first-attention terms of layers
+    # 8..5 and 4..1 are accumulated by two grouped side passes, and layers
+    # 3..1 reuse the dH2 ring slots of layers 8..6
+    cfg = get_config("tiny", arch=ARCH_FALPLUS, dtype=dtype, sched=SCHED_STREAMS_MERGED, n_layer=9)
+    log(f"tiny FAL+ L=9 dtype={dtype}")
+    g, blocks = synth.make_params(cfg, seed=20)
+    tok = synth.make_tokens(cfg, seed=21)
+    compare_step(cfg, gpu_model_step(cfg, g, blocks, tok), _ref(cfg, g, blocks, tok),
+                 label=f"tiny FAL+ L9 dt{dtype}")
+
+
 @pytest.mark.parametrize("sched", SCHEDS)
 @pytest.mark.parametrize("dtype", [0, 1])
 def test_tiny_parallel_schedules(sched, dtype):
