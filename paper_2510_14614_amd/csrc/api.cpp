@@ -670,7 +670,10 @@ struct Run {
     fp_ready = false;
   }
   void queue_fp(const float* dy2, const void* xF, const void* gF, float* acc, int ow, float* dgF, bool close) {
-    if (fp.g.n > 0 && (xF != fp.xF || acc != fp.acc || ow)) run_fp(ctx->sm);  // not one group
+    if (fp.g.n > 0 && (xF != fp.xF || acc != fp.acc || ow)) {  // not one group
+      bias_join();  // an earlier group may still be adding to an accumulator
+      run_fp(ctx->sm);
+    }
     if (fp.g.n == 0) { fp.xF = xF; fp.acc = acc; fp.ow = ow; }
     fp.g.dy2[fp.g.n] = dy2; fp.g.gF[fp.g.n] = gF; fp.g.dgF[fp.g.n] = dgF;
     ++fp.g.n;
@@ -678,8 +681,8 @@ struct Run {
   }
   // the end of an entry point: a group still open runs on the main stream
   void finish() {
-    if (fp.g.n > 0) run_fp(ctx->sm);
     bias_join();
+    if (fp.g.n > 0) run_fp(ctx->sm);
   }
   void flush_bias_async() {
     const bool two = ctx->sa != ctx->sm;  // one-stream contexts stay on one stream
@@ -838,7 +841,10 @@ struct Run {
       if (W.fp_part && falplus_side_ok(dt, D.d, W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst)) {
         queue_fp(W.dh2, first, P(bp, FAL_B_LNF1_G), dfirst, last ? 1 : 0, G(gb, FAL_B_LNF1_G), layer == 1);
       } else {
-        if (fp.g.n > 0) run_fp(sm);  // keep the accumulator's order of terms
+        if (fp.g.n > 0) {  // keep the accumulator's order of terms
+          bias_join();
+          run_fp(sm);
+        }
         a2.xhatF = first; a2.gF = P(bp, FAL_B_LNF1_G);
         a2.dxhatF_acc = dfirst; a2.dxhatF_overwrite = last;
         a2.dgF = G(gb, FAL_B_LNF1_G);
