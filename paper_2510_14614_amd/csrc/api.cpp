@@ -686,11 +686,10 @@ struct Run {
   }
   void flush_bias_async() {
     const bool two = ctx->sa != ctx->sm;  // one-stream contexts stay on one stream
-    const bool fp_queued = fp_ready;
     const bool bias_side = bias.n > 0 && two && bias_bytes() >= 128.0 * (1 << 20);
-    const bool fp_side = fp_queued && two;
+    const bool fp_side = fp_ready && two;
     if (bias.n > 0 && !bias_side) flush_bias(ctx->sm);
-    if (fp_queued && !fp_side) run_fp(ctx->sm);
+    if (fp_ready && !fp_side) run_fp(ctx->sm);
     if (!bias_side && !fp_side) return;
     FAL_TRY(hipEventRecord(ctx->ev_bfork, ctx->sm));
     FAL_TRY(hipStreamWaitEvent(ctx->sb, ctx->ev_bfork, 0));

@@ -138,9 +138,11 @@ __global__ __launch_bounds__(256) void ln_bwd_rows(LnBwdArgs a) {
 // 256 columns x kPartRows rows: 64 threads across the columns (4 consecutive
 // columns each, 16-byte loads) times 4 row groups that each walk
 // kPartRows/4 rows in order; the 4 group sums are then added in a fixed
-// order through LDS.  partials: [nblk][6][d].
-// 32 rows gives 768 workgroups at M = 8192, d = 768, enough loads in flight
-// to beat 64 rows (LayerNorm kernels of a GPT-2-small step 1.10 -> 1.02 ms).
+// order through LDS.  partials: [nblk][6][d].  Used for widths that are
+// not a multiple of 256 and for the FAL+ terms when the side pass cannot
+// take them.  32 rows gave 768 workgroups at M = 8192, d = 768, enough
+// loads in flight to beat 64 rows (measured while that width still used
+// this pass: LayerNorm kernels of a GPT-2-small step 1.10 -> 1.02 ms).
 constexpr int kPartRows = 32;
 
 template <typename S>
