@@ -670,7 +670,8 @@ struct Run {
     fp_ready = false;
   }
   void queue_fp(const float* dy2, const void* xF, const void* gF, float* acc, int ow, float* dgF, bool close) {
-    if (fp.g.n > 0 && (xF != fp.xF || acc != fp.acc || ow)) {  // not one group
+    if (fp.g.n == kSideGroup || (fp.g.n > 0 && (xF != fp.xF || acc != fp.acc || ow))) {
+      // a full group not yet flushed, or not one group
       bias_join();  // an earlier group may still be adding to an accumulator
       run_fp(ctx->sm);
     }
