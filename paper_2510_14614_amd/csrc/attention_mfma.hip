@@ -382,6 +382,11 @@ __global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
         s[r] = p;
         dp[r] = p * (dp[r] - sD[qr]);
       }
+      // head_dim 128 (one wavefront per SIMD): the dV and dK MFMAs in a
+      // region of their own, each issued with the transposing LDS reads of
+      // the next few in flight, so a fragment read does not wait right
+      // before its MFMA
+      if (HD == 128) __builtin_amdgcn_sched_barrier(0);
       {
         const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
 #pragma unroll
@@ -397,6 +402,17 @@ __global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
           dk[t] = mfma32(d0, frag_tr<HD>(sQ, 32 * sub, 32 * t, lane), dk[t]);
           dk[t] = mfma32(d1, frag_tr<HD>(sQ, 32 * sub + 16, 32 * t, lane), dk[t]);
         }
+      }
+      if (HD == 128) {
+        constexpr int LA = 4;  // MFMAs whose LDS reads are in flight ahead
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * LA, 0);  // LDS reads of the first LA MFMAs
+#pragma unroll
+        for (int q = 0; q < 4 * NT - LA; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads of the MFMA LA ahead
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, LA, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
