@@ -285,6 +285,23 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16* qkv, int T, 
   }
 }
 
+// Scheduling groups for a run of N MFMAs that take R LDS read instructions
+// each: the reads of the next LA MFMAs stay in flight, so a fragment read
+// is not waited for right before its MFMA (head_dim 128, where one
+// wavefront per SIMD leaves nothing else to cover that wait).  Ends the
+// scheduling region.
+template <int N, int R, int LA>
+__device__ __forceinline__ void lds_ahead() {
+  __builtin_amdgcn_sched_group_barrier(0x100, R * LA, 0);  // LDS reads of the first LA MFMAs
+#pragma unroll
+  for (int q = 0; q < N - LA; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);  // LDS reads of the MFMA LA ahead
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, LA, 0);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // ------------------------------------------------------- backward: dK dV --
 // dK and dV of a key block in one pass.  head_dim 64: two wavefronts per
 // SIMD; head_dim 128: the accumulators take most of the register file, one
@@ -370,6 +387,7 @@ __global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
         s = mfma32(frag_rows<HD>(sQ, 32 * sub, c, kk, g), kf[kk], s);
         dp = mfma32(frag_rows<HD>(sdO, 32 * sub, c, kk, g), vf[kk], dp);
       }
+      if (HD == 128) lds_ahead<2 * KK, 1, 4>();
       // s[r] = S[query qs + acc_row(r, g)][key].  Queries past T have zero
       // Q and dO rows and zero L and D, so they add nothing; only the
       // diagonal sub-tile (qs == kw) has queries before this wave's keys.
@@ -382,10 +400,8 @@ __global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
         s[r] = p;
         dp[r] = p * (dp[r] - sD[qr]);
       }
-      // head_dim 128 (one wavefront per SIMD): the dV and dK MFMAs in a
-      // region of their own, each issued with the transposing LDS reads of
-      // the next few in flight, so a fragment read does not wait right
-      // before its MFMA
+      // head_dim 128: the dV and dK MFMAs in a scheduling region of their
+      // own, with the transposing reads of the next four in flight
       if (HD == 128) __builtin_amdgcn_sched_barrier(0);
       {
         const bf16x8v p0 = pack8(s, 0), p1 = pack8(s, 8);
@@ -403,17 +419,7 @@ __global__ __launch_bounds__(256, HD == 128 ? 1 : 2) void attn_bwd_dkdv_mfma(
           dk[t] = mfma32(d1, frag_tr<HD>(sQ, 32 * sub + 16, 32 * t, lane), dk[t]);
         }
       }
-      if (HD == 128) {
-        constexpr int LA = 4;  // MFMAs whose LDS reads are in flight ahead
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * LA, 0);  // LDS reads of the first LA MFMAs
-#pragma unroll
-        for (int q = 0; q < 4 * NT - LA; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads of the MFMA LA ahead
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, LA, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      if (HD == 128) lds_ahead<4 * NT, 2, 4>();
     }
   }
   // dk[t][r] = dK[key kw + acc_row(r, g)][dim 32t + c]
@@ -498,6 +504,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
         s = mfma32(frag_rows<HD>(sK, 32 * sub, c, kk, g), qf[kk], s);
         dp = mfma32(frag_rows<HD>(sV, 32 * sub, c, kk, g), of[kk], dp);
       }
+      if (HD == 128) lds_ahead<2 * KK, 1, 4>();
       // s[r] = S^T[key kb + acc_row(r, g)][query tq].  Keys past T have
       // zero K and V rows (dS there multiplies a zero K row); only the
       // diagonal sub-tile (kb == q0) has keys after a query.
@@ -508,12 +515,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16* qkv, cons
         if (diag && kb + acc_row(r, g) > tq) p = 0.f;
         dp[r] = p * (dp[r] - Dq);
       }
+      if (HD == 128) __builtin_amdgcn_sched_barrier(0);
       const bf16x8v d0 = pack8(dp, 0), d1 = pack8(dp, 8);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         dq[t] = mfma32(frag_tr<HD>(sK, 32 * sub, 32 * t, lane), d0, dq[t]);
         dq[t] = mfma32(frag_tr<HD>(sK, 32 * sub + 16, 32 * t, lane), d1, dq[t]);
       }
+      if (HD == 128) lds_ahead<2 * NT, 2, 4>();
     }
   }
   if (tq < T) {
