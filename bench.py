@@ -504,8 +504,8 @@ def main():
         summarize_hbm(*args.summarize_hbm, args.cmd)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
-              f"(the hot path is single-GPU; see the sharding notes in DESIGN.md).", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported: the training step "
+              f"runs on a single GPU (multi-GPU sharding is not implemented).", file=sys.stderr)
         sys.exit(2)
     import torch
 
