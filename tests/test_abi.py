@@ -108,6 +108,22 @@ def test_workspace_grows_with_layers():
     assert b > a
 
 
+@pytest.mark.parametrize("name", ["tiny", "gpt2-small", "gpt-1.3b"])
+def test_falplus_workspace_holds_the_side_pass_ring(name):
+    # FAL+ keeps the MLP-input gradient dH2 of up to four consecutive blocks
+    # for the grouped first-attention pass (a ring of five fp32 [M, d]
+    # buffers, four beyond the one every architecture has) plus that pass's
+    # partial sums (four blocks x one row per 32 rows x d fp32); otherwise
+    # its workspace is the GPT one
+    from paper_2510_14614_amd.config import ARCH_FALPLUS, ARCH_GPT
+    gpt = get_config(name, arch=ARCH_GPT)
+    fp = get_config(name, arch=ARCH_FALPLUS)
+    M, d = gpt.tokens, gpt.d_model
+    extra = 4 * M * d * 4 + 4 * ((M + 31) // 32) * d * 4
+    diff = fal.workspace_bytes(fp) - fal.workspace_bytes(gpt)
+    assert extra <= diff <= extra + 5 * 256, (diff, extra)
+
+
 def test_init_rejects_bad_arguments_without_gpu():
     lib = fal.lib()
     c = fal.to_c(get_config("tiny"))
